@@ -1,0 +1,236 @@
+"""Benchmark of the Forcing-KV hot path on one MI355X.
+
+One step = one AR step of one attention layer (a "unit"): segment scoring and
+BottomK selection + compaction for the dynamic heads, structural gather for
+the static heads, then chunk attention of all heads over their compressed
+caches -- the four C-ABI calls, on the 480P Wan-1.3B-style layer (12 heads,
+d = 128, 1560 tokens/frame, 21-frame history, 3-frame chunk, heads 0-5 static
+with sink + 6 recent frames, heads 6-11 dynamic with sink + 10 of 20 frames).
+
+Inputs are seeded synthetic tensors already resident in HBM.  The step
+rotates through several independent copies of the layer's buffers (as the
+layers of a real rollout would), so a step never finds its cache in the
+256 MB last-level cache from the previous step.
+
+Prints ONE JSON line (see the keys below).  `value` is the wall-clock ms per
+step over the timed steps (lower is better).  `roofline` covers the dominant
+kernel (chunk attention, MFMA-bound) timed with HIP events on the stream the
+kernels run on.  `cpu_baseline` times the CPU oracle on the host cores on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "ms per AR chunk (score+compact+attn) and attn TFLOP/s, 480P/1080P shapes"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--resolution", default="480p", choices=["480p", "1080p"])
+    p.add_argument("--copies", type=int, default=4, help="independent layer buffers rotated per step")
+    p.add_argument("--cpu-rows", type=int, default=1024, help="query rows per head in the CPU oracle sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "attention_traffic.json"),
+                   help="HBM bytes per attention launch measured with rocprofv3 counters")
+    return p.parse_args()
+
+
+def to_dev(a, dtype):
+    import numpy as np
+    import torch
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def cpu_baseline(cfg, x, rows_per_head):
+    """Time the CPU oracle on the host cores: full compression of every head
+    and attention for a seeded sample of query rows per head, scaled to one
+    unit (the attention time is multiplied by Lq / rows_per_head)."""
+    import numpy as np
+    import oracle
+    oracle.lib()
+    rng = np.random.default_rng(0)
+    rows = np.sort(rng.choice(cfg.lq, size=min(rows_per_head, cfg.lq), replace=False)).astype(np.int32)
+    t0 = time.perf_counter()
+    res = oracle.run_layer(cfg, x, attention=False)
+    t1 = time.perf_counter()
+    scale = 1.0 / math.sqrt(cfg.head_dim)
+    for h in range(cfg.n_heads):
+        oracle.attention_rows(x.Q[h], res.Kc[h], res.Vc[h], x.K_cur[h], x.V_cur[h], scale, rows)
+    t2 = time.perf_counter()
+    per_unit_s = (t1 - t0) + (t2 - t1) * cfg.lq / len(rows)
+    return {
+        "value": round(per_unit_s * 1e3, 1),
+        "unit": "ms",
+        "cores": oracle.max_threads(),
+        "kind": "oracle",
+        "sample": (f"fp64 C oracle: scoring+selection+compaction of all {cfg.n_heads} heads in full "
+                   f"({t1 - t0:.2f} s) + attention of {len(rows)} of {cfg.lq} query rows per head "
+                   f"({t2 - t1:.2f} s), attention scaled x{cfg.lq / len(rows):.1f} to one unit"),
+        "measured_s": round(t2 - t0, 2),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "the Forcing-KV hot path shards by head with no exchange, so N GPUs run N "
+              "independent copies of this step.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    import paper_2605_09681_amd as fkv
+    from paper_2605_09681_amd.layer import CompressedLayer
+
+    fkv.lib()  # fail loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    cfg = W.wan_layer_config(args.resolution)
+    x = W.make_layer_inputs(cfg, seed=0)
+
+    layers, bufs = [], []
+    base = {k: to_dev(getattr(x, k), cfg.dtype) for k in ("K_hist", "V_hist", "K_cur", "V_cur", "Q")}
+    for c in range(args.copies):
+        b = base if c == 0 else {k: v.clone() for k, v in base.items()}
+        b["O"] = torch.empty_like(b["Q"])
+        bufs.append(b)
+        layers.append(CompressedLayer(cfg.n_heads, cfg.head_dim, cfg.frame_tokens, cfg.hist_frames,
+                                      cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype,
+                                      cfg.heads))
+    slots = x.frame_slot
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        L, b = layers[i % len(layers)], bufs[i % len(layers)]
+        if ev is not None:
+            ev[0].record(stream)
+        L.score(b["K_hist"], slots, b["K_cur"])
+        if ev is not None:
+            ev[1].record(stream)
+        L.select_compact(b["K_hist"], b["V_hist"], slots)
+        if ev is not None:
+            ev[2].record(stream)
+        L.compress_static(b["K_hist"], b["V_hist"], slots)
+        if ev is not None:
+            ev[3].record(stream)
+        L.attention(b["Q"], b["K_cur"], b["V_cur"], b["O"])
+        if ev is not None:
+            ev[4].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, events[i])
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    stage = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(4)] for e in events])  # ms
+    score_ms, select_ms, static_ms, attn_ms = stage.mean(axis=0).tolist()
+
+    # algorithmic work per unit
+    kv_len = layers[0].kv_len.cpu().numpy().astype(np.int64)
+    d, e, F, H, Lq = cfg.head_dim, 2, cfg.frame_tokens, cfg.hist_frames, cfg.lq
+    n_dyn = sum(1 for b in cfg.heads if b.type == W.DYNAMIC)
+    dyn = np.array([b.type == W.DYNAMIC for b in cfg.heads])
+    attn_flop = float(4.0 * Lq * d * np.sum(kv_len + Lq))
+    score_bytes = n_dyn * (H + 1) * F * d * e
+    dyn_copy_bytes = 4 * d * e * int(kv_len[dyn].sum())
+    static_copy_bytes = 4 * d * e * int(kv_len[~dyn].sum())
+    attn_tflops = attn_flop / (attn_ms * 1e-3) / 1e12
+
+    traffic = None
+    if os.path.exists(args.traffic_json):
+        try:
+            with open(args.traffic_json) as f:
+                tj = json.load(f)
+            if tj.get("workload") == cfg.name and tj.get("kernel_source_sha") == _kernel_sha():
+                traffic = tj.get("bytes_per_launch")
+        except (OSError, ValueError):
+            traffic = None
+
+    out = {
+        "metric": METRIC,
+        "value": round(wall_ms, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic: seeded AR(1) keys (rho 0.9) across frames, N(0,1) queries/values",
+        "config": {
+            "workload": (f"{cfg.name}: one layer, one AR step; {cfg.n_heads} heads x d{d}, "
+                         f"{F} tokens/frame, {H}-frame history, {cfg.chunk_frames}-frame chunk "
+                         f"(Lq {Lq}); heads 0-5 static (sink 1 + recent 6), heads 6-11 dynamic "
+                         f"(sink 1 + 10 of 20 frame segments)"),
+            "kv_len": kv_len.tolist(),
+            "rotating_copies": args.copies,
+        },
+        "roofline": {
+            "kernel": "attn_bf16_kernel<128> (fkv_chunk_attention)",
+            "bound": "mfma",
+            "achieved": round(attn_tflops, 1),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "algorithmic_flop_per_launch": attn_flop,
+            "avg_launch_ms": round(attn_ms, 4),
+        },
+        "breakdown_ms": {
+            "score_segments": round(score_ms, 4),
+            "select_compact": round(select_ms, 4),
+            "compress_static": round(static_ms, 4),
+            "chunk_attention": round(attn_ms, 4),
+        },
+        "breakdown_gbs": {
+            "score_segments": round(score_bytes / (score_ms * 1e-3) / 1e9, 1),
+            "select_compact": round(dyn_copy_bytes / (select_ms * 1e-3) / 1e9, 1),
+            "compress_static": round(static_copy_bytes / (static_ms * 1e-3) / 1e9, 1),
+            "peak": PEAK_HBM_GBS,
+        },
+        "attn_tflops": round(attn_tflops, 1),
+        "ms_per_chunk_extrapolated_30layers_4steps": round(wall_ms * 120, 2),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, x, args.cpu_rows)
+    print(json.dumps(out), flush=True)
+
+
+def _kernel_sha():
+    import hashlib
+    p = os.path.join(ROOT, "paper_2605_09681_amd", "csrc", "k_attn.hip")
+    with open(p, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+if __name__ == "__main__":
+    main()

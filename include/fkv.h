@@ -1,0 +1,184 @@
+/* fkv.h -- C ABI of the Forcing-KV hot path on AMD MI355X (gfx950).
+ *
+ * Forcing-KV (arXiv 2605.09681) compresses the KV cache of streaming
+ * autoregressive video-diffusion attention head by head:
+ *   - static heads keep the sink frame(s) and the transition anchor frame(s)
+ *     -- the most recent history frames -- (Sec. 4.2, Eq. 2);
+ *   - dynamic heads split every history frame into segments, score each
+ *     segment by the cosine similarity of its keys with the same segment of
+ *     the next frame, keep the least similar ones (BottomK) and gather them
+ *     (Sec. 4.3, Eq. 3 and the union defining the compressed cache);
+ *   - the current chunk's queries then attend, without a mask, over
+ *     [retained history; current chunk] (Eq. 2, Eq. 4).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Tensors are DEVICE pointers to row-major, contiguous memory, head_dim
+ * innermost, element type `shape->dtype` (bf16 or fp32), 16-byte aligned:
+ *   K_hist, V_hist : [n_heads][cap_frames][F][d]   history cache, physical slots
+ *   K_cur, V_cur, Q: [n_heads][C*F][d]             current chunk (Lq = C*F tokens)
+ *   Kc, Vc         : [n_heads][slab][d]            compressed history per head
+ *   O              : [n_heads][C*F][d]             attention output
+ *   scores         : float [n_heads][n_seg]        segment similarity (dynamic rows)
+ *   kept_seg       : int32 [n_heads][n_seg]        kept segment ids, ascending, -1 padded
+ *   kv_len         : int32 [n_heads]               retained history tokens per head
+ * `frame_slot` is a HOST array of int32[hist_frames]: logical history frame t
+ * (0 = oldest, the sink first) lives in physical slot frame_slot[t] of the
+ * cache; this expresses a ring-buffer cache with pinned sink frames.
+ * `heads` is a HOST array of fkv_head[n_heads]; `shape` a HOST struct.
+ * Logical history tokens are numbered x = t*F + p (frame t, position p);
+ * segment g covers tokens [g*L, min(g*L + L, H*F)), n_seg = ceil(H*F / L).
+ *
+ * Streams and ownership: every call validates its arguments on the host,
+ * then enqueues kernels on `stream` (a hipStream_t, NULL = default stream)
+ * and returns without synchronising; outputs are valid once the stream has
+ * run them.  The caller owns every buffer; the library allocates no device
+ * memory and keeps no pointer after a call returns.  K_hist and V_hist are
+ * only read: dynamic heads keep their whole history for later similarity
+ * scoring (Sec. 5.2), so compaction never modifies the cache.
+ *
+ * A slab of 0 tokens (nothing retained) may come with NULL Kc / Vc.
+ *
+ * Errors: a non-OK status is returned before anything is enqueued, so a
+ * failed call writes nothing.  FKV_ERR_ARG: null pointer, bad enum, negative
+ * budget, non-positive scale, slot out of range.  FKV_ERR_SHAPE: unsupported
+ * shape (see fkv_shape).  FKV_ERR_CAPACITY: `slab` or the workspace is too
+ * small.  FKV_ERR_DEVICE: the HIP runtime reported a launch error.
+ * fkv_last_error() returns a message for the last non-OK status of the calling
+ * thread.  Calls on distinct streams are independent; calls that share an
+ * output buffer must be ordered by the caller.
+ */
+#ifndef FKV_H
+#define FKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FKV_MAX_HEADS 64     /* n_heads limit */
+#define FKV_MAX_FRAMES 256   /* cap_frames limit */
+#define FKV_MAX_SEGMENTS 4096 /* n_seg limit */
+
+typedef enum {
+    FKV_OK = 0,
+    FKV_ERR_ARG = 1,
+    FKV_ERR_SHAPE = 2,
+    FKV_ERR_CAPACITY = 3,
+    FKV_ERR_DEVICE = 4
+} fkv_status;
+
+typedef enum { FKV_BF16 = 0, FKV_F32 = 1 } fkv_dtype;
+typedef enum { FKV_STATIC = 0, FKV_DYNAMIC = 1 } fkv_head_type;
+/* Selection group of dynamic heads: FKV_SCOPE_FRAME keeps k segments in every
+ * frame (the paper's per-frame BottomK, needs L < F); FKV_SCOPE_GLOBAL keeps k
+ * segments among all candidate segments of the history. */
+typedef enum { FKV_SCOPE_FRAME = 0, FKV_SCOPE_GLOBAL = 1 } fkv_scope;
+
+typedef struct {
+    int32_t n_heads;      /* 1..FKV_MAX_HEADS */
+    int32_t head_dim;     /* d: 64 or 128 */
+    int32_t frame_tokens; /* F >= 1: tokens per latent frame */
+    int32_t hist_frames;  /* H: logical history frames, 0..cap_frames (0: nothing cached) */
+    int32_t cap_frames;   /* physical slots in K_hist/V_hist, 1..FKV_MAX_FRAMES */
+    int32_t chunk_frames; /* C >= 1: frames of the current chunk */
+    int32_t seg_tokens;   /* L >= 1, with F % L == 0 or L % F == 0 */
+    int32_t dtype;        /* fkv_dtype */
+} fkv_shape;
+
+typedef struct {
+    int32_t type;          /* fkv_head_type */
+    int32_t sink_frames;   /* >= 0: leading logical frames always kept */
+    int32_t recent_frames; /* >= 0: trailing logical frames always kept (the
+                              transition anchor frame is recent_frames = 1) */
+    int32_t keep_k;        /* >= 0: dynamic heads keep min(keep_k, |group|)
+                              segments per selection group */
+    int32_t scope;         /* fkv_scope (dynamic heads) */
+} fkv_head;
+
+/* Number of segments n_seg = ceil(H*F / L) of `shape` (0 on a bad shape). */
+int32_t fkv_num_segments(const fkv_shape *shape);
+
+/* Largest kv_len head `head` can produce under its budget: for a static head
+ * the exact |kept frames|*F, for a dynamic head the maximum over all score
+ * outcomes (only a partial last segment makes it data dependent).  A `slab`
+ * of at least the maximum over the heads of one call is accepted. */
+fkv_status fkv_kept_tokens_max(const fkv_shape *shape, const fkv_head *heads,
+                               int32_t head, int64_t *tokens);
+
+/* Static structural pruning (Sec. 4.2, Eq. 2).  For every head of type
+ * FKV_STATIC: the kept logical frames are [0, min(sink,H)) U [max(H-recent,0),
+ * H), ascending, each once; their K and V rows are copied from physical slot
+ * frame_slot[t] to Kc[h] / Vc[h] in that order, and kv_len[h] = |kept|*F.
+ * Rows of dynamic heads are not touched.  FKV_ERR_CAPACITY if `slab` is below
+ * the kept token count of a static head. */
+fkv_status fkv_compress_static(const fkv_shape *shape, const fkv_head *heads,
+                               const void *K_hist, const void *V_hist,
+                               const int32_t *frame_slot, void *Kc, void *Vc,
+                               int32_t slab, int32_t *kv_len, void *stream);
+
+/* Device workspace fkv_score_segments needs for `shape` and the dynamic heads
+ * of `heads` (a multiple of 256 bytes; 0 when no head is dynamic or H = 0). */
+fkv_status fkv_score_workspace_size(const fkv_shape *shape, const fkv_head *heads,
+                                    size_t *bytes);
+
+/* Segment-wise similarity (Sec. 4.3, Eq. 3).  For every head of type
+ * FKV_DYNAMIC and every segment g: a = the keys of tokens [g*L, min(g*L+L,
+ * H*F)), b = the keys of the same tokens shifted by one frame (x + F; tokens
+ * at or past H*F are rows x + F - H*F of K_cur, i.e. the first frame of the
+ * current chunk follows the last history frame).  Every product is exact in
+ * fp64 and summed in fp64: dot = sum a*b, na = sum a*a, nb = sum b*b; then
+ * scores[h][g] = (float)(dot / sqrt(na*nb)) rounded to nearest even, or 0 when
+ * na*nb == 0.  The cosine is taken over the flattened segment (tokens x d).
+ * `workspace` holds fp64 partial sums (device memory of at least
+ * fkv_score_workspace_size bytes; its contents need no initialisation).  Rows
+ * of static heads are not touched.  H = 0 enqueues nothing. */
+fkv_status fkv_score_segments(const fkv_shape *shape, const fkv_head *heads,
+                              const void *K_hist, const int32_t *frame_slot,
+                              const void *K_cur, float *scores, void *workspace,
+                              size_t workspace_bytes, void *stream);
+
+/* BottomK selection and compaction (Sec. 4.3, Eq. 3 and the union defining
+ * the compressed cache).  For every head of type FKV_DYNAMIC: a segment is
+ * forced (kept) when it touches one of the first sink_frames frames or the
+ * last recent_frames frames; the other segments are candidates, grouped per
+ * frame (FKV_SCOPE_FRAME) or all together (FKV_SCOPE_GLOBAL), and each group
+ * keeps the min(keep_k, |group|) candidates of smallest key (isNaN(s), s, g):
+ * the least similar segments, NaN scores evicted first, equal scores (-0 ==
+ * +0) resolved by the lower index.  kept_seg[h] lists the kept segments in
+ * ascending order, padded with -1; their K and V rows are copied to Kc[h] /
+ * Vc[h] in that order; kv_len[h] = the number of tokens copied.  Reads
+ * `scores` as fkv_score_segments leaves them (any fp32 values are accepted).
+ * Rows of static heads are not touched.  FKV_ERR_CAPACITY if `slab` is below
+ * fkv_kept_tokens_max of a dynamic head. */
+fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads,
+                              const float *scores, const void *K_hist,
+                              const void *V_hist, const int32_t *frame_slot,
+                              int32_t *kept_seg, void *Kc, void *Vc, int32_t slab,
+                              int32_t *kv_len, void *stream);
+
+/* Chunk attention over the compressed cache (Eq. 2 for static heads, Eq. 4
+ * for dynamic heads).  For every head h and query row r < C*F, with keys
+ * [Kc[h][0:n]; K_cur[h]] and values [Vc[h][0:n]; V_cur[h]], n = kv_len[h]
+ * (read on the device, clamped to [0, slab]):
+ *   O[h][r] = softmax(scale * Q[h][r] . keys^T) . values   (no mask)
+ * bf16: bf16 inputs, MFMA products accumulated in fp32, fp32 online softmax,
+ * probabilities rounded to bf16 for the value product, output normalised and
+ * rounded to bf16.  fp32: all fp32.  lse (nullable, float [n_heads][C*F])
+ * receives the natural-log normaliser log(sum exp(scale*q.k)).  scale must be
+ * positive and finite (1/sqrt(d) is the usual choice). */
+fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q,
+                               const void *Kc, const void *Vc, int32_t slab,
+                               const int32_t *kv_len, const void *K_cur,
+                               const void *V_cur, float scale, void *O,
+                               float *lse, void *stream);
+
+/* Message describing the calling thread's last non-OK status ("" if none). */
+const char *fkv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FKV_H */

@@ -1,0 +1,253 @@
+"""Forcing-KV hot path on AMD MI355X: Python binding of libfkv.
+
+Thin ctypes layer over the C ABI declared in ``include/fkv.h``; every
+function has the C entry point's name and only marshals arguments (torch
+tensors supply device memory, ``torch.cuda.current_stream()`` the stream).
+All compute runs in the HIP kernels of ``libfkv.so``; there is no CPU
+fallback.  If the library has not been built, calls raise
+:class:`FkvLibraryMissing`.
+
+Entry points (see ``include/fkv.h`` for the full contract):
+
+* :func:`fkv_compress_static`  -- static structural pruning (Sec. 4.2, Eq. 2)
+* :func:`fkv_score_segments`   -- segment similarity (Sec. 4.3, Eq. 3)
+* :func:`fkv_select_compact`   -- BottomK + compaction (Sec. 4.3, Eq. 3)
+* :func:`fkv_chunk_attention`  -- chunk attention (Eq. 2 / Eq. 4)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfkv.so")
+
+FKV_OK, FKV_ERR_ARG, FKV_ERR_SHAPE, FKV_ERR_CAPACITY, FKV_ERR_DEVICE = range(5)
+FKV_BF16, FKV_F32 = 0, 1
+FKV_STATIC, FKV_DYNAMIC = 0, 1
+FKV_SCOPE_FRAME, FKV_SCOPE_GLOBAL = 0, 1
+FKV_MAX_HEADS, FKV_MAX_FRAMES, FKV_MAX_SEGMENTS = 64, 256, 4096
+
+EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
+            "fkv_score_workspace_size", "fkv_score_segments", "fkv_select_compact",
+            "fkv_chunk_attention", "fkv_last_error")
+
+
+class FkvLibraryMissing(RuntimeError):
+    pass
+
+
+class FkvError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"fkv status {status}: {message}")
+        self.status = status
+        self.message = message
+
+
+class fkv_shape(ctypes.Structure):
+    _fields_ = [("n_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("frame_tokens", ctypes.c_int32), ("hist_frames", ctypes.c_int32),
+                ("cap_frames", ctypes.c_int32), ("chunk_frames", ctypes.c_int32),
+                ("seg_tokens", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class fkv_head(ctypes.Structure):
+    _fields_ = [("type", ctypes.c_int32), ("sink_frames", ctypes.c_int32),
+                ("recent_frames", ctypes.c_int32), ("keep_k", ctypes.c_int32),
+                ("scope", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libfkv.so (raises FkvLibraryMissing if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise FkvLibraryMissing(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2605_09681_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I32, I64, SZ, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+        S, Hd = ctypes.POINTER(fkv_shape), ctypes.POINTER(fkv_head)
+        L.fkv_num_segments.argtypes = [S]
+        L.fkv_num_segments.restype = I32
+        L.fkv_kept_tokens_max.argtypes = [S, Hd, I32, ctypes.POINTER(I64)]
+        L.fkv_kept_tokens_max.restype = ctypes.c_int
+        L.fkv_compress_static.argtypes = [S, Hd, P, P, P, P, P, I32, P, P]
+        L.fkv_compress_static.restype = ctypes.c_int
+        L.fkv_score_workspace_size.argtypes = [S, Hd, ctypes.POINTER(SZ)]
+        L.fkv_score_workspace_size.restype = ctypes.c_int
+        L.fkv_score_segments.argtypes = [S, Hd, P, P, P, P, P, SZ, P]
+        L.fkv_score_segments.restype = ctypes.c_int
+        L.fkv_select_compact.argtypes = [S, Hd, P, P, P, P, P, P, P, I32, P, P]
+        L.fkv_select_compact.restype = ctypes.c_int
+        L.fkv_chunk_attention.argtypes = [S, P, P, P, I32, P, P, P, F, P, P, P]
+        L.fkv_chunk_attention.restype = ctypes.c_int
+        L.fkv_last_error.argtypes = []
+        L.fkv_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+# ---------------------------------------------------------------------------
+# argument marshalling
+# ---------------------------------------------------------------------------
+def make_shape(n_heads, head_dim, frame_tokens, hist_frames, cap_frames, chunk_frames,
+               seg_tokens, dtype) -> fkv_shape:
+    dt = {"bf16": FKV_BF16, "f32": FKV_F32, FKV_BF16: FKV_BF16, FKV_F32: FKV_F32}[dtype]
+    return fkv_shape(n_heads, head_dim, frame_tokens, hist_frames, cap_frames, chunk_frames,
+                     seg_tokens, dt)
+
+
+def make_heads(budgets: Sequence) -> ctypes.Array:
+    """Per-head budgets: objects with type/sink_frames/recent_frames/keep_k/scope
+    attributes, or 5-tuples in that order."""
+    arr = (fkv_head * len(budgets))()
+    for i, b in enumerate(budgets):
+        vals = (b.type, b.sink_frames, b.recent_frames, b.keep_k, b.scope) if hasattr(b, "type") else tuple(b)
+        arr[i] = fkv_head(*map(int, vals))
+    return arr
+
+
+def _torch_dtype(shape: fkv_shape):
+    return torch.bfloat16 if shape.dtype == FKV_BF16 else torch.float32
+
+
+def _check(t: torch.Tensor, name: str, dtype, size=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device})")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if size is not None and tuple(t.shape) != tuple(size):
+        raise ValueError(f"{name} must have shape {tuple(size)} (got {tuple(t.shape)})")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _slots(frame_slot, H):
+    if frame_slot is None:
+        import numpy as np
+        frame_slot = np.arange(H, dtype="int32")
+    arr = (ctypes.c_int32 * max(H, 1))()
+    vals = [int(v) for v in (frame_slot.tolist() if hasattr(frame_slot, "tolist") else frame_slot)]
+    if len(vals) != H:
+        raise ValueError(f"frame_slot needs {H} entries (got {len(vals)})")
+    for i, v in enumerate(vals):
+        arr[i] = v
+    return arr
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _raise(status: int):
+    if status != FKV_OK:
+        raise FkvError(status, lib().fkv_last_error().decode())
+
+
+def _lq(shape):
+    return shape.chunk_frames * shape.frame_tokens
+
+
+# ---------------------------------------------------------------------------
+# entry points
+# ---------------------------------------------------------------------------
+def fkv_num_segments(shape: fkv_shape) -> int:
+    return int(lib().fkv_num_segments(ctypes.byref(shape)))
+
+
+def fkv_kept_tokens_max(shape: fkv_shape, heads, head: int) -> int:
+    out = ctypes.c_int64(0)
+    _raise(lib().fkv_kept_tokens_max(ctypes.byref(shape), heads, int(head), ctypes.byref(out)))
+    return int(out.value)
+
+
+def slab_tokens(shape: fkv_shape, heads) -> int:
+    """Smallest slab (tokens per head of Kc/Vc) that fits every head's budget."""
+    return max([fkv_kept_tokens_max(shape, heads, h) for h in range(shape.n_heads)] + [0])
+
+
+def fkv_score_workspace_size(shape: fkv_shape, heads) -> int:
+    out = ctypes.c_size_t(0)
+    _raise(lib().fkv_score_workspace_size(ctypes.byref(shape), heads, ctypes.byref(out)))
+    return int(out.value)
+
+
+def fkv_compress_static(shape: fkv_shape, heads, K_hist, V_hist, frame_slot, Kc, Vc, kv_len,
+                        stream=None):
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    slab = Kc.shape[1] if Kc.dim() == 3 else -1
+    comp = (shape.n_heads, slab, shape.head_dim)
+    args = [_check(K_hist, "K_hist", dt, hist), _check(V_hist, "V_hist", dt, hist)]
+    sl = _slots(frame_slot, shape.hist_frames)
+    args += [_check(Kc, "Kc", dt, comp), _check(Vc, "Vc", dt, comp)]
+    kl = _check(kv_len, "kv_len", torch.int32, (shape.n_heads,))
+    _raise(lib().fkv_compress_static(ctypes.byref(shape), heads, args[0], args[1], sl, args[2],
+                                     args[3], int(slab), kl, _stream(stream)))
+
+
+def fkv_score_segments(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, scores,
+                       workspace: Optional[torch.Tensor] = None, stream=None):
+    """If ``workspace`` is None a torch uint8 tensor of the required size is
+    allocated on the current device (through torch's caching allocator)."""
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    n_seg = fkv_num_segments(shape)
+    kh = _check(K_hist, "K_hist", dt, hist)
+    sl = _slots(frame_slot, shape.hist_frames)
+    kc = _check(K_cur, "K_cur", dt, (shape.n_heads, _lq(shape), shape.head_dim))
+    sc = _check(scores, "scores", torch.float32, (shape.n_heads, n_seg))
+    need = fkv_score_workspace_size(shape, heads)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=K_hist.device)
+    ws = _check(workspace, "workspace", torch.uint8)
+    _raise(lib().fkv_score_segments(ctypes.byref(shape), heads, kh, sl, kc, sc, ws,
+                                    workspace.numel(), _stream(stream)))
+    return workspace
+
+
+def fkv_select_compact(shape: fkv_shape, heads, scores, K_hist, V_hist, frame_slot, kept_seg,
+                       Kc, Vc, kv_len, stream=None):
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    n_seg = fkv_num_segments(shape)
+    sc = _check(scores, "scores", torch.float32, (shape.n_heads, n_seg))
+    kh, vh = _check(K_hist, "K_hist", dt, hist), _check(V_hist, "V_hist", dt, hist)
+    sl = _slots(frame_slot, shape.hist_frames)
+    ks = _check(kept_seg, "kept_seg", torch.int32, (shape.n_heads, n_seg))
+    slab = Kc.shape[1] if Kc.dim() == 3 else -1
+    comp = (shape.n_heads, slab, shape.head_dim)
+    kc, vc = _check(Kc, "Kc", dt, comp), _check(Vc, "Vc", dt, comp)
+    kl = _check(kv_len, "kv_len", torch.int32, (shape.n_heads,))
+    _raise(lib().fkv_select_compact(ctypes.byref(shape), heads, sc, kh, vh, sl, ks, kc, vc,
+                                    int(slab), kl, _stream(stream)))
+
+
+def fkv_chunk_attention(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, scale: float, O,
+                        lse: Optional[torch.Tensor] = None, stream=None):
+    dt = _torch_dtype(shape)
+    chunk = (shape.n_heads, _lq(shape), shape.head_dim)
+    slab = Kc.shape[1] if Kc.dim() == 3 else -1
+    comp = (shape.n_heads, slab, shape.head_dim)
+    q = _check(Q, "Q", dt, chunk)
+    kc, vc = _check(Kc, "Kc", dt, comp), _check(Vc, "Vc", dt, comp)
+    kl = _check(kv_len, "kv_len", torch.int32, (shape.n_heads,))
+    kq, vq = _check(K_cur, "K_cur", dt, chunk), _check(V_cur, "V_cur", dt, chunk)
+    o = _check(O, "O", dt, chunk)
+    ls = None if lse is None else _check(lse, "lse", torch.float32, (shape.n_heads, _lq(shape)))
+    _raise(lib().fkv_chunk_attention(ctypes.byref(shape), q, kc, vc, int(slab), kl, kq, vq,
+                                     ctypes.c_float(scale), o, ls, _stream(stream)))
+
+
+def fkv_last_error() -> str:
+    return lib().fkv_last_error().decode()

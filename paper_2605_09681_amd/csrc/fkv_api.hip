@@ -1,0 +1,418 @@
+// fkv_api.hip -- the C ABI of libfkv: host-side validation, launch planning
+// and error reporting for the Forcing-KV hot path kernels.
+//
+// Every entry point checks all of its arguments before it touches the HIP
+// runtime, so a non-OK status means nothing was enqueued or written.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "fkv_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+fkv_status fail(fkv_status st, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+fkv_status ok() {
+    g_err[0] = '\0';
+    return FKV_OK;
+}
+
+size_t elem_size(const fkv_shape *s) { return s->dtype == FKV_BF16 ? 2 : 4; }
+
+fkv_status check_shape(const fkv_shape *s) {
+    if (!s) return fail(FKV_ERR_ARG, "shape is NULL");
+    if (s->dtype != FKV_BF16 && s->dtype != FKV_F32)
+        return fail(FKV_ERR_ARG, "dtype %d is not FKV_BF16 or FKV_F32", s->dtype);
+    if (s->n_heads < 1 || s->n_heads > FKV_MAX_HEADS)
+        return fail(FKV_ERR_SHAPE, "n_heads %d outside [1, %d]", s->n_heads, FKV_MAX_HEADS);
+    if (s->head_dim != 64 && s->head_dim != 128)
+        return fail(FKV_ERR_SHAPE, "head_dim %d is not 64 or 128", s->head_dim);
+    if (s->frame_tokens < 1) return fail(FKV_ERR_SHAPE, "frame_tokens %d < 1", s->frame_tokens);
+    if (s->cap_frames < 1 || s->cap_frames > FKV_MAX_FRAMES)
+        return fail(FKV_ERR_SHAPE, "cap_frames %d outside [1, %d]", s->cap_frames, FKV_MAX_FRAMES);
+    if (s->hist_frames < 0 || s->hist_frames > s->cap_frames)
+        return fail(FKV_ERR_SHAPE, "hist_frames %d outside [0, cap_frames=%d]", s->hist_frames,
+                    s->cap_frames);
+    if (s->chunk_frames < 1) return fail(FKV_ERR_SHAPE, "chunk_frames %d < 1", s->chunk_frames);
+    if (s->seg_tokens < 1) return fail(FKV_ERR_SHAPE, "seg_tokens %d < 1", s->seg_tokens);
+    if (s->frame_tokens % s->seg_tokens != 0 && s->seg_tokens % s->frame_tokens != 0)
+        return fail(FKV_ERR_SHAPE, "seg_tokens %d neither divides nor is a multiple of frame_tokens %d",
+                    s->seg_tokens, s->frame_tokens);
+    const int64_t hist_tokens = (int64_t)s->hist_frames * s->frame_tokens;
+    const int64_t lq = (int64_t)s->chunk_frames * s->frame_tokens;
+    const int64_t cap_tokens = (int64_t)s->cap_frames * s->frame_tokens;
+    if (cap_tokens + lq > (int64_t)1 << 30)
+        return fail(FKV_ERR_SHAPE, "cache + chunk of %lld tokens per head is too large",
+                    (long long)(cap_tokens + lq));
+    const int64_t n_seg = (hist_tokens + s->seg_tokens - 1) / s->seg_tokens;
+    if (n_seg > FKV_MAX_SEGMENTS)
+        return fail(FKV_ERR_SHAPE, "%lld segments exceed %d", (long long)n_seg, FKV_MAX_SEGMENTS);
+    return FKV_OK;
+}
+
+fkv_status check_heads(const fkv_shape *s, const fkv_head *heads) {
+    if (!heads) return fail(FKV_ERR_ARG, "heads is NULL");
+    for (int h = 0; h < s->n_heads; ++h) {
+        const fkv_head &b = heads[h];
+        if (b.type != FKV_STATIC && b.type != FKV_DYNAMIC)
+            return fail(FKV_ERR_ARG, "head %d: type %d is not FKV_STATIC or FKV_DYNAMIC", h, b.type);
+        if (b.sink_frames < 0 || b.recent_frames < 0 || b.keep_k < 0)
+            return fail(FKV_ERR_ARG, "head %d: negative budget (sink %d, recent %d, keep_k %d)", h,
+                        b.sink_frames, b.recent_frames, b.keep_k);
+        if (b.scope != FKV_SCOPE_FRAME && b.scope != FKV_SCOPE_GLOBAL)
+            return fail(FKV_ERR_ARG, "head %d: scope %d is not FKV_SCOPE_FRAME or FKV_SCOPE_GLOBAL", h,
+                        b.scope);
+        if (b.type == FKV_DYNAMIC && b.scope == FKV_SCOPE_FRAME && s->seg_tokens >= s->frame_tokens)
+            return fail(FKV_ERR_SHAPE, "head %d: per-frame selection needs seg_tokens %d < frame_tokens %d",
+                        h, s->seg_tokens, s->frame_tokens);
+    }
+    return FKV_OK;
+}
+
+fkv_status check_slots(const fkv_shape *s, const int32_t *slots) {
+    if (s->hist_frames == 0) return FKV_OK;
+    if (!slots) return fail(FKV_ERR_ARG, "frame_slot is NULL");
+    for (int t = 0; t < s->hist_frames; ++t)
+        if (slots[t] < 0 || slots[t] >= s->cap_frames)
+            return fail(FKV_ERR_ARG, "frame_slot[%d] = %d outside [0, cap_frames=%d)", t, slots[t],
+                        s->cap_frames);
+    return FKV_OK;
+}
+
+// --------------------------------------------------------------- budgets
+struct StaticPlan {
+    int n_first, gap, n_kept;
+};
+
+// Kept frames [0, min(sink,H)) U [max(H-recent,0), H): y < n_first -> y, else y + gap.
+StaticPlan static_plan(int H, const fkv_head &b) {
+    const int a = std::min(b.sink_frames, H);
+    const int lo = std::max(H - b.recent_frames, 0);
+    StaticPlan p;
+    if (lo <= a) {  // the two windows meet: the whole history is kept
+        p.n_first = H;
+        p.gap = 0;
+        p.n_kept = H;
+    } else {
+        p.n_first = a;
+        p.gap = lo - a;
+        p.n_kept = a + (H - lo);
+    }
+    return p;
+}
+
+struct DynPlan {
+    int kk;            // kept candidates per group
+    int n_kept;        // kept segments (exact)
+    int64_t max_tokens;  // largest possible kv_len
+};
+
+DynPlan dyn_plan(const fkv_shape *s, const fkv_head &b) {
+    const int H = s->hist_frames, F = s->frame_tokens, L = s->seg_tokens;
+    const int64_t HF = (int64_t)H * F;
+    const int n_seg = (int)((HF + L - 1) / L);
+    std::vector<int64_t> cand_tokens;
+    int n_forced = 0;
+    int64_t forced_tokens = 0;
+    for (int g = 0; g < n_seg; ++g) {
+        const int64_t x0 = (int64_t)g * L, x1 = std::min(x0 + L, HF);
+        const int first = (int)(x0 / F), last = (int)((x1 - 1) / F);
+        if (first < b.sink_frames || last >= H - b.recent_frames) {
+            ++n_forced;
+            forced_tokens += x1 - x0;
+        } else {
+            cand_tokens.push_back(x1 - x0);
+        }
+    }
+    DynPlan p;
+    const int n_cand = (int)cand_tokens.size();
+    if (b.scope == FKV_SCOPE_FRAME) {
+        // every candidate frame holds F/L full segments
+        const int per = F / L;
+        p.kk = std::min(b.keep_k, per);
+        const int cand_frames = n_cand / per;
+        p.n_kept = n_forced + cand_frames * p.kk;
+        p.max_tokens = forced_tokens + (int64_t)cand_frames * p.kk * L;
+    } else {
+        p.kk = std::min(b.keep_k, n_cand);
+        p.n_kept = n_forced + p.kk;
+        std::sort(cand_tokens.begin(), cand_tokens.end(), [](int64_t x, int64_t y) { return x > y; });
+        int64_t t = forced_tokens;
+        for (int i = 0; i < p.kk; ++i) t += cand_tokens[i];
+        p.max_tokens = t;
+    }
+    return p;
+}
+
+fkv_status device_status(hipError_t e, const char *what) {
+    if (e != hipSuccess)
+        return fail(FKV_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+template <typename T>
+T *as(void *p) { return (T *)p; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t fkv_num_segments(const fkv_shape *shape) {
+    if (check_shape(shape) != FKV_OK) return 0;
+    const int64_t ht = (int64_t)shape->hist_frames * shape->frame_tokens;
+    return (int32_t)((ht + shape->seg_tokens - 1) / shape->seg_tokens);
+}
+
+fkv_status fkv_kept_tokens_max(const fkv_shape *shape, const fkv_head *heads, int32_t head,
+                               int64_t *tokens) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if (!tokens) return fail(FKV_ERR_ARG, "tokens is NULL");
+    if (head < 0 || head >= shape->n_heads)
+        return fail(FKV_ERR_ARG, "head %d outside [0, %d)", head, shape->n_heads);
+    const fkv_head &b = heads[head];
+    if (b.type == FKV_STATIC)
+        *tokens = (int64_t)static_plan(shape->hist_frames, b).n_kept * shape->frame_tokens;
+    else
+        *tokens = shape->hist_frames == 0 ? 0 : dyn_plan(shape, b).max_tokens;
+    return ok();
+}
+
+fkv_status fkv_compress_static(const fkv_shape *shape, const fkv_head *heads, const void *K_hist,
+                               const void *V_hist, const int32_t *frame_slot, void *Kc, void *Vc,
+                               int32_t slab, int32_t *kv_len, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if (!K_hist || !V_hist || !kv_len) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (slab < 0) return fail(FKV_ERR_ARG, "slab %d < 0", slab);
+    if (slab > 0 && (!Kc || !Vc)) return fail(FKV_ERR_ARG, "NULL Kc/Vc with slab %d", slab);
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+
+    fkv::StaticCopyArgs a;
+    memset(&a, 0, sizeof a);
+    int max_kept = 0;
+    for (int h = 0; h < shape->n_heads; ++h) {
+        if (heads[h].type != FKV_STATIC) continue;
+        const StaticPlan p = static_plan(shape->hist_frames, heads[h]);
+        const int64_t need = (int64_t)p.n_kept * shape->frame_tokens;
+        if (need > slab)
+            return fail(FKV_ERR_CAPACITY, "head %d keeps %lld tokens but slab is %d", h,
+                        (long long)need, slab);
+        const int li = a.heads.n++;
+        a.heads.head[li] = h;
+        a.n_first[li] = p.n_first;
+        a.gap[li] = p.gap;
+        a.n_kept[li] = p.n_kept;
+        max_kept = std::max(max_kept, p.n_kept);
+    }
+    if (a.heads.n == 0) return ok();
+    const size_t es = elem_size(shape);
+    a.K_hist = (const uint8_t *)K_hist;
+    a.V_hist = (const uint8_t *)V_hist;
+    a.Kc = (uint8_t *)Kc;
+    a.Vc = (uint8_t *)Vc;
+    a.kv_len = kv_len;
+    a.slab = slab;
+    a.row_bytes = (int64_t)shape->head_dim * es;
+    a.frame_vecs = (int64_t)shape->frame_tokens * a.row_bytes / 16;
+    a.F = shape->frame_tokens;
+    a.cap = shape->cap_frames;
+    for (int t = 0; t < shape->hist_frames; ++t) a.slots.slot[t] = frame_slot[t];
+    (void)hipGetLastError();
+    return device_status(fkv::launch_static_copy(a, max_kept, (hipStream_t)stream),
+                         "fkv_compress_static launch");
+}
+
+static void score_geometry(const fkv_shape *s, int *unit_tokens, int *units, int64_t *unit_vecs,
+                           int *chunks) {
+    const int U = std::min(s->seg_tokens, s->frame_tokens);
+    *unit_tokens = U;
+    *units = s->frame_tokens / U;
+    *unit_vecs = (int64_t)U * s->head_dim * elem_size(s) / 16;
+    *chunks = (int)((*unit_vecs + fkv::kScoreThreads - 1) / fkv::kScoreThreads);
+}
+
+fkv_status fkv_score_workspace_size(const fkv_shape *shape, const fkv_head *heads, size_t *bytes) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if (!bytes) return fail(FKV_ERR_ARG, "bytes is NULL");
+    int n_dyn = 0;
+    for (int h = 0; h < shape->n_heads; ++h) n_dyn += heads[h].type == FKV_DYNAMIC;
+    if (n_dyn == 0 || shape->hist_frames == 0) {
+        *bytes = 0;
+        return ok();
+    }
+    int U, units, chunks;
+    int64_t uv;
+    score_geometry(shape, &U, &units, &uv, &chunks);
+    const size_t b = fkv::score_workspace_doubles(n_dyn, shape->hist_frames, units, chunks) * sizeof(double);
+    *bytes = (b + 255) & ~(size_t)255;
+    return ok();
+}
+
+fkv_status fkv_score_segments(const fkv_shape *shape, const fkv_head *heads, const void *K_hist,
+                              const int32_t *frame_slot, const void *K_cur, float *scores,
+                              void *workspace, size_t workspace_bytes, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+    size_t need = 0;
+    if ((st = fkv_score_workspace_size(shape, heads, &need)) != FKV_OK) return st;
+    if (need == 0) return ok();  // no dynamic head, or nothing cached yet
+    if (!K_hist || !K_cur || !scores) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (!workspace) return fail(FKV_ERR_ARG, "workspace is NULL");
+    if (workspace_bytes < need)
+        return fail(FKV_ERR_CAPACITY, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+
+    fkv::ScoreArgs a;
+    memset(&a, 0, sizeof a);
+    for (int h = 0; h < shape->n_heads; ++h)
+        if (heads[h].type == FKV_DYNAMIC) a.heads.head[a.heads.n++] = h;
+    const size_t es = elem_size(shape);
+    a.K_hist = (const uint8_t *)K_hist;
+    a.K_cur = (const uint8_t *)K_cur;
+    a.scores = scores;
+    a.ws = (double *)workspace;
+    a.frame_bytes = (int64_t)shape->frame_tokens * shape->head_dim * es;
+    a.cur_vecs = (int64_t)shape->chunk_frames * a.frame_bytes / 16;
+    a.F = shape->frame_tokens;
+    a.L = shape->seg_tokens;
+    a.H = shape->hist_frames;
+    a.cap = shape->cap_frames;
+    a.n_seg = fkv_num_segments(shape);
+    a.d = shape->head_dim;
+    a.esize = (int)es;
+    score_geometry(shape, &a.unit_tokens, &a.units_per_frame, &a.unit_vecs, &a.chunks_per_unit);
+    for (int t = 0; t < shape->hist_frames; ++t) a.slots.slot[t] = frame_slot[t];
+    (void)hipGetLastError();
+    return device_status(fkv::launch_score(a, shape->dtype == FKV_F32, (hipStream_t)stream),
+                         "fkv_score_segments launch");
+}
+
+fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads, const float *scores,
+                              const void *K_hist, const void *V_hist, const int32_t *frame_slot,
+                              int32_t *kept_seg, void *Kc, void *Vc, int32_t slab, int32_t *kv_len,
+                              void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if (!K_hist || !V_hist || !kv_len) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (slab < 0) return fail(FKV_ERR_ARG, "slab %d < 0", slab);
+    if (slab > 0 && (!Kc || !Vc)) return fail(FKV_ERR_ARG, "NULL Kc/Vc with slab %d", slab);
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+    const int n_seg = fkv_num_segments(shape);
+    if (n_seg > 0 && (!scores || !kept_seg)) return fail(FKV_ERR_ARG, "NULL scores or kept_seg");
+
+    fkv::SelectArgs sa;
+    memset(&sa, 0, sizeof sa);
+    int max_pieces = 0;
+    const int m = shape->seg_tokens > shape->frame_tokens ? shape->seg_tokens / shape->frame_tokens : 1;
+    for (int h = 0; h < shape->n_heads; ++h) {
+        if (heads[h].type != FKV_DYNAMIC) continue;
+        DynPlan p = {0, 0, 0};
+        if (shape->hist_frames > 0) p = dyn_plan(shape, heads[h]);
+        if (p.max_tokens > slab)
+            return fail(FKV_ERR_CAPACITY, "head %d may keep %lld tokens but slab is %d", h,
+                        (long long)p.max_tokens, slab);
+        const int li = sa.heads.n++;
+        sa.heads.head[li] = h;
+        sa.sink[li] = heads[h].sink_frames;
+        sa.recent[li] = heads[h].recent_frames;
+        sa.scope[li] = heads[h].scope;
+        sa.k[li] = p.kk;
+        max_pieces = std::max(max_pieces, p.n_kept * m);
+    }
+    if (sa.heads.n == 0) return ok();
+    (void)hipGetLastError();
+    sa.scores = scores;
+    sa.kept_seg = kept_seg;
+    sa.kv_len = kv_len;
+    sa.F = shape->frame_tokens;
+    sa.L = shape->seg_tokens;
+    sa.H = shape->hist_frames;
+    sa.n_seg = n_seg;
+    // With nothing cached (H = 0, the first AR step) the selection kernel only
+    // writes kv_len = 0 and there is nothing to copy.
+    fkv_status rs = device_status(fkv::launch_select(sa, (hipStream_t)stream), "fkv_select_compact select launch");
+    if (rs != FKV_OK || n_seg == 0) return rs;
+
+    fkv::DynCopyArgs ca;
+    memset(&ca, 0, sizeof ca);
+    const size_t es = elem_size(shape);
+    ca.K_hist = (const uint8_t *)K_hist;
+    ca.V_hist = (const uint8_t *)V_hist;
+    ca.Kc = (uint8_t *)Kc;
+    ca.Vc = (uint8_t *)Vc;
+    ca.kept_seg = kept_seg;
+    ca.slab = slab;
+    ca.row_bytes = (int64_t)shape->head_dim * es;
+    ca.piece_tokens = std::min(shape->seg_tokens, shape->frame_tokens);
+    ca.pieces_per_seg = m;
+    ca.piece_vecs = (int64_t)ca.piece_tokens * ca.row_bytes / 16;
+    ca.F = shape->frame_tokens;
+    ca.L = shape->seg_tokens;
+    ca.H = shape->hist_frames;
+    ca.cap = shape->cap_frames;
+    ca.n_seg = n_seg;
+    ca.heads = sa.heads;
+    for (int t = 0; t < shape->hist_frames; ++t) ca.slots.slot[t] = frame_slot[t];
+    return device_status(fkv::launch_dyn_copy(ca, max_pieces, (hipStream_t)stream),
+                         "fkv_select_compact copy launch");
+}
+
+fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q, const void *Kc, const void *Vc,
+                               int32_t slab, const int32_t *kv_len, const void *K_cur,
+                               const void *V_cur, float scale, void *O, float *lse, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if (!Q || !K_cur || !V_cur || !O || !kv_len) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (slab < 0) return fail(FKV_ERR_ARG, "slab %d < 0", slab);
+    if (slab > 0 && (!Kc || !Vc)) return fail(FKV_ERR_ARG, "NULL Kc/Vc with slab %d", slab);
+    if (!(scale > 0.f) || !isfinite(scale)) return fail(FKV_ERR_ARG, "scale %g must be positive and finite", (double)scale);
+
+    fkv::AttnArgs a;
+    memset(&a, 0, sizeof a);
+    a.Q = Q;
+    a.Kc = Kc ? Kc : K_cur;
+    a.Vc = Vc ? Vc : V_cur;
+    a.K_cur = K_cur;
+    a.V_cur = V_cur;
+    a.O = O;
+    a.lse = lse;
+    a.kv_len = kv_len;
+    a.slab = slab;
+    a.n_heads = shape->n_heads;
+    a.Lq = shape->chunk_frames * shape->frame_tokens;
+    a.scale = scale;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    const bool bf16 = shape->dtype == FKV_BF16;
+    const int rows = bf16 ? fkv::kAttnRowsBf16 : fkv::kAttnRowsF32;
+    a.n_qtiles = (a.Lq + rows - 1) / rows;
+    a.n_items = a.n_heads * a.n_qtiles;
+    a.items_per_xcd = (a.n_items + 7) / 8;
+    (void)hipGetLastError();
+    hipError_t e = bf16 ? fkv::launch_attention_bf16(a, shape->head_dim, (hipStream_t)stream)
+                        : fkv::launch_attention_f32(a, shape->head_dim, (hipStream_t)stream);
+    return device_status(e, "fkv_chunk_attention launch");
+}
+
+const char *fkv_last_error(void) { return g_err; }
+
+}  // extern "C"

@@ -1,0 +1,114 @@
+// fkv_internal.h -- kernel argument blocks and launchers shared by the HIP
+// translation units of libfkv (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fkv.h"
+
+namespace fkv {
+
+// Native 16-byte vector (usable with the nontemporal load/store builtins).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Per-call tables passed by value in the kernel argument segment: the host
+// has validated every entry, so kernels index with them without re-checking.
+struct SlotTable {
+    int32_t slot[FKV_MAX_FRAMES];  // logical history frame -> physical slot
+};
+
+struct HeadList {
+    int32_t n;                      // number of heads in the list
+    int32_t head[FKV_MAX_HEADS];    // head index into the [n_heads] tensors
+};
+
+// ---------------------------------------------------------------- static copy
+struct StaticCopyArgs {
+    const uint8_t *K_hist, *V_hist;
+    uint8_t *Kc, *Vc;
+    int32_t *kv_len;
+    int64_t slab;                   // tokens per head in Kc/Vc
+    int64_t frame_vecs;             // 16-byte vectors per frame (F*d*esize/16)
+    int64_t row_bytes;              // d * esize
+    int32_t F, cap;
+    HeadList heads;
+    int32_t n_first[FKV_MAX_HEADS]; // kept frames y < n_first are frame y
+    int32_t gap[FKV_MAX_HEADS];     // kept frames y >= n_first are frame y + gap
+    int32_t n_kept[FKV_MAX_HEADS];  // kept frame count
+    SlotTable slots;
+};
+
+// --------------------------------------------------------------- dynamic copy
+struct DynCopyArgs {
+    const uint8_t *K_hist, *V_hist;
+    uint8_t *Kc, *Vc;
+    const int32_t *kept_seg;        // [n_heads][n_seg]
+    int64_t slab;
+    int64_t piece_vecs;             // 16-byte vectors per piece
+    int64_t row_bytes;
+    int32_t F, L, H, cap, n_seg;
+    int32_t piece_tokens;           // min(L, F)
+    int32_t pieces_per_seg;         // max(1, L / F)
+    HeadList heads;
+    SlotTable slots;
+};
+
+// ---------------------------------------------------------------- selection
+struct SelectArgs {
+    const float *scores;            // [n_heads][n_seg]
+    int32_t *kept_seg;              // [n_heads][n_seg]
+    int32_t *kv_len;                // [n_heads]
+    int32_t F, L, H, n_seg;
+    HeadList heads;
+    int32_t sink[FKV_MAX_HEADS], recent[FKV_MAX_HEADS], scope[FKV_MAX_HEADS];
+    int32_t k[FKV_MAX_HEADS];       // kk = min(keep_k, |group|) per head
+};
+
+// ------------------------------------------------------------------ scoring
+struct ScoreArgs {
+    const uint8_t *K_hist, *K_cur;
+    float *scores;                  // [n_heads][n_seg]
+    double *ws;                     // partial sums (see k_score.hip)
+    int64_t frame_bytes;            // F*d*esize
+    int64_t unit_vecs;              // 16-byte vectors per unit (U*d*esize/16)
+    int64_t cur_vecs;               // 16-byte vectors per head of K_cur (C*F*d*esize/16)
+    int32_t F, L, H, cap, n_seg, d;
+    int32_t unit_tokens;            // U = min(L, F)
+    int32_t units_per_frame;        // F / U
+    int32_t chunks_per_unit;        // ceil(unit_vecs / 256)
+    int32_t esize;
+    HeadList heads;
+    SlotTable slots;
+};
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+    const void *Q, *Kc, *Vc, *K_cur, *V_cur;
+    void *O;
+    float *lse;
+    const int32_t *kv_len;
+    int64_t slab;
+    int32_t n_heads, Lq;
+    int32_t n_qtiles;               // ceil(Lq / BM)
+    int32_t n_items;                // n_heads * n_qtiles
+    int32_t items_per_xcd;          // ceil(n_items / 8)
+    float scale;                    // softmax scale
+    float scale_log2;               // scale * log2(e)
+};
+
+constexpr int kScoreThreads = 256;
+constexpr int kAttnRowsBf16 = 128;  // query rows per attention workgroup (bf16 MFMA kernel)
+constexpr int kAttnRowsF32 = 32;    // query rows per attention workgroup (fp32 kernel)
+constexpr int kScoreWaves = kScoreThreads / 64;
+
+size_t score_workspace_doubles(int n_dyn, int H, int units_per_frame, int chunks_per_unit);
+
+hipError_t launch_static_copy(const StaticCopyArgs &a, int max_kept, hipStream_t s);
+hipError_t launch_dyn_copy(const DynCopyArgs &a, int max_pieces, hipStream_t s);
+hipError_t launch_select(const SelectArgs &a, hipStream_t s);
+hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s);
+hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s);
+hipError_t launch_attention_f32(const AttnArgs &a, int head_dim, hipStream_t s);
+
+}  // namespace fkv

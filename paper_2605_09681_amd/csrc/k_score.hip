@@ -1,0 +1,182 @@
+// k_score.hip -- segment-wise cosine similarity of adjacent frames for dynamic
+// heads (Sec. 4.3, Eq. 3).
+//
+// Segment g of the history is compared with the same token range one frame
+// later.  Splitting every frame into units of U = min(L, F) tokens (a unit is
+// a segment when L <= F, a whole frame otherwise), each score is a sum of
+// per-(frame t, unit u) quantities:
+//   SQ[t][u]  = sum over the unit's elements of K_t^2          (t = 0..H, frame H
+//               being the first frame of the current chunk)
+//   DOT[t][u] = sum over the unit's elements of K_t * K_{t+1}   (t = 0..H-1)
+// with dot = sum DOT, na = sum SQ[t], nb = sum SQ[t+1] over the frames of the
+// segment.
+//
+// Pass 1 (score_partials_kernel) streams the cache once: a workgroup owns a
+// 256-vector column chunk of one unit of one head and walks the frames t = 0..H
+// in order, keeping the previous frame's elements in registers, so every key
+// byte is read from HBM exactly once (16-byte coalesced loads, loads of the next
+// frames in flight while the current one is reduced).  Every product is exact
+// in fp64 (a bf16*bf16 or fp32*fp32 product has at most 48 significant bits);
+// sums are fp64.  Each wave reduces its per-frame sums with shuffles and writes
+// them to the workspace.
+// Pass 2 (score_finalize_kernel) sums the partials of each segment in a fixed
+// order, forms dot / sqrt(na*nb) in fp64 (0 when na*nb == 0) and rounds once
+// to fp32 (nearest even).  The result is deterministic run to run.
+#include "fkv_internal.h"
+
+namespace fkv {
+namespace {
+
+constexpr int kThreads = kScoreThreads;
+constexpr int kWaves = kScoreWaves;
+constexpr int kDepth = 4;  // frames in flight per thread
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// Widen the 16-byte vector to fp64 elements (exact).
+template <bool F32>
+struct Vec;
+
+template <>
+struct Vec<false> {  // 8 bf16
+    static constexpr int N = 8;
+    __device__ static __forceinline__ void widen(const u32x4 &v, double *x) {
+        const uint32_t w[4] = {v[0], v[1], v[2], v[3]};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[2 * i] = (double)__uint_as_float(w[i] << 16);
+            x[2 * i + 1] = (double)__uint_as_float(w[i] & 0xffff0000u);
+        }
+    }
+};
+
+template <>
+struct Vec<true> {  // 4 fp32
+    static constexpr int N = 4;
+    __device__ static __forceinline__ void widen(const u32x4 &v, double *x) {
+        x[0] = (double)__uint_as_float(v[0]);
+        x[1] = (double)__uint_as_float(v[1]);
+        x[2] = (double)__uint_as_float(v[2]);
+        x[3] = (double)__uint_as_float(v[3]);
+    }
+};
+
+// Workspace layout: ws[(((li*(H+1) + t)*units + u)*chunks + c)*kWaves + w][2]
+// with [0] = SQ of frame t and [1] = DOT of frames (t, t+1).
+__device__ __forceinline__ int64_t ws_index(const ScoreArgs &a, int li, int t, int u, int c, int w) {
+    return ((((int64_t)li * (a.H + 1) + t) * a.units_per_frame + u) * a.chunks_per_unit + c) * kWaves + w;
+}
+
+template <bool F32>
+__global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
+    using V = Vec<F32>;
+    const int c = blockIdx.x, u = blockIdx.y, li = blockIdx.z;
+    const int h = a.heads.head[li];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int64_t v = (int64_t)c * kThreads + tid;       // vector within the unit
+    const bool active = v < a.unit_vecs;
+    const int64_t frame_vecs = a.frame_bytes / 16;
+    const int64_t off = (int64_t)u * a.unit_vecs + v;   // vector within a frame
+    const u32x4 *hist = (const u32x4 *)a.K_hist + (int64_t)h * a.cap * frame_vecs;
+    const u32x4 *cur = (const u32x4 *)a.K_cur + (int64_t)h * a.cur_vecs;
+    const int H = a.H;
+
+    auto load = [&](int t) -> u32x4 {
+        u32x4 r = u32x4{0, 0, 0, 0};
+        if (active && t <= H) {
+            const u32x4 *base = t < H ? hist + (int64_t)a.slots.slot[t] * frame_vecs : cur;
+            r = __builtin_nontemporal_load(base + off);
+        }
+        return r;
+    };
+
+    u32x4 ring[kDepth];
+#pragma unroll
+    for (int i = 0; i < kDepth; ++i) ring[i] = load(i);
+
+    double prev[V::N];
+#pragma unroll
+    for (int i = 0; i < V::N; ++i) prev[i] = 0.0;
+
+    for (int t0 = 0; t0 <= H; t0 += kDepth) {
+#pragma unroll
+        for (int i = 0; i < kDepth; ++i) {
+            const int t = t0 + i;
+            if (t > H) break;
+            double x[V::N];
+            V::widen(ring[i], x);
+            ring[i] = load(t + kDepth);
+            double sq = 0.0, dot = 0.0;
+#pragma unroll
+            for (int e = 0; e < V::N; ++e) {
+                sq = fma(x[e], x[e], sq);
+                dot = fma(prev[e], x[e], dot);
+                prev[e] = x[e];
+            }
+            sq = wave_sum(sq);
+            dot = wave_sum(dot);
+            if (lane == 0) {
+                a.ws[ws_index(a, li, t, u, c, w) * 2 + 0] = sq;
+                if (t > 0) a.ws[ws_index(a, li, t - 1, u, c, w) * 2 + 1] = dot;
+            }
+        }
+    }
+}
+
+// One thread per segment of one dynamic head.
+__global__ __launch_bounds__(kThreads) void score_finalize_kernel(ScoreArgs a) {
+    const int li = blockIdx.x;
+    const int h = a.heads.head[li];
+    const int nparts = a.chunks_per_unit * kWaves;
+    for (int g = threadIdx.x; g < a.n_seg; g += kThreads) {
+        int t0, t1, u;
+        if (a.L <= a.F) {  // one unit = one segment inside frame t0
+            t0 = g / a.units_per_frame;
+            u = g - t0 * a.units_per_frame;
+            t1 = t0 + 1;
+        } else {           // the segment spans frames [t0, t1), one unit each
+            const int m = a.L / a.F;
+            t0 = g * m;
+            t1 = min(t0 + m, a.H);
+            u = 0;
+        }
+        double dot = 0.0, na = 0.0, nb = 0.0;
+        for (int t = t0; t < t1; ++t) {
+            const double *pa = a.ws + ws_index(a, li, t, u, 0, 0) * 2;
+            const double *pb = a.ws + ws_index(a, li, t + 1, u, 0, 0) * 2;
+            for (int i = 0; i < nparts; ++i) {
+                na += pa[2 * i];
+                dot += pa[2 * i + 1];
+                nb += pb[2 * i];
+            }
+        }
+        const double prod = na * nb;
+        const double cosv = prod == 0.0 ? 0.0 : dot / sqrt(prod);
+        a.scores[(int64_t)h * a.n_seg + g] = (float)cosv;
+    }
+}
+
+}  // namespace
+
+size_t score_workspace_doubles(int n_dyn, int H, int units_per_frame, int chunks_per_unit) {
+    return (size_t)n_dyn * (H + 1) * units_per_frame * chunks_per_unit * kWaves * 2;
+}
+
+hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s) {
+    if (a.heads.n == 0 || a.H == 0) return hipSuccess;
+    dim3 grid((unsigned)a.chunks_per_unit, (unsigned)a.units_per_frame, (unsigned)a.heads.n);
+    if (f32)
+        hipLaunchKernelGGL(score_partials_kernel<true>, grid, dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(score_partials_kernel<false>, grid, dim3(kThreads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(score_finalize_kernel, dim3(a.heads.n), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace fkv

@@ -1,0 +1,78 @@
+"""One attention layer's Forcing-KV step: the four C-ABI calls in order.
+
+:class:`CompressedLayer` owns the per-layer intermediate device buffers
+(scores, kept segment ids, compressed K/V slabs, kv_len, score workspace)
+sized from the shape and budgets, and runs one AR step of one layer:
+
+1. ``fkv_score_segments``  (dynamic heads, Eq. 3 similarity)
+2. ``fkv_select_compact``  (dynamic heads, Eq. 3 BottomK + compaction)
+3. ``fkv_compress_static`` (static heads, Eq. 2)
+4. ``fkv_chunk_attention`` (all heads, Eq. 2 / Eq. 4)
+
+All four enqueue on the current torch stream; nothing synchronises.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional, Sequence
+
+import torch
+
+from . import (FKV_DYNAMIC, FKV_STATIC, fkv_chunk_attention, fkv_compress_static,
+               fkv_num_segments, fkv_score_segments, fkv_score_workspace_size,
+               fkv_select_compact, make_heads, make_shape, slab_tokens)
+
+
+class CompressedLayer:
+    def __init__(self, n_heads: int, head_dim: int, frame_tokens: int, hist_frames: int,
+                 cap_frames: int, chunk_frames: int, seg_tokens: int, dtype: str,
+                 budgets: Sequence, device="cuda", slab: Optional[int] = None):
+        self.shape = make_shape(n_heads, head_dim, frame_tokens, hist_frames, cap_frames,
+                                chunk_frames, seg_tokens, dtype)
+        self.heads = make_heads(budgets)
+        self.types = [int(h.type) for h in self.heads]
+        self.dtype = torch.bfloat16 if dtype in ("bf16", 0) else torch.float32
+        self.device = torch.device(device)
+        self.n_seg = fkv_num_segments(self.shape)
+        self.slab = slab_tokens(self.shape, self.heads) if slab is None else slab
+        self.lq = chunk_frames * frame_tokens
+        dev, dt = self.device, self.dtype
+        self.scores = torch.zeros((n_heads, self.n_seg), dtype=torch.float32, device=dev)
+        self.kept_seg = torch.full((n_heads, self.n_seg), -1, dtype=torch.int32, device=dev)
+        self.Kc = torch.zeros((n_heads, self.slab, head_dim), dtype=dt, device=dev)
+        self.Vc = torch.zeros((n_heads, self.slab, head_dim), dtype=dt, device=dev)
+        self.kv_len = torch.zeros((n_heads,), dtype=torch.int32, device=dev)
+        self.ws_bytes = fkv_score_workspace_size(self.shape, self.heads)
+        self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
+        self.scale = 1.0 / math.sqrt(head_dim)
+        self.has_static = FKV_STATIC in self.types
+        self.has_dynamic = FKV_DYNAMIC in self.types
+
+    # individual stages -------------------------------------------------------
+    def score(self, K_hist, frame_slot, K_cur):
+        fkv_score_segments(self.shape, self.heads, K_hist, frame_slot, K_cur, self.scores,
+                           self.workspace)
+
+    def select_compact(self, K_hist, V_hist, frame_slot):
+        fkv_select_compact(self.shape, self.heads, self.scores, K_hist, V_hist, frame_slot,
+                           self.kept_seg, self.Kc, self.Vc, self.kv_len)
+
+    def compress_static(self, K_hist, V_hist, frame_slot):
+        fkv_compress_static(self.shape, self.heads, K_hist, V_hist, frame_slot, self.Kc,
+                            self.Vc, self.kv_len)
+
+    def attention(self, Q, K_cur, V_cur, O, lse=None, scale: Optional[float] = None):
+        fkv_chunk_attention(self.shape, Q, self.Kc, self.Vc, self.kv_len, K_cur, V_cur,
+                            self.scale if scale is None else scale, O, lse)
+
+    # whole step --------------------------------------------------------------
+    def compress(self, K_hist, V_hist, frame_slot, K_cur):
+        if self.has_dynamic:
+            self.score(K_hist, frame_slot, K_cur)
+            self.select_compact(K_hist, V_hist, frame_slot)
+        if self.has_static:
+            self.compress_static(K_hist, V_hist, frame_slot)
+
+    def step(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse=None):
+        self.compress(K_hist, V_hist, frame_slot, K_cur)
+        self.attention(Q, K_cur, V_cur, O, lse)

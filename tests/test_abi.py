@@ -1,0 +1,166 @@
+"""The C ABI on the host: the library loads, exports every function that
+include/fkv.h declares, computes the host-side budget helpers correctly, and
+rejects invalid arguments with the documented status before any device work
+(no call here reaches a kernel launch, so no GPU is needed)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fkv.h")
+
+
+@pytest.fixture(scope="module")
+def fkv():
+    import paper_2605_09681_amd as m
+    if not os.path.exists(m.LIB_PATH):
+        from paper_2605_09681_amd import build
+        build.build()
+    m.lib()
+    return m
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fkv_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_four_entry_points():
+    names = declared_functions()
+    for n in ("fkv_compress_static", "fkv_score_segments", "fkv_select_compact", "fkv_chunk_attention"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(fkv):
+    lib = ctypes.CDLL(fkv.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} declared in fkv.h but not exported"
+    assert set(declared_functions()) == set(fkv.EXPORTED)
+
+
+def _shape(fkv, **kw):
+    base = dict(n_heads=2, head_dim=128, frame_tokens=64, hist_frames=4, cap_frames=4,
+                chunk_frames=1, seg_tokens=64, dtype="bf16")
+    base.update(kw)
+    return fkv.make_shape(**base)
+
+
+def _heads(fkv, *budgets):
+    return fkv.make_heads(budgets or (W.HeadBudget(W.STATIC, 1, 1), W.HeadBudget(W.DYNAMIC, 0, 0, 2)))
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+
+
+def _call_static(fkv, shape, heads, slab=1 << 20, slots=None, K=FAKE):
+    H = shape.hist_frames
+    sl = (ctypes.c_int32 * max(H, 1))(*(range(H) if slots is None else slots))
+    return fkv.lib().fkv_compress_static(ctypes.byref(shape), heads, K, FAKE, sl, FAKE, FAKE,
+                                         slab, FAKE, None)
+
+
+def _call_select(fkv, shape, heads, slab=1 << 20):
+    H = shape.hist_frames
+    sl = (ctypes.c_int32 * max(H, 1))(*range(H))
+    return fkv.lib().fkv_select_compact(ctypes.byref(shape), heads, FAKE, FAKE, FAKE, sl, FAKE,
+                                        FAKE, FAKE, slab, FAKE, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_heads=0), 2), (dict(n_heads=65), 2), (dict(head_dim=96), 2), (dict(frame_tokens=0), 2),
+    (dict(hist_frames=5), 2), (dict(hist_frames=-1), 2), (dict(cap_frames=300, hist_frames=4), 2),
+    (dict(chunk_frames=0), 2), (dict(seg_tokens=48), 2), (dict(seg_tokens=0), 2),
+    (dict(dtype=7), 1),
+])
+def test_bad_shapes_rejected(fkv, kw, status):
+    dt = kw.pop("dtype", None)
+    shape = _shape(fkv, **kw)
+    if dt is not None:
+        shape.dtype = dt
+    heads = _heads(fkv)
+    assert _call_static(fkv, shape, heads) == status
+    assert fkv.fkv_last_error() != ""
+
+
+def test_bad_budgets_rejected(fkv):
+    shape = _shape(fkv)
+    assert _call_static(fkv, shape, _heads(fkv, W.HeadBudget(W.STATIC, -1, 1), W.HeadBudget(W.STATIC))) == 1
+    assert _call_static(fkv, shape, _heads(fkv, W.HeadBudget(5), W.HeadBudget(W.STATIC))) == 1
+    assert _call_static(fkv, shape, _heads(fkv, W.HeadBudget(W.DYNAMIC, 0, 0, -2), W.HeadBudget(W.STATIC))) == 1
+    assert _call_static(fkv, shape, _heads(fkv, W.HeadBudget(W.DYNAMIC, 0, 0, 1, 9), W.HeadBudget(W.STATIC))) == 1
+    # per-frame selection needs segments shorter than a frame
+    assert _call_select(fkv, shape, _heads(fkv, W.HeadBudget(W.DYNAMIC, 0, 0, 1, W.SCOPE_FRAME),
+                                           W.HeadBudget(W.STATIC))) == 2
+
+
+def test_null_and_slot_errors(fkv):
+    shape = _shape(fkv)
+    heads = _heads(fkv)
+    assert fkv.lib().fkv_compress_static(None, heads, FAKE, FAKE, None, FAKE, FAKE, 100, FAKE, None) == 1
+    assert _call_static(fkv, shape, heads, K=None) == 1
+    assert _call_static(fkv, shape, heads, slots=[0, 1, 4, 2]) == 1
+    assert _call_static(fkv, shape, heads, slots=[0, -1, 2, 3]) == 1
+    assert "frame_slot" in fkv.fkv_last_error()
+
+
+def test_capacity_errors(fkv):
+    shape = _shape(fkv)
+    heads = _heads(fkv)
+    assert _call_static(fkv, shape, heads, slab=127) == 3   # static keeps 2 frames = 128 tokens
+    assert _call_select(fkv, shape, heads, slab=127) == 3   # dynamic keeps 2 segments = 128 tokens
+    assert "slab" in fkv.fkv_last_error()
+    need = fkv.fkv_score_workspace_size(shape, heads)
+    assert need > 0 and need % 256 == 0
+    sl = (ctypes.c_int32 * 4)(0, 1, 2, 3)
+    assert fkv.lib().fkv_score_segments(ctypes.byref(shape), heads, FAKE, sl, FAKE, FAKE, FAKE,
+                                        need - 1, None) == 3
+
+
+def test_attention_arg_errors(fkv):
+    shape = _shape(fkv)
+    L = fkv.lib()
+    assert L.fkv_chunk_attention(ctypes.byref(shape), FAKE, FAKE, FAKE, 10, FAKE, FAKE, FAKE,
+                                 ctypes.c_float(0.0), FAKE, None, None) == 1
+    assert L.fkv_chunk_attention(ctypes.byref(shape), FAKE, FAKE, FAKE, 10, FAKE, FAKE, FAKE,
+                                 ctypes.c_float(float("nan")), FAKE, None, None) == 1
+    assert L.fkv_chunk_attention(ctypes.byref(shape), None, FAKE, FAKE, 10, FAKE, FAKE, FAKE,
+                                 ctypes.c_float(0.1), FAKE, None, None) == 1
+    assert L.fkv_chunk_attention(ctypes.byref(shape), FAKE, FAKE, FAKE, -1, FAKE, FAKE, FAKE,
+                                 ctypes.c_float(0.1), FAKE, None, None) == 1
+
+
+def test_segment_count(fkv):
+    for H, F, L in [(21, 1560, 1560), (21, 1560, 390), (21, 1560, 4680), (20, 1560, 4680), (0, 64, 64)]:
+        assert fkv.fkv_num_segments(_shape(fkv, frame_tokens=F, hist_frames=H, cap_frames=max(H, 1),
+                                           seg_tokens=L)) == -(-H * F // L)
+
+
+def test_kept_tokens_max_matches_oracle_selection(fkv, oracle_lib):
+    """The host bound equals the largest kv_len over many score draws, and is
+    reached (only a short last segment makes kv_len data dependent)."""
+    rng = np.random.default_rng(0)
+    for H, F, L, b in [(21, 1560, 1560, W.HeadBudget(W.DYNAMIC, 1, 0, 10, 1)),
+                       (20, 1560, 4680, W.HeadBudget(W.DYNAMIC, 1, 0, 3, 1)),
+                       (7, 100, 300, W.HeadBudget(W.DYNAMIC, 0, 1, 1, 1)),
+                       (21, 1560, 390, W.HeadBudget(W.DYNAMIC, 1, 2, 2, 0)),
+                       (5, 100, 100, W.HeadBudget(W.STATIC, 1, 2)),
+                       (3, 100, 100, W.HeadBudget(W.STATIC, 2, 2))]:
+        shape = _shape(fkv, frame_tokens=F, hist_frames=H, cap_frames=H, seg_tokens=L, n_heads=1)
+        bound = fkv.fkv_kept_tokens_max(shape, fkv.make_heads([b]), 0)
+        if b.type == W.STATIC:
+            assert bound == len(oracle.static_frames(H, b.sink_frames, b.recent_frames)) * F
+            continue
+        n = -(-H * F // L)
+        seen = set()
+        for _ in range(200):
+            kept, cnt = oracle.select_head(rng.standard_normal(n).astype(np.float32), H, F, L,
+                                           b.sink_frames, b.recent_frames, b.keep_k, b.scope)
+            seen.add(sum(min(g * L + L, H * F) - g * L for g in kept[:cnt]))
+        assert max(seen) == bound
