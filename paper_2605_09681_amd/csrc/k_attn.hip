@@ -38,8 +38,9 @@
 // Global K/V rows come in through buffer loads whose per-lane offsets are loop
 // invariant; rows past the end of a source fall outside the buffer's range and
 // read as zero (the straddling tile merges both sources that way).  LDS rows
-// are padded by 16 bytes, which spreads the MFMA operand reads over all banks
-// and lets every LDS access use an immediate offset.
+// are padded (K by 16 bytes, V by 64 bytes, measured best for the 16-byte K
+// operand reads and the transpose reads of V) so the operand reads spread over
+// the banks and every LDS access uses an immediate offset.
 //
 // Work items (head, 128-row query tile) are dealt so that each XCD (blocks go
 // to the 8 XCDs round-robin) receives a contiguous range: the query tiles of a
@@ -61,13 +62,15 @@ constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw 32-bit buffer, range checke
 
 template <int D>
 struct Cfg {
-    static constexpr int RSE = D + 8;           // LDS row stride, elements
+    static constexpr int RSE = D + 8;           // K row stride in LDS (16-byte pad), elements
+    static constexpr int VRSE = D + 32;         // V row stride in LDS (64-byte pad), elements
     static constexpr int CPR = D / 8;           // 16-byte chunks per row
     static constexpr int RPP = kThreads / CPR;  // rows covered by one pass of the workgroup
     static constexpr int NV = BN / RPP;         // 16-byte vectors per thread per tile and tensor
     static constexpr int KS = D / 16;           // k-steps of S^T = K Q^T
     static constexpr int MB = D / 32;           // 32-row blocks of O^T
-    static constexpr int TILE = BN * RSE;       // elements per LDS tile
+    static constexpr int TILE = BN * RSE;       // elements per K tile
+    static constexpr int VTILE = BN * VRSE;     // elements per V tile
     static_assert(NV >= 1 && BN % RPP == 0, "tile shape");
 };
 
@@ -83,7 +86,7 @@ template <int D>
 __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     using C = Cfg<D>;
     __shared__ __attribute__((aligned(16))) uint16_t Ks[2][C::TILE];
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[2][C::TILE];
+    __shared__ __attribute__((aligned(16))) uint16_t Vs[2][C::VTILE];
 
     const int item = (blockIdx.x & 7) * a.items_per_xcd + (blockIdx.x >> 3);
     if (item >= a.n_items) return;
@@ -118,7 +121,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     // Loop-invariant per-thread load geometry: rows r0 + RPP*i, chunk c.
     const int c = tid % C::CPR, r0 = tid / C::CPR;
     const uint32_t voff = (uint32_t)(r0 * D + c * 8) * 2u;   // + i*RPP*D*2 bytes
-    const int wofs = r0 * C::RSE + c * 8;                     // + i*RPP*RSE elements
+    const int wofs = r0 * C::RSE + c * 8;                      // + i*RPP*RSE elements
+    const int vwofs = r0 * C::VRSE + c * 8;                    // + i*RPP*VRSE elements
 
     // Rows j0 .. j0+BN-1 of [hist; chunk] into registers, zeros past Lk.
     auto load_rows = [&](const uint16_t *hist, const uint16_t *chunk, int j0, u32x4 (&dst)[C::NV]) {
@@ -148,6 +152,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < C::NV; ++i) *(u32x4 *)(tile + wofs + i * C::RPP * C::RSE) = src[i];
     };
+    auto store_vrows = [&](uint16_t *tile, const u32x4 (&src)[C::NV]) {
+#pragma unroll
+        for (int i = 0; i < C::NV; ++i) *(u32x4 *)(tile + vwofs + i * C::RPP * C::VRSE) = src[i];
+    };
 
     // LDS read bases of the MFMA operands.
     // K (A of S^T): lane reads row 32*kb + l32, dims 16*kk + 8*hl.
@@ -156,7 +164,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     // points at V[4*hl + k/4 (+16t +8half)][16*(group&1) + 4*(k%4) (+32mb)] and
     // receives V[keys 16t + 8half + 4hl + 0..3][dim 32mb + l32].
     const int g16 = lane >> 4, k16 = lane & 15;
-    const int vbase = (4 * hl + (k16 >> 2)) * C::RSE + 16 * (g16 & 1) + 4 * (k16 & 3);
+    const int vbase = (4 * hl + (k16 >> 2)) * C::VRSE + 16 * (g16 & 1) + 4 * (k16 & 3);
 
     auto qk = [&](const uint16_t *ks, f32x16_t (&s)[2]) {
 #pragma unroll
@@ -229,7 +237,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
 
         // ---- LDS stores: K(it+1) and V(it) -----------------------------------
         if (it + 1 < ntiles) store_rows(Ks[(it + 1) & 1], kreg);
-        store_rows(Vs[it & 1], vreg);
+        store_vrows(Vs[it & 1], vreg);
         __syncthreads();
         if (it + 2 < ntiles) load_rows(Kc, Kq, j0 + 2 * BN, kreg);
         if (it + 1 < ntiles) load_rows(Vc, Vq, j0 + BN, vreg);
@@ -241,11 +249,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
         for (int t = 0; t < 4; ++t)
 #pragma unroll
             for (int mb = 0; mb < C::MB; ++mb) {
-                const uint16_t *p0 = vs + vbase + (16 * t) * C::RSE + 32 * mb;
+                const uint16_t *p0 = vs + vbase + (16 * t) * C::VRSE + 32 * mb;
                 const i16x4_t v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                     (__attribute__((address_space(3))) i16x4_t *)(p0));
                 const i16x4_t v2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) i16x4_t *)(p0 + 8 * C::RSE));
+                    (__attribute__((address_space(3))) i16x4_t *)(p0 + 8 * C::VRSE));
                 const bf16x8_t av = __builtin_bit_cast(
                     bf16x8_t, __builtin_shufflevector(v1, v2, 0, 1, 2, 3, 4, 5, 6, 7));
                 o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[t], o[mb], 0, 0, 0);
