@@ -98,7 +98,7 @@ struct AttnArgs {
 };
 
 constexpr int kScoreThreads = 256;
-constexpr int kAttnRowsBf16 = 128;  // query rows per attention workgroup (bf16 MFMA kernel)
+constexpr int kAttnRowsBf16 = 256;  // query rows per attention workgroup (bf16 MFMA kernel)
 constexpr int kAttnRowsF32 = 32;    // query rows per attention workgroup (fp32 kernel)
 constexpr int kScoreWaves = kScoreThreads / 64;
 

@@ -54,8 +54,9 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kThreads = 256;
-constexpr int BM = kAttnRowsBf16;  // query rows per workgroup
+constexpr int kThreads = 512;      // 8 waves: two groups of 4
+constexpr int kGroupThreads = 256; // one group stages a whole K or V tile
+constexpr int BM = kAttnRowsBf16;  // query rows per workgroup (128 per group)
 constexpr int BN = 64;             // keys per tile
 constexpr float kRescaleSlack = 8.f;  // log2 units the running max may lag behind
 constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw 32-bit buffer, range checked
@@ -63,14 +64,15 @@ constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw 32-bit buffer, range checke
 template <int D>
 struct Cfg {
     static constexpr int RSE = D + 8;           // K row stride in LDS (16-byte pad), elements
-    static constexpr int VRSE = D + 32;         // V row stride in LDS (64-byte pad), elements
+    static constexpr int TRSE = BN + 8;         // V^T row stride in LDS (16-byte pad), elements
     static constexpr int CPR = D / 8;           // 16-byte chunks per row
-    static constexpr int RPP = kThreads / CPR;  // rows covered by one pass of the workgroup
-    static constexpr int NV = BN / RPP;         // 16-byte vectors per thread per tile and tensor
+    static constexpr int RPP = kGroupThreads / CPR;  // rows one pass of a 256-thread group covers
+    static constexpr int NV = BN / RPP;              // 16-byte vectors per thread per staged tile
     static constexpr int KS = D / 16;           // k-steps of S^T = K Q^T
     static constexpr int MB = D / 32;           // 32-row blocks of O^T
     static constexpr int TILE = BN * RSE;       // elements per K tile
-    static constexpr int VTILE = BN * VRSE;     // elements per V tile
+    static constexpr int VTILE = D * TRSE;      // elements per V^T tile
+    static constexpr int VUNITS = (BN / 4) * CPR;  // (4 keys x 8 dims) units of a V tile
     static_assert(NV >= 1 && BN % RPP == 0, "tile shape");
 };
 
@@ -80,6 +82,98 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_
 
 __device__ __forceinline__ u32x4 bload(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+// Rows of the key tile starting at j0 of [hist (kvl rows); chunk (Lq rows)] into
+// registers, zeros past Lk = kvl + Lq: N 16-byte vectors at byte offsets
+// off0 + i*step within the tile.  Rows past the end of a source fall outside
+// its buffer range and read as zero; the tile straddling the history/chunk
+// boundary merges both sources that way.
+template <int D, int N>
+__device__ __forceinline__ void load_tile(const uint16_t *hist, const uint16_t *chunk, int j0, int kvl,
+                                          int Lk, int Lq, u32x4 *dst, uint32_t off0, uint32_t step) {
+    if (j0 + BN <= kvl) {
+        const auto r = rsrc(hist + (size_t)j0 * D, BN * D * 2);
+#pragma unroll
+        for (int i = 0; i < N; ++i) dst[i] = bload(r, off0 + i * step);
+    } else if (j0 >= kvl) {
+        const auto r = rsrc(chunk + (size_t)(j0 - kvl) * D, (uint32_t)(Lk - j0) * D * 2);
+#pragma unroll
+        for (int i = 0; i < N; ++i) dst[i] = bload(r, off0 + i * step);
+    } else {
+        const int nh = kvl - j0;
+        const int nc = min(BN - nh, Lq);
+        const auto rh = rsrc(hist + (size_t)j0 * D, (uint32_t)nh * D * 2);
+        const auto rc = rsrc(chunk, (uint32_t)nc * D * 2);
+        const uint32_t shift = (uint32_t)nh * D * 2;  // chunk rows start at tile row nh
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const uint32_t o = off0 + i * step;
+            // below tile row nh, o - shift wraps to a huge offset: out of range, reads 0
+            dst[i] = bload(rh, o) | bload(rc, o - shift);
+        }
+    }
+}
+
+// One MFMA block of a wave: optionally O^T += V^T P^T for one key tile (4 x MB
+// products, accumulators o[mb] cycled so consecutive products are independent),
+// then optionally S^T = K Q^T for the next tile (KS x 2 products, the two
+// accumulators interleaved).  The A operand of every product comes from LDS;
+// its reads are issued kPrefetch products ahead so their latency overlaps the
+// preceding products.
+constexpr int kPrefetch = 4;
+
+template <int D, bool PV, bool QK>
+__device__ __forceinline__ void mfma_block(const uint16_t *vs, const uint16_t *ks, int vbase, int kbase,
+                                           const bf16x8_t (&pb)[4], const bf16x8_t (&qf)[D / 16],
+                                           f32x16_t (&o)[D / 32], f32x16_t (&s)[2]) {
+    using C = Cfg<D>;
+    constexpr int NPV = PV ? 4 * C::MB : 0;
+    constexpr int NQK = QK ? 2 * C::KS : 0;
+    constexpr int NSTEP = NPV + NQK;
+    // Step order: the value products (accumulators o[mb] cycled) then the score
+    // products (accumulators s[0], s[1] alternating).
+    auto is_pv = [&](int st) { return st < NPV; };
+    auto index = [&](int st) { return st < NPV ? st : st - NPV; };
+    auto read_a = [&](int st) -> bf16x8_t {
+        const int i = index(st);
+        if (is_pv(st)) {
+            const int t = i / C::MB, mb = i % C::MB;
+            return __builtin_bit_cast(bf16x8_t, *(const u32x4 *)(vs + vbase + (32 * mb) * C::TRSE + 16 * t));
+        }
+        const int kk = i >> 1, kb = i & 1;
+        return __builtin_bit_cast(bf16x8_t, *(const u32x4 *)(ks + kbase + kb * 32 * C::RSE + kk * 16));
+    };
+    if (QK) {
+        s[0] = f32x16_t{};
+        s[1] = f32x16_t{};
+    }
+    bf16x8_t fr[kPrefetch];
+#pragma unroll
+    for (int i = 0; i < kPrefetch; ++i)
+        if (i < NSTEP) fr[i] = read_a(i);
+#pragma unroll
+    for (int st = 0; st < NSTEP; ++st) {
+        const bf16x8_t a = fr[st % kPrefetch];
+        if (st + kPrefetch < NSTEP) fr[st % kPrefetch] = read_a(st + kPrefetch);
+        const int i = index(st);
+        if (is_pv(st)) {
+            const int t = i / C::MB, mb = i % C::MB;
+            o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[t], o[mb], 0, 0, 0);
+        } else {
+            const int kk = i >> 1, kb = i & 1;
+            s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[kb], 0, 0, 0);
+        }
+    }
+    // Keep the operand reads kPrefetch products ahead: kPrefetch LDS reads,
+    // then alternate one MFMA and one LDS read.
+#pragma unroll
+    for (int i = 0; i < kPrefetch && i < NSTEP; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+    for (int st = 0; st < NSTEP; ++st) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (st + kPrefetch < NSTEP) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
 }
 
 template <int D>
@@ -94,6 +188,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     const int qt = item - h * a.n_qtiles;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int grp = wave >> 2;  // 0: leads by half a tile, 1: trails
     const int l32 = lane & 31, hl = lane >> 5;
     const int Lq = a.Lq;
 
@@ -118,88 +213,64 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     const uint16_t *Kq = (const uint16_t *)a.K_cur + (size_t)h * Lq * D;
     const uint16_t *Vq = (const uint16_t *)a.V_cur + (size_t)h * Lq * D;
 
-    // Loop-invariant per-thread load geometry: rows r0 + RPP*i, chunk c.
-    const int c = tid % C::CPR, r0 = tid / C::CPR;
-    const uint32_t voff = (uint32_t)(r0 * D + c * 8) * 2u;   // + i*RPP*D*2 bytes
+    // Loop-invariant per-thread load geometry within the thread's group of 256:
+    // rows r0 + RPP*i, chunk c (group 1 stages K tiles, group 0 V tiles).
+    const int gtid = tid & 255;
+    const int c = gtid % C::CPR, r0 = gtid / C::CPR;
+    const uint32_t voff = (uint32_t)(r0 * D + c * 8) * 2u;    // + i*RPP*D*2 bytes
     const int wofs = r0 * C::RSE + c * 8;                      // + i*RPP*RSE elements
-    const int vwofs = r0 * C::VRSE + c * 8;                    // + i*RPP*VRSE elements
+    // V staging unit of this thread: keys 4*vq .. 4*vq+3 of the tile, dims 8*vc .. 8*vc+7.
+    const int vq = gtid % (BN / 4), vc = gtid / (BN / 4);
+    const uint32_t voffv = (uint32_t)(4 * vq * D + vc * 8) * 2u;  // + r*D*2 bytes
 
-    // Rows j0 .. j0+BN-1 of [hist; chunk] into registers, zeros past Lk.
-    auto load_rows = [&](const uint16_t *hist, const uint16_t *chunk, int j0, u32x4 (&dst)[C::NV]) {
-        if (j0 + BN <= kvl) {
-            const auto r = rsrc(hist + (size_t)j0 * D, BN * D * 2);
-#pragma unroll
-            for (int i = 0; i < C::NV; ++i) dst[i] = bload(r, voff + i * C::RPP * D * 2);
-        } else if (j0 >= kvl) {
-            const auto r = rsrc(chunk + (size_t)(j0 - kvl) * D, (uint32_t)(Lk - j0) * D * 2);
-#pragma unroll
-            for (int i = 0; i < C::NV; ++i) dst[i] = bload(r, voff + i * C::RPP * D * 2);
-        } else {  // straddles the history/chunk boundary
-            const int nh = kvl - j0;
-            const int nc = min(BN - nh, Lq);
-            const auto rh = rsrc(hist + (size_t)j0 * D, (uint32_t)nh * D * 2);
-            const auto rc = rsrc(chunk, (uint32_t)nc * D * 2);
-            const uint32_t shift = (uint32_t)nh * D * 2;  // chunk rows start at tile row nh
-#pragma unroll
-            for (int i = 0; i < C::NV; ++i) {
-                const uint32_t o = voff + i * C::RPP * D * 2;
-                // below tile row nh, o - shift wraps to a huge offset: out of range, reads 0
-                dst[i] = bload(rh, o) | bload(rc, o - shift);
-            }
-        }
+    auto load_k = [&](int j0, u32x4 (&dst)[4]) {
+        load_tile<D, C::NV>(Kc, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
     };
-    auto store_rows = [&](uint16_t *tile, const u32x4 (&src)[C::NV]) {
+    auto load_v = [&](int j0, u32x4 (&dst)[4]) {
+        if (gtid < C::VUNITS) load_tile<D, 4>(Vc, Vq, j0, kvl, Lk, Lq, dst, voffv, D * 2);
+    };
+    auto store_k = [&](uint16_t *tile, const u32x4 (&src)[4]) {
 #pragma unroll
         for (int i = 0; i < C::NV; ++i) *(u32x4 *)(tile + wofs + i * C::RPP * C::RSE) = src[i];
     };
-    auto store_vrows = [&](uint16_t *tile, const u32x4 (&src)[C::NV]) {
+    // V^T tile: row d holds the tile's 64 keys; within each 16-key group the key
+    // quads are stored in the order 0, 2, 1, 3 so that the 8 keys a lane feeds to
+    // the value product (16t + 4hl + 0..3 and 16t + 8 + 4hl + 0..3) are contiguous.
+    auto store_vt = [&](uint16_t *vt, const u32x4 (&src)[4]) {
+        if (gtid < C::VUNITS) {
+            const int qi = vq & 3;
+            const int col = 16 * (vq >> 2) + 4 * (((qi & 1) << 1) | (qi >> 1));
+            uint16_t *dst = vt + (8 * vc) * C::TRSE + col;
 #pragma unroll
-        for (int i = 0; i < C::NV; ++i) *(u32x4 *)(tile + vwofs + i * C::RPP * C::VRSE) = src[i];
+            for (int e = 0; e < 4; ++e) {
+                // dims 8vc+2e (low halves) and 8vc+2e+1 (high halves) of the 4 keys
+                const uint2 lo = make_uint2((src[0][e] & 0xffffu) | (src[1][e] << 16),
+                                            (src[2][e] & 0xffffu) | (src[3][e] << 16));
+                const uint2 hi = make_uint2((src[0][e] >> 16) | (src[1][e] & 0xffff0000u),
+                                            (src[2][e] >> 16) | (src[3][e] & 0xffff0000u));
+                *(uint2 *)(dst + (2 * e) * C::TRSE) = lo;
+                *(uint2 *)(dst + (2 * e + 1) * C::TRSE) = hi;
+            }
+        }
     };
 
     // LDS read bases of the MFMA operands.
     // K (A of S^T): lane reads row 32*kb + l32, dims 16*kk + 8*hl.
     const int kbase = l32 * C::RSE + hl * 8;
-    // V^T (A of O^T) via the transpose read: within each 16-lane group, lane k
-    // points at V[4*hl + k/4 (+16t +8half)][16*(group&1) + 4*(k%4) (+32mb)] and
-    // receives V[keys 16t + 8half + 4hl + 0..3][dim 32mb + l32].
-    const int g16 = lane >> 4, k16 = lane & 15;
-    const int vbase = (4 * hl + (k16 >> 2)) * C::VRSE + 16 * (g16 & 1) + 4 * (k16 & 3);
-
-    auto qk = [&](const uint16_t *ks, f32x16_t (&s)[2]) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            s[kb] = f32x16_t{};
-#pragma unroll
-            for (int kk = 0; kk < C::KS; ++kk) {
-                const u32x4 kv = *(const u32x4 *)(ks + kbase + kb * 32 * C::RSE + kk * 16);
-                s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kv),
-                                                               qf[kk], s[kb], 0, 0, 0);
-            }
-        }
-    };
+    // V^T (A of O^T): lane reads row 32*mb + l32, keys 16t + 8hl .. +8 of the
+    // permuted V^T tile.
+    const int vbase = l32 * C::TRSE + 8 * hl;
 
     f32x16_t o[C::MB];
 #pragma unroll
     for (int mb = 0; mb < C::MB; ++mb) o[mb] = f32x16_t{};
+    f32x16_t s[2];
+    bf16x8_t pb[4];
     float m_run = -__builtin_inff();  // running max of scale*log2(e)*s (may lag by <= 8)
     float l_run = 0.f;                // this lane's share of the running sum
     const float c2 = a.scale_log2;
 
-    u32x4 kreg[C::NV], vreg[C::NV];
-    f32x16_t s[2];
-
-    // Prologue: K(0) into LDS and S(0); V(0) and K(1) in flight.
-    load_rows(Kc, Kq, 0, kreg);
-    store_rows(Ks[0], kreg);
-    load_rows(Vc, Vq, 0, vreg);
-    if (ntiles > 1) load_rows(Kc, Kq, BN, kreg);
-    __syncthreads();
-    qk(Ks[0], s);
-
-    for (int it = 0; it < ntiles; ++it) {
-        const int j0 = it * BN;
-        // ---- softmax of tile it (VALU) ------------------------------------
+    auto softmax = [&](int j0) {
         if (j0 + BN > Lk) {
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
@@ -225,7 +296,6 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
         }
         // P^T as the B operand: k-step t covers keys 16t + {4hl..4hl+3, 8+4hl..8+4hl+3},
         // i.e. accumulator entries s[t/2][8*(t%2) + j].
-        bf16x8_t pb[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t)
 #pragma unroll
@@ -234,33 +304,65 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
                 l_run += p;
                 pb[t][j] = (__bf16)p;
             }
+    };
 
-        // ---- LDS stores: K(it+1) and V(it) -----------------------------------
-        if (it + 1 < ntiles) store_rows(Ks[(it + 1) & 1], kreg);
-        store_vrows(Vs[it & 1], vreg);
-        __syncthreads();
-        if (it + 2 < ntiles) load_rows(Kc, Kq, j0 + 2 * BN, kreg);
-        if (it + 1 < ntiles) load_rows(Vc, Vq, j0 + BN, vreg);
-
-        // ---- MFMA block: O += P V(it); S = K(it+1) Q^T ------------------------
-        __builtin_amdgcn_s_setprio(1);
-        const uint16_t *vs = Vs[it & 1];
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-            for (int mb = 0; mb < C::MB; ++mb) {
-                const uint16_t *p0 = vs + vbase + (16 * t) * C::VRSE + 32 * mb;
-                const i16x4_t v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) i16x4_t *)(p0));
-                const i16x4_t v2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) i16x4_t *)(p0 + 8 * C::VRSE));
-                const bf16x8_t av = __builtin_bit_cast(
-                    bf16x8_t, __builtin_shufflevector(v1, v2, 0, 1, 2, 3, 4, 5, 6, 7));
-                o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[t], o[mb], 0, 0, 0);
-            }
-        if (it + 1 < ntiles) qk(Ks[(it + 1) & 1], s);
-        __builtin_amdgcn_s_setprio(0);
+    // Prologue: group 0 copies K(0) and K(1) into LDS, group 1 copies V(0);
+    // then group 1 fetches K(2) and group 0 fetches V(1) into registers, and
+    // group 0 computes S(0).
+    u32x4 stage[4];
+    if (grp == 0) {
+        load_k(0, stage);
+        store_k(Ks[0], stage);
+        if (ntiles > 1) {
+            load_k(BN, stage);
+            store_k(Ks[1], stage);
+        }
+        if (ntiles > 1) load_v(BN, stage);
+    } else {
+        load_v(0, stage);
+        store_vt(Vs[0], stage);
+        if (ntiles > 2) load_k(2 * BN, stage);
     }
+    __syncthreads();
+    if (grp == 0) mfma_block<D, false, true>(nullptr, Ks[0], vbase, kbase, pb, qf, o, s);
+
+    // Both groups run the same loop body -- softmax of tile j, barrier, MFMA
+    // block (P(j)V(j), then S(j+1) = K(j+1)Q^T), barrier -- with group 1 one
+    // phase behind group 0, so on every SIMD one wave's softmax overlaps the
+    // other wave's MFMA block.  In global phase terms:
+    //   phase 2j:   group 0 softmax(j)     | group 1 MFMA block of tile j-1
+    //   phase 2j+1: group 0 MFMA block j   | group 1 softmax(j)
+    // K(j) is read in phases 2j-1 and 2j from Ks[j%2]; V(j) in phases 2j+1 and
+    // 2j+2 from Vs[j%2].  Group 0 stores V(j) during its softmax(j) and fetches
+    // V(j+1); group 1 stores K(j+2) during its softmax(j) and fetches K(j+3).
+    // Every store lands in a buffer whose previous tile was last read before the
+    // preceding barrier and is first read after the next one.  The MFMA block of
+    // the last tile also runs the score product on a stale K buffer; its result
+    // is never used.  Both groups meet 2*ntiles + 1 barriers.
+    if (grp == 1) {
+        mfma_block<D, false, true>(nullptr, Ks[0], vbase, kbase, pb, qf, o, s);
+        __syncthreads();
+    }
+    // Let every outstanding load (the Q fragments included) land once here, so
+    // the loop's score products carry no wait on the staging loads in flight.
+    __builtin_amdgcn_s_waitcnt(0);
+    for (int it = 0; it < ntiles; ++it) {
+        const int j0 = it * BN;
+        softmax(j0);
+        if (grp == 0) {
+            if (it >= 1) store_vt(Vs[it & 1], stage);
+            if (it >= 1 && it + 1 < ntiles) load_v(j0 + BN, stage);
+        } else {
+            if (it + 2 < ntiles) store_k(Ks[it & 1], stage);
+            if (it + 3 < ntiles) load_k(j0 + 3 * BN, stage);
+        }
+        __syncthreads();
+        __builtin_amdgcn_s_setprio(1);
+        mfma_block<D, true, true>(Vs[it & 1], Ks[(it + 1) & 1], vbase, kbase, pb, qf, o, s);
+        __builtin_amdgcn_s_setprio(0);
+        __syncthreads();
+    }
+    if (grp == 0) __syncthreads();
 
     const float l_tot = l_run + __shfl_xor(l_run, 32);
     const float inv = 1.f / l_tot;
