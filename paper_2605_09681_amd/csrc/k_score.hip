@@ -17,8 +17,8 @@
 // byte is read from HBM exactly once (16-byte coalesced loads, loads of the next
 // frames in flight while the current one is reduced).  Every product is exact
 // in fp64 (a bf16*bf16 or fp32*fp32 product has at most 48 significant bits);
-// sums are fp64.  Each wave reduces its per-frame sums with shuffles and writes
-// them to the workspace.
+// sums are fp64.  Each wave reduces its per-frame sums with DPP row operations
+// and writes them to the workspace.
 // Pass 2 (score_finalize_kernel) sums the partials of each segment in a fixed
 // order, forms dot / sqrt(na*nb) in fp64 (0 when na*nb == 0) and rounds once
 // to fp32 (nearest even).  The result is deterministic run to run.
@@ -29,12 +29,29 @@ namespace {
 
 constexpr int kThreads = kScoreThreads;
 constexpr int kWaves = kScoreWaves;
-constexpr int kDepth = 4;  // frames in flight per thread
+constexpr int kDepth = 8;  // frames in flight per thread
 
+// One DPP step on a double (both 32-bit halves moved with the same control);
+// lanes without a source, or outside row_mask, contribute 0.
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ double dpp_d(double v) {
+    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, ROW_MASK, 0xF, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, ROW_MASK, 0xF, true);
+    return __hiloint2double(hi, lo);
+}
+
+// Sum over the 64 lanes of a wave, in a fixed order: inclusive scans inside each
+// 16-lane row (row_shr 1, 2, 4, 8), then row 0's total into row 1 and row 2's
+// into row 3 (row_bcast:15), then rows 0+1 into rows 2 and 3 (row_bcast:31).
+// Lane 63 ends with the total.  VALU only (no LDS crossbar traffic).
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    return v;
+    v += dpp_d<0x111>(v);
+    v += dpp_d<0x112>(v);
+    v += dpp_d<0x114>(v);
+    v += dpp_d<0x118>(v);
+    v += dpp_d<0x142, 0xA>(v);
+    v += dpp_d<0x143, 0xC>(v);
+    return v;  // valid in lane 63
 }
 
 // Widen the 16-byte vector to fp64 elements (exact).
@@ -119,7 +136,7 @@ __global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
             }
             sq = wave_sum(sq);
             dot = wave_sum(dot);
-            if (lane == 0) {
+            if (lane == 63) {
                 a.ws[ws_index(a, li, t, u, c, w) * 2 + 0] = sq;
                 if (t > 0) a.ws[ws_index(a, li, t - 1, u, c, w) * 2 + 1] = dot;
             }
@@ -127,35 +144,51 @@ __global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
     }
 }
 
-// One thread per segment of one dynamic head.
+// One workgroup per (segment, dynamic head): every thread sums a strided slice
+// of the segment's partials, then a fixed-order tree over the workgroup; the
+// result does not depend on timing.
 __global__ __launch_bounds__(kThreads) void score_finalize_kernel(ScoreArgs a) {
-    const int li = blockIdx.x;
+    __shared__ double red[3][kThreads];
+    const int g = blockIdx.x, li = blockIdx.y;
     const int h = a.heads.head[li];
+    const int tid = threadIdx.x;
     const int nparts = a.chunks_per_unit * kWaves;
-    for (int g = threadIdx.x; g < a.n_seg; g += kThreads) {
-        int t0, t1, u;
-        if (a.L <= a.F) {  // one unit = one segment inside frame t0
-            t0 = g / a.units_per_frame;
-            u = g - t0 * a.units_per_frame;
-            t1 = t0 + 1;
-        } else {           // the segment spans frames [t0, t1), one unit each
-            const int m = a.L / a.F;
-            t0 = g * m;
-            t1 = min(t0 + m, a.H);
-            u = 0;
+    int t0, t1, u;
+    if (a.L <= a.F) {  // one unit = one segment inside frame t0
+        t0 = g / a.units_per_frame;
+        u = g - t0 * a.units_per_frame;
+        t1 = t0 + 1;
+    } else {           // the segment spans frames [t0, t1), one unit each
+        const int m = a.L / a.F;
+        t0 = g * m;
+        t1 = min(t0 + m, a.H);
+        u = 0;
+    }
+    const int n = (t1 - t0) * nparts;
+    double dot = 0.0, na = 0.0, nb = 0.0;
+    for (int i = tid; i < n; i += kThreads) {
+        const int t = t0 + i / nparts, k = i % nparts;
+        const double *pa = a.ws + ws_index(a, li, t, u, 0, 0) * 2;
+        const double *pb = a.ws + ws_index(a, li, t + 1, u, 0, 0) * 2;
+        na += pa[2 * k];
+        dot += pa[2 * k + 1];
+        nb += pb[2 * k];
+    }
+    red[0][tid] = dot;
+    red[1][tid] = na;
+    red[2][tid] = nb;
+    __syncthreads();
+    for (int w = kThreads / 2; w > 0; w >>= 1) {
+        if (tid < w) {
+            red[0][tid] += red[0][tid + w];
+            red[1][tid] += red[1][tid + w];
+            red[2][tid] += red[2][tid + w];
         }
-        double dot = 0.0, na = 0.0, nb = 0.0;
-        for (int t = t0; t < t1; ++t) {
-            const double *pa = a.ws + ws_index(a, li, t, u, 0, 0) * 2;
-            const double *pb = a.ws + ws_index(a, li, t + 1, u, 0, 0) * 2;
-            for (int i = 0; i < nparts; ++i) {
-                na += pa[2 * i];
-                dot += pa[2 * i + 1];
-                nb += pb[2 * i];
-            }
-        }
-        const double prod = na * nb;
-        const double cosv = prod == 0.0 ? 0.0 : dot / sqrt(prod);
+        __syncthreads();
+    }
+    if (tid == 0) {
+        const double prod = red[1][0] * red[2][0];
+        const double cosv = prod == 0.0 ? 0.0 : red[0][0] / sqrt(prod);
         a.scores[(int64_t)h * a.n_seg + g] = (float)cosv;
     }
 }
@@ -175,7 +208,7 @@ hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s) {
         hipLaunchKernelGGL(score_partials_kernel<false>, grid, dim3(kThreads), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(score_finalize_kernel, dim3(a.heads.n), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(score_finalize_kernel, dim3(a.n_seg, a.heads.n), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
