@@ -39,15 +39,31 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=100)
     p.add_argument("--resolution", default="480p", choices=["480p", "1080p"])
     p.add_argument("--copies", type=int, default=4, help="independent layer buffers rotated per step")
-    p.add_argument("--cpu-rows", type=int, default=1024, help="query rows per head in the CPU oracle sample")
+    p.add_argument("--cpu-rows", type=int, default=4680,
+                   help="query rows per head in the CPU oracle sample (4680 = every row at 480P)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "attention_traffic.json"),
                    help="HBM bytes per attention launch measured with rocprofv3 counters")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only run a plain 256 MiB device-to-device copy three times (the known-size "
+                        "kernel that FETCH_SIZE / WRITE_SIZE are scaled by) and exit")
     return p.parse_args()
+
+
+def copy_calibration():
+    import torch
+    n = 256 << 20
+    a = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n, "launches": 3}), flush=True)
 
 
 def to_dev(a, dtype):
@@ -95,6 +111,9 @@ def main():
               "the Forcing-KV hot path shards by head with no exchange, so N GPUs run N "
               "independent copies of this step.", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     import numpy as np
     import torch
