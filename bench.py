@@ -46,6 +46,8 @@ def parse():
     p.add_argument("--cpu-rows", type=int, default=4680,
                    help="query rows per head in the CPU oracle sample (4680 = every row at 480P)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--schedule", default="balanced", choices=["balanced", "per-item"],
+                   help="attention work schedule (balanced needs the attention workspace)")
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "attention_traffic.json"),
                    help="HBM bytes per attention launch measured with rocprofv3 counters")
     p.add_argument("--copy-calibration", action="store_true",
@@ -135,7 +137,7 @@ def main():
         bufs.append(b)
         layers.append(CompressedLayer(cfg.n_heads, cfg.head_dim, cfg.frame_tokens, cfg.hist_frames,
                                       cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype,
-                                      cfg.heads))
+                                      cfg.heads, balanced=args.schedule == "balanced"))
     slots = x.frame_slot
     stream = torch.cuda.current_stream()
 
@@ -212,6 +214,7 @@ def main():
                          f"(sink 1 + 10 of 20 frame segments)"),
             "kv_len": kv_len.tolist(),
             "rotating_copies": args.copies,
+            "attention_schedule": args.schedule,
         },
         "roofline": {
             "kernel": "attn_bf16_kernel<128> (fkv_chunk_attention)",

@@ -32,8 +32,8 @@
  * Streams and ownership: every call validates its arguments on the host,
  * then enqueues kernels on `stream` (a hipStream_t, NULL = default stream)
  * and returns without synchronising; outputs are valid once the stream has
- * run them.  The caller owns every buffer; the library allocates no device
- * memory and keeps no pointer after a call returns.  K_hist and V_hist are
+ * run them.  The caller owns every buffer, workspaces included; the library
+ * allocates no device memory and keeps no pointer after a call returns.  K_hist and V_hist are
  * only read: dynamic heads keep their whole history for later similarity
  * scoring (Sec. 5.2), so compaction never modifies the cache.
  *
@@ -159,6 +159,13 @@ fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads,
                               int32_t *kept_seg, void *Kc, void *Vc, int32_t slab,
                               int32_t *kv_len, void *stream);
 
+/* Device workspace fkv_chunk_attention takes for its balanced schedule on the
+ * CURRENT device (hipGetDevice): 2 x the device's compute units, rounded down
+ * to a multiple of 8, partial-result slots of 256 rows x (head_dim + 2) floats
+ * (about 68 MB for head_dim 128 on a 256-CU device).  0 for FKV_F32, which has
+ * no balanced schedule.  FKV_ERR_DEVICE if the device cannot be queried. */
+fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes);
+
 /* Chunk attention over the compressed cache (Eq. 2 for static heads, Eq. 4
  * for dynamic heads).  For every head h and query row r < C*F, with keys
  * [Kc[h][0:n]; K_cur[h]] and values [Vc[h][0:n]; V_cur[h]], n = kv_len[h]
@@ -168,12 +175,23 @@ fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads,
  * probabilities rounded to bf16 for the value product, output normalised and
  * rounded to bf16.  fp32: all fp32.  lse (nullable, float [n_heads][C*F])
  * receives the natural-log normaliser log(sum exp(scale*q.k)).  scale must be
- * positive and finite (1/sqrt(d) is the usual choice). */
+ * positive and finite (1/sqrt(d) is the usual choice).
+ *
+ * Work schedule (bf16): with workspace == NULL every (head, 256-row query
+ * tile) is one workgroup; heads with longer caches then finish last.  With a
+ * device workspace of at least fkv_attention_workspace_size bytes (contents
+ * need no initialisation) the key tiles of all heads and query tiles are split
+ * evenly over one workgroup per compute unit, and tiles cut by a split are
+ * combined by a second kernel on the same stream (FKV_ERR_CAPACITY if the
+ * workspace is smaller).  Both schedules compute the same function; rounding
+ * may differ in the last bit.  fp32 ignores the workspace.  Two calls that
+ * share a workspace must be ordered by the caller. */
 fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q,
                                const void *Kc, const void *Vc, int32_t slab,
                                const int32_t *kv_len, const void *K_cur,
                                const void *V_cur, float scale, void *O,
-                               float *lse, void *stream);
+                               float *lse, void *workspace, size_t workspace_bytes,
+                               void *stream);
 
 /* Message describing the calling thread's last non-OK status ("" if none). */
 const char *fkv_last_error(void);

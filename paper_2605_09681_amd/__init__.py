@@ -33,7 +33,7 @@ FKV_MAX_HEADS, FKV_MAX_FRAMES, FKV_MAX_SEGMENTS = 64, 256, 4096
 
 EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_score_workspace_size", "fkv_score_segments", "fkv_select_compact",
-            "fkv_chunk_attention", "fkv_last_error")
+            "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_last_error")
 
 
 class FkvLibraryMissing(RuntimeError):
@@ -85,7 +85,9 @@ def lib():
         L.fkv_score_segments.restype = ctypes.c_int
         L.fkv_select_compact.argtypes = [S, Hd, P, P, P, P, P, P, P, I32, P, P]
         L.fkv_select_compact.restype = ctypes.c_int
-        L.fkv_chunk_attention.argtypes = [S, P, P, P, I32, P, P, P, F, P, P, P]
+        L.fkv_attention_workspace_size.argtypes = [S, ctypes.POINTER(SZ)]
+        L.fkv_attention_workspace_size.restype = ctypes.c_int
+        L.fkv_chunk_attention.argtypes = [S, P, P, P, I32, P, P, P, F, P, P, P, SZ, P]
         L.fkv_chunk_attention.restype = ctypes.c_int
         L.fkv_last_error.argtypes = []
         L.fkv_last_error.restype = ctypes.c_char_p
@@ -233,8 +235,18 @@ def fkv_select_compact(shape: fkv_shape, heads, scores, K_hist, V_hist, frame_sl
                                     int(slab), kl, _stream(stream)))
 
 
+def fkv_attention_workspace_size(shape: fkv_shape) -> int:
+    """Bytes of the balanced-schedule workspace on the current device."""
+    out = ctypes.c_size_t(0)
+    _raise(lib().fkv_attention_workspace_size(ctypes.byref(shape), ctypes.byref(out)))
+    return int(out.value)
+
+
 def fkv_chunk_attention(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, scale: float, O,
-                        lse: Optional[torch.Tensor] = None, stream=None):
+                        lse: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                        stream=None):
+    """``workspace`` (uint8 device tensor of fkv_attention_workspace_size bytes)
+    selects the balanced schedule; None runs one workgroup per query tile."""
     dt = _torch_dtype(shape)
     chunk = (shape.n_heads, _lq(shape), shape.head_dim)
     slab = Kc.shape[1] if Kc.dim() == 3 else -1
@@ -245,8 +257,11 @@ def fkv_chunk_attention(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, scale
     kq, vq = _check(K_cur, "K_cur", dt, chunk), _check(V_cur, "V_cur", dt, chunk)
     o = _check(O, "O", dt, chunk)
     ls = None if lse is None else _check(lse, "lse", torch.float32, (shape.n_heads, _lq(shape)))
+    ws, nws = None, 0
+    if workspace is not None:
+        ws, nws = _check(workspace, "workspace", torch.uint8), workspace.numel()
     _raise(lib().fkv_chunk_attention(ctypes.byref(shape), q, kc, vc, int(slab), kl, kq, vq,
-                                     ctypes.c_float(scale), o, ls, _stream(stream)))
+                                     ctypes.c_float(scale), o, ls, ws, nws, _stream(stream)))
 
 
 def fkv_last_error() -> str:

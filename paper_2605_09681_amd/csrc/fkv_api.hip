@@ -166,6 +166,25 @@ fkv_status device_status(hipError_t e, const char *what) {
 template <typename T>
 T *as(void *p) { return (T *)p; }
 
+// Workgroups of the balanced attention schedule on the current device: its
+// compute-unit count rounded down to a multiple of 8 (one workgroup fills a CU).
+fkv_status balanced_blocks(int *blocks) {
+    static int cached[64];  // per device id, 0 = not queried yet
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(FKV_ERR_DEVICE, "hipGetDevice: %s", hipGetErrorString(e));
+    int n = (dev >= 0 && dev < 64) ? __atomic_load_n(&cached[dev], __ATOMIC_RELAXED) : 0;
+    if (n == 0) {
+        int cus = 0;
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return fail(FKV_ERR_DEVICE, "hipDeviceGetAttribute: %s", hipGetErrorString(e));
+        n = std::max(8, cus / 8 * 8);
+        if (dev >= 0 && dev < 64) __atomic_store_n(&cached[dev], n, __ATOMIC_RELAXED);
+    }
+    *blocks = n;
+    return FKV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -377,15 +396,36 @@ fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads, con
                          "fkv_select_compact copy launch");
 }
 
+fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if (!bytes) return fail(FKV_ERR_ARG, "bytes is NULL");
+    *bytes = 0;
+    if (shape->dtype != FKV_BF16) return ok();
+    int blocks = 0;
+    if ((st = balanced_blocks(&blocks)) != FKV_OK) return st;
+    *bytes = 2 * (size_t)blocks * fkv::attention_part_bytes(shape->head_dim);
+    return ok();
+}
+
 fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q, const void *Kc, const void *Vc,
                                int32_t slab, const int32_t *kv_len, const void *K_cur,
-                               const void *V_cur, float scale, void *O, float *lse, void *stream) {
+                               const void *V_cur, float scale, void *O, float *lse, void *workspace,
+                               size_t workspace_bytes, void *stream) {
     fkv_status st;
     if ((st = check_shape(shape)) != FKV_OK) return st;
     if (!Q || !K_cur || !V_cur || !O || !kv_len) return fail(FKV_ERR_ARG, "NULL tensor pointer");
     if (slab < 0) return fail(FKV_ERR_ARG, "slab %d < 0", slab);
     if (slab > 0 && (!Kc || !Vc)) return fail(FKV_ERR_ARG, "NULL Kc/Vc with slab %d", slab);
     if (!(scale > 0.f) || !isfinite(scale)) return fail(FKV_ERR_ARG, "scale %g must be positive and finite", (double)scale);
+    const bool bf16 = shape->dtype == FKV_BF16;
+    int blocks = 0;
+    if (bf16 && workspace) {
+        if ((st = balanced_blocks(&blocks)) != FKV_OK) return st;
+        const size_t need = 2 * (size_t)blocks * fkv::attention_part_bytes(shape->head_dim);
+        if (workspace_bytes < need)
+            return fail(FKV_ERR_CAPACITY, "attention workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    }
 
     fkv::AttnArgs a;
     memset(&a, 0, sizeof a);
@@ -402,11 +442,12 @@ fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q, const void
     a.Lq = shape->chunk_frames * shape->frame_tokens;
     a.scale = scale;
     a.scale_log2 = scale * 1.4426950408889634f;
-    const bool bf16 = shape->dtype == FKV_BF16;
     const int rows = bf16 ? fkv::kAttnRowsBf16 : fkv::kAttnRowsF32;
     a.n_qtiles = (a.Lq + rows - 1) / rows;
     a.n_items = a.n_heads * a.n_qtiles;
     a.items_per_xcd = (a.n_items + 7) / 8;
+    a.n_blocks = blocks;
+    a.part = (float *)workspace;
     (void)hipGetLastError();
     hipError_t e = bf16 ? fkv::launch_attention_bf16(a, shape->head_dim, (hipStream_t)stream)
                         : fkv::launch_attention_f32(a, shape->head_dim, (hipStream_t)stream);

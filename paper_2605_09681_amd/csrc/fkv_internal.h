@@ -93,6 +93,8 @@ struct AttnArgs {
     int32_t n_qtiles;               // ceil(Lq / BM)
     int32_t n_items;                // n_heads * n_qtiles
     int32_t items_per_xcd;          // ceil(n_items / 8)
+    int32_t n_blocks;               // balanced schedule: workgroups (multiple of 8); 0 = one per item
+    float *part;                    // balanced schedule: 2 * n_blocks partial-result slots
     float scale;                    // softmax scale
     float scale_log2;               // scale * log2(e)
 };
@@ -109,6 +111,7 @@ hipError_t launch_dyn_copy(const DynCopyArgs &a, int max_pieces, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, hipStream_t s);
 hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s);
 hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s);
+size_t attention_part_bytes(int head_dim);  // bytes of one partial-result slot (bf16 kernel)
 hipError_t launch_attention_f32(const AttnArgs &a, int head_dim, hipStream_t s);
 
 }  // namespace fkv

@@ -7,44 +7,40 @@
 // ragged (it comes from the device-side kv_len), and one key tile may straddle
 // the history/chunk boundary.
 //
-// Workgroup = 4 waves = 128 query rows of one head (32 per wave); two
-// workgroups share a CU.  Keys are processed in tiles of 64.  Per wave and
-// tile, with v_mfma_f32_32x32x16_bf16:
-//   S^T = K . Q^T   (A = K rows from LDS, B = the wave's Q rows, held in VGPRs
-//                    for the whole kernel), 2 x (d/16) MFMAs;
+// Workgroup = 8 waves = 256 query rows of one head (32 per wave), in two
+// groups of four waves; one workgroup fills a CU.  Keys are processed in tiles
+// of 64.  Per wave and tile, with v_mfma_f32_32x32x16_bf16:
+//   S^T = K . Q^T   (A = K rows from LDS, B = the wave's Q rows, held in VGPRs),
+//                   2 x (d/16) MFMAs;
 //   online softmax in fp32 (exp2 with the scale folded into log2 units);
-//   O^T += V^T . P^T (A = V^T read from the row-major V tile with the gfx950
-//                    LDS transpose read, B = P taken straight from the S^T
-//                    accumulators, rounded to bf16), 4 x (d/32) MFMAs.
+//   O^T += V^T . P^T (A = rows of a V^T tile in LDS, B = P taken straight from
+//                    the S^T accumulators, rounded to bf16), 4 x (d/32) MFMAs.
 // Computing S transposed makes each lane own one query column, so P needs no
 // data movement between the two products: in the 32x32 accumulator layout a
 // lane holds 16 keys of its query, which are exactly the 8-element k-slices the
 // B operand of the value product takes (any consistent permutation of the
-// contraction index is allowed; V^T is read with the same permutation).  Row
-// maxima need one cross-lane exchange (lanes l and l^32 share a query).
+// contraction index is allowed; the V^T tile is stored with the same
+// permutation).  Row maxima need one cross-lane exchange (lanes l and l^32
+// share a query).  Both operands are read from LDS with 16-byte reads; V is
+// transposed on its way into LDS (measured faster than the LDS transpose
+// reads).
 //
-// Pipeline (one barrier per tile): iteration j runs the softmax of tile j on
-// the VALU, stores K of tile j+1 and V of tile j (fetched one iteration
-// earlier) into LDS, meets the barrier, issues the global loads of K(j+2) and
-// V(j+1), then runs one contiguous MFMA block at raised wave priority: the
-// value product of tile j followed by the score product of tile j+1.  The two
-// workgroups on a CU are not synchronised with each other, so one's softmax
-// overlaps the other's MFMA block.  K and V are double-buffered separately.
-//
-// The running max is only moved when a tile's max exceeds it by more than 8
-// (log2 units): probabilities then stay below 2^8 and the accumulator rescale
-// is skipped for most tiles; the final normalisation is exact either way.
+// The two wave groups run the same loop one phase apart (see attn_segment), so
+// on every SIMD one wave's softmax overlaps the other wave's MFMA block -- VALU
+// and MFMA work of two waves overlap well, that of one wave much less.  The
+// running max only moves when a tile's max exceeds it by more than 8 (log2
+// units): probabilities stay below 2^8 and the accumulator rescale is skipped
+// for most tiles; the final normalisation is exact either way.
 //
 // Global K/V rows come in through buffer loads whose per-lane offsets are loop
 // invariant; rows past the end of a source fall outside the buffer's range and
-// read as zero (the straddling tile merges both sources that way).  LDS rows
-// are padded (K by 16 bytes, V by 64 bytes, measured best for the 16-byte K
-// operand reads and the transpose reads of V) so the operand reads spread over
-// the banks and every LDS access uses an immediate offset.
+// read as zero (the straddling tile merges both sources that way).
 //
-// Work items (head, 128-row query tile) are dealt so that each XCD (blocks go
-// to the 8 XCDs round-robin) receives a contiguous range: the query tiles of a
-// head then share that XCD's L2 while they sweep the same K/V.
+// Schedules: one workgroup per (head, query tile), or the balanced schedule
+// (Schedule below) that splits the key tiles of all items evenly over one
+// workgroup per CU and merges split items in a second kernel.  Heads with
+// longer caches make the per-item schedule uneven (at 480P a dynamic head has
+// 342 key tiles per query tile, a static head 245, on 228 items for 256 CUs).
 #include "fkv_internal.h"
 
 namespace fkv {
@@ -176,21 +172,61 @@ __device__ __forceinline__ void mfma_block(const uint16_t *vs, const uint16_t *k
     }
 }
 
+// Number of key tiles of head h: [Kc[h][0:kv_len]; K_cur[h]] in tiles of BN.
+__device__ __forceinline__ int head_kvl(const AttnArgs &a, int h) {
+    const int kvl = a.kv_len[h];
+    return kvl < 0 ? 0 : (kvl > a.slab ? (int)a.slab : kvl);
+}
+__device__ __forceinline__ int head_tiles(const AttnArgs &a, int h) {
+    return (head_kvl(a, h) + a.Lq + BN - 1) / BN;
+}
+
+// Balanced schedule.  Work item i = (head h, query tile qt), h-major, has
+// T_h key tiles; concatenating all items gives one sequence of `total` tiles,
+// which G = min(n_blocks, total) workgroups split into equal contiguous ranges:
+// workgroup r takes tiles [r*total/G, (r+1)*total/G).  An item cut by a range
+// boundary is computed in parts whose unnormalised results are combined by
+// attn_merge_kernel.  Both kernels derive the same schedule from kv_len.
+struct Schedule {
+    int64_t total;
+    int G;
+    __device__ __forceinline__ int64_t start(int r) const { return (int64_t)r * total / G; }
+    // workgroup whose range holds tile x: the largest r with start(r) <= x
+    __device__ __forceinline__ int owner(int64_t x) const { return (int)(((x + 1) * G - 1) / total); }
+};
+
+__device__ __forceinline__ Schedule make_schedule(const AttnArgs &a) {
+    int64_t total = 0;
+    for (int h = 0; h < a.n_heads; ++h) total += (int64_t)a.n_qtiles * head_tiles(a, h);
+    Schedule sc;
+    sc.total = total;
+    sc.G = (int)(total < a.n_blocks ? total : a.n_blocks);
+    return sc;
+}
+
+// Partial result of one part of an item, in a slot of BM*(D+2) floats: the
+// unnormalised O^T accumulators exactly as the waves hold them (float4 index
+// ((wave*MB + mb)*4 + g)*64 + lane), then the running max m (log2 units) of
+// the BM rows, then their probability sums l.
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
+__device__ __forceinline__ size_t slot_floats() { return (size_t)BM * (D + 2); }
+
+// One segment: positions [t0, t1) of item (h, qt), where position j is key
+// tile (j + rot) mod T of the item's T tiles (the order of key tiles does not
+// change the result beyond rounding).  slot == nullptr means the segment is the
+// whole item and the normalised output (and lse) is written; otherwise the
+// partial result goes to the slot.  Uses every thread of the workgroup and
+// leaves no LDS read pending.
+template <int D>
+__device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2][Cfg<D>::TILE],
+                                             uint16_t (&Vs)[2][Cfg<D>::VTILE], int h, int qt, int t0,
+                                             int t1, int rot, float *slot) {
     using C = Cfg<D>;
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][C::TILE];
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[2][C::VTILE];
-
-    const int item = (blockIdx.x & 7) * a.items_per_xcd + (blockIdx.x >> 3);
-    if (item >= a.n_items) return;
-    const int h = item / a.n_qtiles;
-    const int qt = item - h * a.n_qtiles;
-
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int grp = wave >> 2;  // 0: leads by half a tile, 1: trails
     const int l32 = lane & 31, hl = lane >> 5;
     const int Lq = a.Lq;
+    const int n = t1 - t0;       // >= 1
 
     // The wave's 32 query rows, in the B-operand layout: lane holds row l32,
     // dims [16*kk + 8*hl, +8).
@@ -204,17 +240,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
         qf[kk] = __builtin_bit_cast(bf16x8_t, v);
     }
 
-    int kvl = a.kv_len[h];
-    kvl = kvl < 0 ? 0 : (kvl > a.slab ? (int)a.slab : kvl);
+    const int kvl = head_kvl(a, h);
     const int Lk = kvl + Lq;
-    const int ntiles = (Lk + BN - 1) / BN;
     const uint16_t *Kc = (const uint16_t *)a.Kc + (size_t)h * a.slab * D;
     const uint16_t *Vc = (const uint16_t *)a.Vc + (size_t)h * a.slab * D;
     const uint16_t *Kq = (const uint16_t *)a.K_cur + (size_t)h * Lq * D;
     const uint16_t *Vq = (const uint16_t *)a.V_cur + (size_t)h * Lq * D;
 
     // Loop-invariant per-thread load geometry within the thread's group of 256:
-    // rows r0 + RPP*i, chunk c (group 1 stages K tiles, group 0 V tiles).
+    // rows r0 + RPP*i, chunk c (group 0 stages K tiles, group 1 V tiles).
     const int gtid = tid & 255;
     const int c = gtid % C::CPR, r0 = gtid / C::CPR;
     const uint32_t voff = (uint32_t)(r0 * D + c * 8) * 2u;    // + i*RPP*D*2 bytes
@@ -223,6 +257,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     const int vq = gtid % (BN / 4), vc = gtid / (BN / 4);
     const uint32_t voffv = (uint32_t)(4 * vq * D + vc * 8) * 2u;  // + r*D*2 bytes
 
+    // first key of the segment's tile j
+    const int T = (Lk + BN - 1) / BN;
+    const int kt0 = (t0 + rot) % T;
+    auto tile0 = [&](int j) {
+        const int k = kt0 + j;
+        return (k >= T ? k - T : k) * BN;
+    };
     auto load_k = [&](int j0, u32x4 (&dst)[4]) {
         load_tile<D, C::NV>(Kc, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
     };
@@ -311,17 +352,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     // group 0 computes S(0).
     u32x4 stage[4];
     if (grp == 0) {
-        load_k(0, stage);
+        load_k(tile0(0), stage);
         store_k(Ks[0], stage);
-        if (ntiles > 1) {
-            load_k(BN, stage);
+        if (n > 1) {
+            load_k(tile0(1), stage);
             store_k(Ks[1], stage);
         }
-        if (ntiles > 1) load_v(BN, stage);
+        if (n > 1) load_v(tile0(1), stage);
     } else {
-        load_v(0, stage);
+        load_v(tile0(0), stage);
         store_vt(Vs[0], stage);
-        if (ntiles > 2) load_k(2 * BN, stage);
+        if (n > 2) load_k(tile0(2), stage);
     }
     __syncthreads();
     if (grp == 0) mfma_block<D, false, true>(nullptr, Ks[0], vbase, kbase, pb, qf, o, s);
@@ -338,7 +379,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     // Every store lands in a buffer whose previous tile was last read before the
     // preceding barrier and is first read after the next one.  The MFMA block of
     // the last tile also runs the score product on a stale K buffer; its result
-    // is never used.  Both groups meet 2*ntiles + 1 barriers.
+    // is never used.  Both groups meet 2*n + 1 barriers, the last one after
+    // every LDS read of the segment.
     if (grp == 1) {
         mfma_block<D, false, true>(nullptr, Ks[0], vbase, kbase, pb, qf, o, s);
         __syncthreads();
@@ -346,15 +388,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     // Let every outstanding load (the Q fragments included) land once here, so
     // the loop's score products carry no wait on the staging loads in flight.
     __builtin_amdgcn_s_waitcnt(0);
-    for (int it = 0; it < ntiles; ++it) {
-        const int j0 = it * BN;
+    for (int it = 0; it < n; ++it) {
+        const int j0 = tile0(it);
         softmax(j0);
         if (grp == 0) {
             if (it >= 1) store_vt(Vs[it & 1], stage);
-            if (it >= 1 && it + 1 < ntiles) load_v(j0 + BN, stage);
+            if (it >= 1 && it + 1 < n) load_v(tile0(it + 1), stage);
         } else {
-            if (it + 2 < ntiles) store_k(Ks[it & 1], stage);
-            if (it + 3 < ntiles) load_k(j0 + 3 * BN, stage);
+            if (it + 2 < n) store_k(Ks[it & 1], stage);
+            if (it + 3 < n) load_k(tile0(it + 3), stage);
         }
         __syncthreads();
         __builtin_amdgcn_s_setprio(1);
@@ -365,6 +407,20 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     if (grp == 0) __syncthreads();
 
     const float l_tot = l_run + __shfl_xor(l_run, 32);
+    if (slot) {
+        float4 *op = (float4 *)slot;
+#pragma unroll
+        for (int mb = 0; mb < C::MB; ++mb)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                op[((wave * C::MB + mb) * 4 + g) * 64 + lane] =
+                    make_float4(o[mb][4 * g], o[mb][4 * g + 1], o[mb][4 * g + 2], o[mb][4 * g + 3]);
+        if (hl == 0) {
+            slot[BM * D + wave * 32 + l32] = m_run;
+            slot[BM * D + BM + wave * 32 + l32] = l_tot;
+        }
+        return;
+    }
     const float inv = 1.f / l_tot;
     if (qok) {
         uint16_t *Oh = (uint16_t *)a.O + ((size_t)h * Lq + qrow) * D;
@@ -387,15 +443,149 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     }
 }
 
+// BAL = false: one workgroup per work item (head, query tile), dealt so that
+// each XCD (blocks go to the 8 XCDs round-robin) receives a contiguous range
+// of items: the query tiles of a head then share that XCD's L2.
+// BAL = true: the balanced schedule above, with the same XCD-contiguous
+// assignment of ranges (n_blocks is a multiple of 8).
+template <int D, bool BAL>
+__global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
+    using C = Cfg<D>;
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][C::TILE];
+    __shared__ __attribute__((aligned(16))) uint16_t Vs[2][C::VTILE];
+
+    if (!BAL) {
+        const int item = (blockIdx.x & 7) * a.items_per_xcd + (blockIdx.x >> 3);
+        if (item >= a.n_items) return;
+        const int h = item / a.n_qtiles;
+        attn_segment<D>(a, Ks, Vs, h, item - h * a.n_qtiles, 0, head_tiles(a, h), 0, nullptr);
+        return;
+    }
+    const Schedule sc = make_schedule(a);
+    const int r = (blockIdx.x & 7) * (a.n_blocks >> 3) + (blockIdx.x >> 3);
+    if (r >= sc.G) return;
+    const int64_t end = sc.start(r + 1);
+    int64_t cur = sc.start(r);
+    bool first = true;
+    while (cur < end) {
+        // locate the item holding tile `cur`
+        int h = 0, T = head_tiles(a, 0);
+        int64_t base = 0;
+        while (cur >= base + (int64_t)a.n_qtiles * T) {
+            base += (int64_t)a.n_qtiles * T;
+            T = head_tiles(a, ++h);
+        }
+        const int qt = (int)((cur - base) / T);
+        const int64_t ibase = base + (int64_t)qt * T;
+        const int t0 = (int)(cur - ibase);
+        const int t1 = (int)((end < ibase + T ? end : ibase + T) - ibase);
+        float *slot = (t0 == 0 && t1 == T)
+                          ? nullptr
+                          : a.part + (size_t)(2 * r + (first ? 0 : 1)) * slot_floats<D>();
+        // Rotate the item's key tiles so that its first part, started at time
+        // tau0 = ibase - start(owner(ibase)) of its workgroup, reads key tile
+        // tau mod T at time tau: the first parts of all items of a head then
+        // sweep its K/V in step (later parts in step among themselves, shifted
+        // by a range length), so the XCD's L2 serves the re-reads.
+        const int rot = (int)((ibase - sc.start(sc.owner(ibase))) % T);
+        attn_segment<D>(a, Ks, Vs, h, qt, t0, t1, rot, slot);
+        cur = ibase + t1;
+        first = false;
+    }
+}
+
+// Combines the parts of every item the balanced schedule split: with part
+// maxima m_j, sums l_j and unnormalised outputs O_j of a row,
+//   M = max_j m_j,  L = sum_j 2^(m_j - M) l_j,  O = sum_j 2^(m_j - M) O_j / L,
+// and lse = ln 2 * M + ln L.  Workgroup (item, w) handles the 32 rows of wave
+// w of the item's query tile; items computed whole are skipped.
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+    using C = Cfg<D>;
+    __shared__ float Mrow[32], Linv[32];
+    const int item = blockIdx.x, w = blockIdx.y;
+    const int h = item / a.n_qtiles, qt = item - h * a.n_qtiles;
+    const Schedule sc = make_schedule(a);
+    int64_t P = 0;
+    for (int hh = 0; hh < h; ++hh) P += (int64_t)a.n_qtiles * head_tiles(a, hh);
+    const int T = head_tiles(a, h);
+    P += (int64_t)qt * T;
+    const int b0 = sc.owner(P), b1 = sc.owner(P + T - 1);
+    if (b0 == b1) return;
+    // the item is b0's last segment unless b0's range starts with it, and the
+    // first segment of every later workgroup up to b1
+    const int s0 = sc.start(b0) == P ? 2 * b0 : 2 * b0 + 1;
+    auto part = [&](int b) -> const float * {
+        return a.part + (size_t)(b == b0 ? s0 : 2 * b) * slot_floats<D>();
+    };
+    const int tid = threadIdx.x;
+    if (tid < 32) {
+        const int row = w * 32 + tid;
+        float M = -__builtin_inff();
+        for (int b = b0; b <= b1; ++b) M = fmaxf(M, part(b)[BM * D + row]);
+        float L = 0.f;
+        for (int b = b0; b <= b1; ++b) {
+            const float *p = part(b);
+            L += __builtin_amdgcn_exp2f(p[BM * D + row] - M) * p[BM * D + BM + row];
+        }
+        Mrow[tid] = M;
+        Linv[tid] = 1.f / L;
+        const int qrow = qt * BM + row;
+        if (a.lse && qrow < a.Lq) a.lse[(size_t)h * a.Lq + qrow] = M * 0.69314718055994530942f + logf(L);
+    }
+    __syncthreads();
+    constexpr int kVecs = C::MB * 4 * 64;  // float4s of one wave's accumulators
+#pragma unroll
+    for (int i = 0; i < kVecs / 256; ++i) {
+        const int q = i * 256 + tid;
+        const int mb = q / (4 * 64), g = (q / 64) % 4, ln = q % 64;
+        const int r = ln & 31;
+        const int qrow = qt * BM + w * 32 + r;
+        if (qrow >= a.Lq) continue;
+        const float M = Mrow[r];
+        const size_t idx = (size_t)w * kVecs + q;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int b = b0; b <= b1; ++b) {
+            const float *p = part(b);
+            const float wgt = __builtin_amdgcn_exp2f(p[BM * D + w * 32 + r] - M);
+            const float4 v = ((const float4 *)p)[idx];
+            acc.x += wgt * v.x;
+            acc.y += wgt * v.y;
+            acc.z += wgt * v.z;
+            acc.w += wgt * v.w;
+        }
+        const float inv = Linv[r];
+        const __bf16 e0 = (__bf16)(acc.x * inv), e1 = (__bf16)(acc.y * inv);
+        const __bf16 e2 = (__bf16)(acc.z * inv), e3 = (__bf16)(acc.w * inv);
+        const uint2 pk = make_uint2(
+            (uint32_t)__builtin_bit_cast(uint16_t, e0) | ((uint32_t)__builtin_bit_cast(uint16_t, e1) << 16),
+            (uint32_t)__builtin_bit_cast(uint16_t, e2) | ((uint32_t)__builtin_bit_cast(uint16_t, e3) << 16));
+        const int d0 = 32 * mb + 8 * g + 4 * (ln >> 5);
+        *(uint2 *)((uint16_t *)a.O + ((size_t)h * a.Lq + qrow) * D + d0) = pk;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s) {
+    if (a.n_blocks > 0) {
+        if (head_dim == 128) {
+            hipLaunchKernelGGL((attn_bf16_kernel<128, true>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
+            hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(a.n_items, BM / 32), dim3(256), 0, s, a);
+        } else {
+            hipLaunchKernelGGL((attn_bf16_kernel<64, true>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
+            hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(a.n_items, BM / 32), dim3(256), 0, s, a);
+        }
+        return hipGetLastError();
+    }
     const unsigned blocks = (unsigned)a.items_per_xcd * 8u;
     if (head_dim == 128)
-        hipLaunchKernelGGL(attn_bf16_kernel<128>, dim3(blocks), dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL((attn_bf16_kernel<128, false>), dim3(blocks), dim3(kThreads), 0, s, a);
     else
-        hipLaunchKernelGGL(attn_bf16_kernel<64>, dim3(blocks), dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL((attn_bf16_kernel<64, false>), dim3(blocks), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
+
+size_t attention_part_bytes(int head_dim) { return (size_t)kAttnRowsBf16 * (head_dim + 2) * 4; }
 
 }  // namespace fkv

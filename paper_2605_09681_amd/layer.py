@@ -1,8 +1,9 @@
 """One attention layer's Forcing-KV step: the four C-ABI calls in order.
 
 :class:`CompressedLayer` owns the per-layer intermediate device buffers
-(scores, kept segment ids, compressed K/V slabs, kv_len, score workspace)
-sized from the shape and budgets, and runs one AR step of one layer:
+(scores, kept segment ids, compressed K/V slabs, kv_len, the scoring and
+attention workspaces) sized from the shape and budgets, and runs one AR step
+of one layer:
 
 1. ``fkv_score_segments``  (dynamic heads, Eq. 3 similarity)
 2. ``fkv_select_compact``  (dynamic heads, Eq. 3 BottomK + compaction)
@@ -18,15 +19,17 @@ from typing import Optional, Sequence
 
 import torch
 
-from . import (FKV_DYNAMIC, FKV_STATIC, fkv_chunk_attention, fkv_compress_static,
-               fkv_num_segments, fkv_score_segments, fkv_score_workspace_size,
-               fkv_select_compact, make_heads, make_shape, slab_tokens)
+from . import (FKV_DYNAMIC, FKV_STATIC, fkv_attention_workspace_size, fkv_chunk_attention,
+               fkv_compress_static, fkv_num_segments, fkv_score_segments,
+               fkv_score_workspace_size, fkv_select_compact, make_heads, make_shape,
+               slab_tokens)
 
 
 class CompressedLayer:
     def __init__(self, n_heads: int, head_dim: int, frame_tokens: int, hist_frames: int,
                  cap_frames: int, chunk_frames: int, seg_tokens: int, dtype: str,
-                 budgets: Sequence, device="cuda", slab: Optional[int] = None):
+                 budgets: Sequence, device="cuda", slab: Optional[int] = None,
+                 balanced: bool = True):
         self.shape = make_shape(n_heads, head_dim, frame_tokens, hist_frames, cap_frames,
                                 chunk_frames, seg_tokens, dtype)
         self.heads = make_heads(budgets)
@@ -44,6 +47,12 @@ class CompressedLayer:
         self.kv_len = torch.zeros((n_heads,), dtype=torch.int32, device=dev)
         self.ws_bytes = fkv_score_workspace_size(self.shape, self.heads)
         self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
+        self.attn_workspace = None
+        if balanced:
+            with torch.cuda.device(dev):
+                n = fkv_attention_workspace_size(self.shape)
+            if n > 0:
+                self.attn_workspace = torch.empty(n, dtype=torch.uint8, device=dev)
         self.scale = 1.0 / math.sqrt(head_dim)
         self.has_static = FKV_STATIC in self.types
         self.has_dynamic = FKV_DYNAMIC in self.types
@@ -63,7 +72,7 @@ class CompressedLayer:
 
     def attention(self, Q, K_cur, V_cur, O, lse=None, scale: Optional[float] = None):
         fkv_chunk_attention(self.shape, Q, self.Kc, self.Vc, self.kv_len, K_cur, V_cur,
-                            self.scale if scale is None else scale, O, lse)
+                            self.scale if scale is None else scale, O, lse, self.attn_workspace)
 
     # whole step --------------------------------------------------------------
     def compress(self, K_hist, V_hist, frame_slot, K_cur):

@@ -40,16 +40,18 @@ def dev_inputs(x: W.LayerInputs):
                 V_cur=to_dev(x.V_cur, dt), Q=to_dev(x.Q, dt))
 
 
-def make_layer(cfg: W.LayerConfig, heads=None, slab=None):
+def make_layer(cfg: W.LayerConfig, heads=None, slab=None, balanced=True):
     from paper_2605_09681_amd.layer import CompressedLayer
     return CompressedLayer(cfg.n_heads, cfg.head_dim, cfg.frame_tokens, cfg.hist_frames,
                            cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype,
-                           cfg.heads if heads is None else heads, slab=slab)
+                           cfg.heads if heads is None else heads, slab=slab, balanced=balanced)
 
 
-def run_gpu(cfg: W.LayerConfig, x: W.LayerInputs, heads=None, with_lse=True, scale=None):
-    """Run one layer step on the GPU; returns (layer, O, lse) with device tensors."""
-    layer = make_layer(cfg, heads)
+def run_gpu(cfg: W.LayerConfig, x: W.LayerInputs, heads=None, with_lse=True, scale=None,
+            balanced=True):
+    """Run one layer step on the GPU; returns (layer, O, lse) with device tensors.
+    balanced selects the attention schedule (workspace given or not)."""
+    layer = make_layer(cfg, heads, balanced=balanced)
     d = dev_inputs(x)
     O = torch.empty_like(d["Q"])
     lse = torch.empty((cfg.n_heads, cfg.lq), dtype=torch.float32, device="cuda") if with_lse else None
@@ -60,9 +62,9 @@ def run_gpu(cfg: W.LayerConfig, x: W.LayerInputs, heads=None, with_lse=True, sca
 
 
 def sample_rows(lq: int, n_random: int = 48, seed: int = 0) -> np.ndarray:
-    """First rows, the ragged tail of the last 128-row tile, and random rows."""
+    """First rows, the ragged tail of the last 256-row tile, and random rows."""
     rng = np.random.default_rng(seed)
-    tail_start = (lq // 128) * 128
+    tail_start = (lq // 256) * 256
     rows = set(range(min(16, lq))) | set(range(max(0, min(tail_start, lq - 40)), lq))
     rows |= set(rng.integers(0, lq, n_random).tolist())
     return np.array(sorted(rows), dtype=np.int32)
@@ -106,11 +108,11 @@ def assert_attention_close(O_dev, ref, dtype, lse_dev=None):
     return max_abs, rel
 
 
-def check_layer(cfg, x, heads=None, rows=None, scale=None):
+def check_layer(cfg, x, heads=None, rows=None, scale=None, balanced=True):
     """Full parity check of one layer step: compression bit-exact on every
     head, attention on the given query rows (all rows by default)."""
     heads = cfg.heads if heads is None else heads
-    layer, O, lse = run_gpu(cfg, x, heads=heads, scale=scale)
+    layer, O, lse = run_gpu(cfg, x, heads=heads, scale=scale, balanced=balanced)
     ref = oracle.run_layer(cfg, x, rows=rows, heads=heads,
                            scale=(1 / math.sqrt(cfg.head_dim)) if scale is None else scale)
     assert_compression_exact(cfg, layer, ref, heads)

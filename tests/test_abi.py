@@ -127,13 +127,19 @@ def test_attention_arg_errors(fkv):
     shape = _shape(fkv)
     L = fkv.lib()
     assert L.fkv_chunk_attention(ctypes.byref(shape), FAKE, FAKE, FAKE, 10, FAKE, FAKE, FAKE,
-                                 ctypes.c_float(0.0), FAKE, None, None) == 1
+                                 ctypes.c_float(0.0), FAKE, None, None, 0, None) == 1
     assert L.fkv_chunk_attention(ctypes.byref(shape), FAKE, FAKE, FAKE, 10, FAKE, FAKE, FAKE,
-                                 ctypes.c_float(float("nan")), FAKE, None, None) == 1
+                                 ctypes.c_float(float("nan")), FAKE, None, None, 0, None) == 1
     assert L.fkv_chunk_attention(ctypes.byref(shape), None, FAKE, FAKE, 10, FAKE, FAKE, FAKE,
-                                 ctypes.c_float(0.1), FAKE, None, None) == 1
+                                 ctypes.c_float(0.1), FAKE, None, None, 0, None) == 1
     assert L.fkv_chunk_attention(ctypes.byref(shape), FAKE, FAKE, FAKE, -1, FAKE, FAKE, FAKE,
-                                 ctypes.c_float(0.1), FAKE, None, None) == 1
+                                 ctypes.c_float(0.1), FAKE, None, None, 0, None) == 1
+    bad = fkv.make_shape(2, 96, 64, 4, 4, 1, 64, "bf16")
+    out = ctypes.c_size_t(7)
+    assert L.fkv_attention_workspace_size(ctypes.byref(bad), ctypes.byref(out)) == 2
+    assert L.fkv_attention_workspace_size(ctypes.byref(shape), None) == 1
+    f32 = fkv.make_shape(2, 128, 64, 4, 4, 1, 64, "f32")
+    assert L.fkv_attention_workspace_size(ctypes.byref(f32), ctypes.byref(out)) == 0 and out.value == 0
 
 
 def test_segment_count(fkv):

@@ -86,6 +86,43 @@ def test_small_all_rows(d, F, L):
     check_layer(cfg, x)
 
 
+@pytest.mark.parametrize("d", [128, 64])
+def test_small_per_item_schedule(d):
+    """Attention without a workspace: one workgroup per (head, query tile)."""
+    cfg = _small(F=100, L=25, d=d)
+    slot = np.array([3, 0, 8, 1, 5, 2, 7], np.int32)
+    _print_case("small-per-item", d=d)
+    check_layer(cfg, W.make_layer_inputs(cfg, seed=d + 1, frame_slot=slot), balanced=False)
+
+
+def test_balanced_many_items():
+    """48 heads with ragged budgets and 2 query tiles each: the balanced
+    schedule gives workgroups several whole items plus cut ones, every row
+    checked."""
+    heads = tuple(W.HeadBudget(W.STATIC, h % 2, h % 7) if h % 3 else
+                  W.HeadBudget(W.DYNAMIC, 1, h % 2, 1 + h % 9, W.SCOPE_GLOBAL) for h in range(48))
+    cfg = W.LayerConfig("many", 48, 64, 128, 12, 12, 4, 128, "bf16", heads, 0.9)
+    _print_case("balanced-many")
+    check_layer(cfg, W.make_layer_inputs(cfg, seed=21))
+
+
+def test_schedules_agree_480p():
+    """Balanced and per-item schedules on the 480P layer agree to rounding:
+    split parts round their probabilities against their own running max and
+    sum in another order, so outputs may differ by one bf16 step plus a small
+    absolute amount near zero."""
+    cfg = W.wan_layer_config("480p")
+    _print_case("480p-schedules")
+    x = W.make_layer_inputs(cfg, seed=2)
+    _, Ob, lb = run_gpu(cfg, x, balanced=True)
+    _, Ou, lu = run_gpu(cfg, x, balanced=False)
+    ob = W.bf16_bits_to_f32(from_dev(Ob)).astype(np.float64)
+    ou = W.bf16_bits_to_f32(from_dev(Ou)).astype(np.float64)
+    tol = np.abs(ou) * 2.0 ** -7 + 2e-4
+    assert (np.abs(ob - ou) <= tol).all(), float(np.abs(ob - ou).max())
+    np.testing.assert_allclose(from_dev(lb), from_dev(lu), rtol=0, atol=1e-4)
+
+
 def test_small_fp32_multitile():
     cfg = _small(F=48, L=16, H=5, cap=6, C=3, d=64, dtype="f32")
     _print_case("small-fp32")
