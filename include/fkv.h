@@ -161,8 +161,8 @@ fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads,
 
 /* Device workspace fkv_chunk_attention takes for its balanced schedule on the
  * CURRENT device (hipGetDevice): 2 x the device's compute units, rounded down
- * to a multiple of 8, partial-result slots of 256 rows x (head_dim + 2) floats
- * (about 68 MB for head_dim 128 on a 256-CU device).  0 for FKV_F32, which has
+ * to a multiple of 8, partial-result slots of 256 rows x (2*head_dim + 8)
+ * bytes (about 34 MB for head_dim 128 on a 256-CU device).  0 for FKV_F32, which has
  * no balanced schedule.  FKV_ERR_DEVICE if the device cannot be queried. */
 fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes);
 
@@ -183,9 +183,11 @@ fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes);
  * need no initialisation) the key tiles of all heads and query tiles are split
  * evenly over one workgroup per compute unit, and tiles cut by a split are
  * combined by a second kernel on the same stream (FKV_ERR_CAPACITY if the
- * workspace is smaller).  Both schedules compute the same function; rounding
- * may differ in the last bit.  fp32 ignores the workspace.  Two calls that
- * share a workspace must be ordered by the caller. */
+ * workspace is smaller).  Both schedules compute the same function; a split
+ * tile's parts are normalised and rounded to bf16 before they are combined, so
+ * its output may differ from the one-workgroup result by about one bf16 step.
+ * fp32 ignores the workspace.  Two calls that share a workspace must be
+ * ordered by the caller. */
 fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q,
                                const void *Kc, const void *Vc, int32_t slab,
                                const int32_t *kv_len, const void *K_cur,

@@ -204,12 +204,22 @@ __device__ __forceinline__ Schedule make_schedule(const AttnArgs &a) {
     return sc;
 }
 
-// Partial result of one part of an item, in a slot of BM*(D+2) floats: the
-// unnormalised O^T accumulators exactly as the waves hold them (float4 index
+// Partial result of one part of an item, in a slot of BM*(D/2 + 2) floats:
+// the part's own normalised output o/l rounded to bf16, in the accumulator
+// layout of the waves (4 values per lane and uint2 index
 // ((wave*MB + mb)*4 + g)*64 + lane), then the running max m (log2 units) of
 // the BM rows, then their probability sums l.
 template <int D>
-__device__ __forceinline__ size_t slot_floats() { return (size_t)BM * (D + 2); }
+__device__ __forceinline__ size_t slot_floats() { return (size_t)BM * (D / 2 + 2); }
+
+__device__ __forceinline__ uint2 pack_bf16x4(float x0, float x1, float x2, float x3) {
+    const uint32_t b0 = __builtin_bit_cast(uint16_t, (__bf16)x0), b1 = __builtin_bit_cast(uint16_t, (__bf16)x1);
+    const uint32_t b2 = __builtin_bit_cast(uint16_t, (__bf16)x2), b3 = __builtin_bit_cast(uint16_t, (__bf16)x3);
+    return make_uint2(b0 | (b1 << 16), b2 | (b3 << 16));
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 
 // One segment: positions [t0, t1) of item (h, qt), where position j is key
 // tile (j + rot) mod T of the item's T tiles (the order of key tiles does not
@@ -407,37 +417,31 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
     if (grp == 0) __syncthreads();
 
     const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float inv = 1.f / l_tot;
     if (slot) {
-        float4 *op = (float4 *)slot;
+        uint2 *op = (uint2 *)slot;
 #pragma unroll
         for (int mb = 0; mb < C::MB; ++mb)
 #pragma unroll
             for (int g = 0; g < 4; ++g)
                 op[((wave * C::MB + mb) * 4 + g) * 64 + lane] =
-                    make_float4(o[mb][4 * g], o[mb][4 * g + 1], o[mb][4 * g + 2], o[mb][4 * g + 3]);
+                    pack_bf16x4(o[mb][4 * g] * inv, o[mb][4 * g + 1] * inv, o[mb][4 * g + 2] * inv,
+                                o[mb][4 * g + 3] * inv);
         if (hl == 0) {
-            slot[BM * D + wave * 32 + l32] = m_run;
-            slot[BM * D + BM + wave * 32 + l32] = l_tot;
+            slot[BM * D / 2 + wave * 32 + l32] = m_run;
+            slot[BM * D / 2 + BM + wave * 32 + l32] = l_tot;
         }
         return;
     }
-    const float inv = 1.f / l_tot;
     if (qok) {
         uint16_t *Oh = (uint16_t *)a.O + ((size_t)h * Lq + qrow) * D;
 #pragma unroll
         for (int mb = 0; mb < C::MB; ++mb)
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                // O^T rows d = 32mb + 8g + 4hl + {0..3}
-                const __bf16 b0 = (__bf16)(o[mb][4 * g + 0] * inv);
-                const __bf16 b1 = (__bf16)(o[mb][4 * g + 1] * inv);
-                const __bf16 b2 = (__bf16)(o[mb][4 * g + 2] * inv);
-                const __bf16 b3 = (__bf16)(o[mb][4 * g + 3] * inv);
-                const uint2 pk = make_uint2(
-                    (uint32_t)__builtin_bit_cast(uint16_t, b0) | ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16),
-                    (uint32_t)__builtin_bit_cast(uint16_t, b2) | ((uint32_t)__builtin_bit_cast(uint16_t, b3) << 16));
-                *(uint2 *)(Oh + mb * 32 + 8 * g + 4 * hl) = pk;
-            }
+            for (int g = 0; g < 4; ++g)  // O^T rows d = 32mb + 8g + 4hl + {0..3}
+                *(uint2 *)(Oh + mb * 32 + 8 * g + 4 * hl) =
+                    pack_bf16x4(o[mb][4 * g] * inv, o[mb][4 * g + 1] * inv, o[mb][4 * g + 2] * inv,
+                                o[mb][4 * g + 3] * inv);
         if (a.lse && hl == 0)
             a.lse[(size_t)h * Lq + qrow] = m_run * 0.69314718055994530942f + logf(l_tot);
     }
@@ -495,14 +499,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
 }
 
 // Combines the parts of every item the balanced schedule split: with part
-// maxima m_j, sums l_j and unnormalised outputs O_j of a row,
-//   M = max_j m_j,  L = sum_j 2^(m_j - M) l_j,  O = sum_j 2^(m_j - M) O_j / L,
+// maxima m_j, sums l_j and normalised outputs o_j of a row,
+//   M = max_j m_j,  w_j = 2^(m_j - M) l_j,  L = sum_j w_j,  O = sum_j w_j o_j / L,
 // and lse = ln 2 * M + ln L.  Workgroup (item, w) handles the 32 rows of wave
 // w of the item's query tile; items computed whole are skipped.
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     using C = Cfg<D>;
-    __shared__ float Mrow[32], Linv[32];
+    constexpr int kML = BM * D / 2;  // float offset of m within a slot
     const int item = blockIdx.x, w = blockIdx.y;
     const int h = item / a.n_qtiles, qt = item - h * a.n_qtiles;
     const Schedule sc = make_schedule(a);
@@ -518,50 +522,43 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     auto part = [&](int b) -> const float * {
         return a.part + (size_t)(b == b0 ? s0 : 2 * b) * slot_floats<D>();
     };
+    // Thread tid handles row r = tid % 32 of the wave's 32 rows; it combines
+    // the row's parts in one pass with a running maximum.
     const int tid = threadIdx.x;
-    if (tid < 32) {
-        const int row = w * 32 + tid;
-        float M = -__builtin_inff();
-        for (int b = b0; b <= b1; ++b) M = fmaxf(M, part(b)[BM * D + row]);
-        float L = 0.f;
-        for (int b = b0; b <= b1; ++b) {
-            const float *p = part(b);
-            L += __builtin_amdgcn_exp2f(p[BM * D + row] - M) * p[BM * D + BM + row];
-        }
-        Mrow[tid] = M;
-        Linv[tid] = 1.f / L;
-        const int qrow = qt * BM + row;
-        if (a.lse && qrow < a.Lq) a.lse[(size_t)h * a.Lq + qrow] = M * 0.69314718055994530942f + logf(L);
-    }
-    __syncthreads();
-    constexpr int kVecs = C::MB * 4 * 64;  // float4s of one wave's accumulators
+    const int r = tid & 31, row = w * 32 + r;
+    const int qrow = qt * BM + row;
+    constexpr int kVecs = C::MB * 4 * 64;  // uint2s (4 values) of one wave's accumulators
+    constexpr int kPer = kVecs / 256;
+    float M = -__builtin_inff(), L = 0.f;
+    float x[kPer][4] = {};
+    for (int b = b0; b <= b1; ++b) {
+        const float *p = part(b);
+        const float m = p[kML + row], l = p[kML + BM + row];
+        uint2 v[kPer];
 #pragma unroll
-    for (int i = 0; i < kVecs / 256; ++i) {
-        const int q = i * 256 + tid;
-        const int mb = q / (4 * 64), g = (q / 64) % 4, ln = q % 64;
-        const int r = ln & 31;
-        const int qrow = qt * BM + w * 32 + r;
-        if (qrow >= a.Lq) continue;
-        const float M = Mrow[r];
-        const size_t idx = (size_t)w * kVecs + q;
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int b = b0; b <= b1; ++b) {
-            const float *p = part(b);
-            const float wgt = __builtin_amdgcn_exp2f(p[BM * D + w * 32 + r] - M);
-            const float4 v = ((const float4 *)p)[idx];
-            acc.x += wgt * v.x;
-            acc.y += wgt * v.y;
-            acc.z += wgt * v.z;
-            acc.w += wgt * v.w;
+        for (int i = 0; i < kPer; ++i) v[i] = ((const uint2 *)p)[(size_t)w * kVecs + i * 256 + tid];
+        const float Mn = fmaxf(M, m);
+        const float sc = __builtin_amdgcn_exp2f(M - Mn), wg = __builtin_amdgcn_exp2f(m - Mn) * l;
+        M = Mn;
+        L = L * sc + wg;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            x[i][0] = x[i][0] * sc + wg * bf16_lo(v[i].x);
+            x[i][1] = x[i][1] * sc + wg * bf16_hi(v[i].x);
+            x[i][2] = x[i][2] * sc + wg * bf16_lo(v[i].y);
+            x[i][3] = x[i][3] * sc + wg * bf16_hi(v[i].y);
         }
-        const float inv = Linv[r];
-        const __bf16 e0 = (__bf16)(acc.x * inv), e1 = (__bf16)(acc.y * inv);
-        const __bf16 e2 = (__bf16)(acc.z * inv), e3 = (__bf16)(acc.w * inv);
-        const uint2 pk = make_uint2(
-            (uint32_t)__builtin_bit_cast(uint16_t, e0) | ((uint32_t)__builtin_bit_cast(uint16_t, e1) << 16),
-            (uint32_t)__builtin_bit_cast(uint16_t, e2) | ((uint32_t)__builtin_bit_cast(uint16_t, e3) << 16));
-        const int d0 = 32 * mb + 8 * g + 4 * (ln >> 5);
-        *(uint2 *)((uint16_t *)a.O + ((size_t)h * a.Lq + qrow) * D + d0) = pk;
+    }
+    if (qrow >= a.Lq) return;
+    if (a.lse && tid < 32) a.lse[(size_t)h * a.Lq + qrow] = M * 0.69314718055994530942f + logf(L);
+    const float inv = 1.f / L;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int q = i * 256 + tid;
+        const int mb = q / (4 * 64), g = (q / 64) % 4;
+        const int d0 = 32 * mb + 8 * g + 4 * ((tid & 63) >> 5);
+        *(uint2 *)((uint16_t *)a.O + ((size_t)h * a.Lq + qrow) * D + d0) =
+            pack_bf16x4(x[i][0] * inv, x[i][1] * inv, x[i][2] * inv, x[i][3] * inv);
     }
 }
 
@@ -586,6 +583,6 @@ hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s)
     return hipGetLastError();
 }
 
-size_t attention_part_bytes(int head_dim) { return (size_t)kAttnRowsBf16 * (head_dim + 2) * 4; }
+size_t attention_part_bytes(int head_dim) { return (size_t)kAttnRowsBf16 * (head_dim / 2 + 2) * 4; }
 
 }  // namespace fkv
