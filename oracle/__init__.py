@@ -62,6 +62,8 @@ def lib():
         L.fkvo_n_segments.restype = I
         L.fkvo_score_head.argtypes = [I, I, I, I, I, P, P, P, P, P]
         L.fkvo_score_head.restype = None
+        L.fkvo_score_pooled.argtypes = [I, I, I, I, I, I, I, LG, P, P, P, P, P]
+        L.fkvo_score_pooled.restype = None
         L.fkvo_select_head.argtypes = [I, I, I, I, I, I, I, P, P]
         L.fkvo_select_head.restype = I
         L.fkvo_compact_head.argtypes = [I, I, I, I, I, P, I, P, P, P]
@@ -132,6 +134,23 @@ def score_head(hist_head: np.ndarray, frame_slot: np.ndarray, cur_head: np.ndarr
     s64 = np.empty(max(n, 1), np.float64)
     lib().fkvo_score_head(_dt(hist_head), d, F, H, L, _ptr(hist_head), _ptr(slot),
                           _ptr(cur_head), _ptr(s32), _ptr(s64))
+    return s32[:n].copy(), s64[:n].copy()
+
+
+def score_pooled(hist: np.ndarray, frame_slot: np.ndarray, cur: np.ndarray, H: int, L: int):
+    """First-block proxy (Sec. 4.3): one similarity per segment from the keys of
+    all heads together.  hist: [n_heads][cap][F][d]; cur: [n_heads][lq][d].
+    Returns (fp32 scores, fp64 cosines)."""
+    hist = _c(hist)
+    cur = _c(cur)
+    nh, cap, F, d = hist.shape
+    assert cur.dtype == hist.dtype and cur.shape[0] == nh and cur.shape[2] == d
+    slot = _c(frame_slot, np.int32)
+    n = n_segments(H, F, L)
+    s32 = np.empty(max(n, 1), np.float32)
+    s64 = np.empty(max(n, 1), np.float64)
+    lib().fkvo_score_pooled(_dt(hist), nh, d, F, H, L, cap, cur.shape[1], _ptr(hist), _ptr(slot),
+                            _ptr(cur), _ptr(s32), _ptr(s64))
     return s32[:n].copy(), s64[:n].copy()
 
 

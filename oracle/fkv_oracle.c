@@ -116,6 +116,53 @@ void fkvo_score_head(int dtype, int d, int F, int H, int L, const void *hist,
 }
 
 /* ---------------------------------------------------------------------------
+ * The first-block proxy of Sec. 4.3: the similarity is computed from the key
+ * states of all attention heads together, i.e. the segment is the matrix
+ * heads x tokens x head_dim and its cosine is taken over all of those
+ * elements.  Same products, sums and rounding as fkvo_score_head.
+ * hist: [n_heads][cap][F][d]; cur: [n_heads][lq][d]; s32/s64: [n_seg].
+ * ------------------------------------------------------------------------- */
+void fkvo_score_pooled(int dtype, int n_heads, int d, int F, int H, int L,
+                       int cap, long lq, const void *hist,
+                       const int32_t *frame_slot, const void *cur, float *s32,
+                       double *s64) {
+    const long HF = (long)H * F;
+    const int n_seg = fkvo_n_segments(H, F, L);
+    const size_t hist_head = (size_t)cap * F * d, cur_head = (size_t)lq * d;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int g = 0; g < n_seg; ++g) {
+        long x0 = (long)g * L;
+        long x1 = x0 + L < HF ? x0 + L : HF;
+        double dot = 0.0, na = 0.0, nb = 0.0;
+        for (int h = 0; h < n_heads; ++h) {
+            for (long x = x0; x < x1; ++x) {
+                size_t ra = h * hist_head + hist_row(x, F, d, frame_slot);
+                long y = x + F;
+                const void *bbase;
+                size_t rb;
+                if (y < HF) {
+                    bbase = hist;
+                    rb = h * hist_head + hist_row(y, F, d, frame_slot);
+                } else {
+                    bbase = cur;
+                    rb = h * cur_head + (size_t)(y - HF) * d;
+                }
+                for (int c = 0; c < d; ++c) {
+                    double a = load_elem(hist, dtype, ra + c);
+                    double b = load_elem(bbase, dtype, rb + c);
+                    dot += a * b;
+                    na += a * a;
+                    nb += b * b;
+                }
+            }
+        }
+        double cosv = (na * nb == 0.0) ? 0.0 : dot / sqrt(na * nb);
+        s64[g] = cosv;
+        s32[g] = (float)cosv;
+    }
+}
+
+/* ---------------------------------------------------------------------------
  * Eq. 3 BottomK.  A segment is forced (always kept) when it touches one of the
  * sink frames or one of the `recent` most recent frames.  The other segments
  * are candidates; within each selection group the min(k, |group|) candidates

@@ -53,6 +53,14 @@ void fkvo_score_head(int dtype, int d, int F, int H, int L, const void *hist,
                      const int32_t *frame_slot, const void *cur, float *s32,
                      double *s64);
 
+/* The first-block proxy of Sec. 4.3: one similarity per segment from the keys
+ * of all heads together (the cosine over heads x tokens x head_dim elements).
+ * hist: [n_heads][cap][F][d]; cur: [n_heads][lq][d]; s32/s64: [n_seg]. */
+void fkvo_score_pooled(int dtype, int n_heads, int d, int F, int H, int L,
+                       int cap, long lq, const void *hist,
+                       const int32_t *frame_slot, const void *cur, float *s32,
+                       double *s64);
+
 /* Eq. 3 BottomK: keeps the forced segments (those touching the sink frames or
  * the last `recent` frames) plus, in every selection group, the min(k, |group|)
  * candidates of smallest key (isNaN(s), s, g).  scope 0: one group per frame;

@@ -6,6 +6,10 @@ oracle is pinned by:
 * Eq. 2 static kept set: hand-listed closed-form cases (overlapping sink and
   recent windows, empty history, the paper's one-anchor-frame rule), and the
   frame gather against numpy fancy indexing.
+* Sec. 4.3 first-block proxy (pooled over heads): exact rational arithmetic,
+  the closed form (a - b) / (a + b) of a repeating and a sign-alternating
+  head, reduction to the per-head score for one or 2^k identical heads, torch
+  cosine of the concatenation over heads.
 * Eq. 3 similarity: exact rational arithmetic (``fractions`` + 80-digit
   ``decimal``, rounded to fp32 by hand) on tiny bf16 and fp32 inputs for
   segments shorter than, equal to and longer than a frame; closed forms
@@ -252,6 +256,79 @@ def test_score_ar1_statistic(oracle_lib):
     s = oracle.score_head(hist, np.arange(H, dtype=np.int32), cur, H, F)[0]
     sd = (1 - rho ** 2) / math.sqrt(F * d)
     assert abs(float(s.mean()) - rho) < 4 * sd / math.sqrt(H) + 2e-3
+
+
+# ---------------------------------------------------------------------------
+# Sec. 4.3 first-block proxy: one similarity from the keys of all heads
+# ---------------------------------------------------------------------------
+def _tiny_heads(dtype, n_heads, H, F, d, C, seed, rho=0.7):
+    frames = W.ar1_key_frames(seed, n_heads, H + C, F, d, rho, dtype)
+    hist = np.ascontiguousarray(frames[:, :H])
+    cur = np.ascontiguousarray(frames[:, H:].reshape(n_heads, C * F, d))
+    return hist, cur
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("F,L", [(4, 2), (4, 4), (4, 8)])
+def test_pooled_score_exact_rational(oracle_lib, dtype, F, L):
+    """Cosine over the concatenation of all heads' segment keys, in exact
+    rational arithmetic, rounded to fp32 by hand."""
+    nh, H, d, C = 3, 4, 5, 1
+    for seed in range(2):
+        hist, cur = _tiny_heads(dtype, nh, H, F, d, C, seed)
+        slot = np.arange(H, dtype=np.int32)
+        s32, _ = oracle.score_pooled(hist, slot, cur, H, L)
+        toks = [logical_tokens(to_f(hist[h], dtype), slot, H) for h in range(nh)]
+        nxts = [np.concatenate([toks[h][F:], to_f(cur[h], dtype)[:F]]) for h in range(nh)]
+        for g in range(-(-H * F // L)):
+            x0, x1 = g * L, min(g * L + L, H * F)
+            a = np.concatenate([t[x0:x1] for t in toks])
+            b = np.concatenate([t[x0:x1] for t in nxts])
+            want, near = exact_cos_f32(a, b)
+            if not near:
+                assert s32[g].view(np.uint32) == want.view(np.uint32), (g, s32[g], want)
+
+
+def test_pooled_score_closed_forms(oracle_lib):
+    """Head A repeats its frame (cosine 1, squared norm a per frame), head B
+    alternates sign (cosine -1, squared norm b): the pooled cosine is
+    (a - b) / (a + b).  With one head the pooled score is that head's score;
+    with 2 or 4 identical heads it equals the per-head score bit for bit."""
+    rng = np.random.default_rng(17)
+    H, F, d = 4, 3, 8
+    X = W.bf16_bits_to_f32(W.f32_to_bf16_bits(rng.standard_normal((F, d), dtype=np.float32)))
+    Y = W.bf16_bits_to_f32(W.f32_to_bf16_bits(rng.standard_normal((F, d), dtype=np.float32)))
+    slot = np.arange(H, dtype=np.int32)
+    hist = W.f32_to_bf16_bits(np.stack([np.stack([X] * H), np.stack([Y, -Y, Y, -Y])]))
+    cur = W.f32_to_bf16_bits(np.stack([X, Y]))
+    s32, s64 = oracle.score_pooled(hist, slot, cur, H, F)
+    a, b = float((X.astype(np.float64) ** 2).sum()), float((Y.astype(np.float64) ** 2).sum())
+    np.testing.assert_allclose(s64, (a - b) / (a + b), rtol=1e-15, atol=0)
+
+    h1, c1 = _tiny_heads("bf16", 1, H, F, d, 1, seed=3)
+    for L in (1, 3, 6):
+        one = oracle.score_pooled(h1, slot, c1, H, L)[0]
+        per = oracle.score_head(h1[0], slot, c1[0], H, L)[0]
+        np.testing.assert_array_equal(one.view(np.uint32), per.view(np.uint32))
+        for n in (2, 4):
+            rep = oracle.score_pooled(np.repeat(h1, n, 0), slot, np.repeat(c1, n, 0), H, L)[0]
+            np.testing.assert_array_equal(rep.view(np.uint32), per.view(np.uint32))
+
+
+def test_pooled_score_matches_torch_cosine(oracle_lib):
+    nh, H, F, d, L = 4, 5, 6, 16, 3
+    hist, cur = _tiny_heads("bf16", nh, H, F, d, 1, seed=9, rho=0.6)
+    perm = np.array([2, 0, 4, 1, 3], np.int32)
+    phys = np.zeros((nh, 5, F, d), np.uint16)
+    phys[:, perm] = hist
+    _, s64 = oracle.score_pooled(phys, perm, cur, H, L)
+    slot = np.arange(H, dtype=np.int32)
+    toks = [torch.from_numpy(logical_tokens(to_f(hist[h], "bf16"), slot, H)) for h in range(nh)]
+    nxts = [torch.cat([toks[h][F:], torch.from_numpy(to_f(cur[h], "bf16"))[:F]]) for h in range(nh)]
+    a = torch.cat([t.reshape(-1, L * d) for t in toks], dim=1)
+    b = torch.cat([t.reshape(-1, L * d) for t in nxts], dim=1)
+    ref = torch.nn.functional.cosine_similarity(a, b, dim=1, eps=0.0).numpy()
+    np.testing.assert_allclose(s64, ref, rtol=0, atol=1e-13)
 
 
 # ---------------------------------------------------------------------------
