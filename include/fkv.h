@@ -159,6 +159,34 @@ fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads,
                               int32_t *kept_seg, void *Kc, void *Vc, int32_t slab,
                               int32_t *kv_len, void *stream);
 
+/* Device workspace fkv_score_pooled needs for `shape` (a multiple of 256
+ * bytes; 0 when H = 0). */
+fkv_status fkv_score_pooled_workspace_size(const fkv_shape *shape, size_t *bytes);
+
+/* The first-block proxy of Sec. 4.3: one similarity per segment from the key
+ * states of ALL n_heads heads together, computed once (from the first
+ * transformer block's keys) and reused by every layer.  For segment g, with
+ * the per-head quantities of fkv_score_segments summed over the heads,
+ *   scores[g] = (float)(sum_h dot_h / sqrt(sum_h na_h * sum_h nb_h)),
+ * i.e. the cosine over heads x tokens x head_dim elements (0 when the
+ * product of the sums is 0).  Same exact fp64 products, fp64 sums and single
+ * rounding as fkv_score_segments.  scores: float [n_seg] (device).  The
+ * workspace needs no initialisation.  H = 0 enqueues nothing. */
+fkv_status fkv_score_pooled(const fkv_shape *shape, const void *K_hist,
+                            const int32_t *frame_slot, const void *K_cur,
+                            float *scores, void *workspace, size_t workspace_bytes,
+                            void *stream);
+
+/* fkv_select_compact with one score row shared by every dynamic head: scores
+ * is float [n_seg] (as fkv_score_pooled writes it) instead of
+ * [n_heads][n_seg].  Everything else, outputs and errors included, is as in
+ * fkv_select_compact. */
+fkv_status fkv_select_compact_pooled(const fkv_shape *shape, const fkv_head *heads,
+                                     const float *scores, const void *K_hist,
+                                     const void *V_hist, const int32_t *frame_slot,
+                                     int32_t *kept_seg, void *Kc, void *Vc,
+                                     int32_t slab, int32_t *kv_len, void *stream);
+
 /* Device workspace fkv_chunk_attention takes for its balanced schedule on the
  * CURRENT device (hipGetDevice): 2 x the device's compute units, rounded down
  * to a multiple of 8, partial-result slots of 256 rows x (2*head_dim + 8)

@@ -13,6 +13,9 @@ Entry points (see ``include/fkv.h`` for the full contract):
 * :func:`fkv_score_segments`   -- segment similarity (Sec. 4.3, Eq. 3)
 * :func:`fkv_select_compact`   -- BottomK + compaction (Sec. 4.3, Eq. 3)
 * :func:`fkv_chunk_attention`  -- chunk attention (Eq. 2 / Eq. 4)
+* :func:`fkv_score_pooled`, :func:`fkv_select_compact_pooled` -- the
+  first-block proxy of Sec. 4.3: one similarity row pooled over all heads,
+  shared by the dynamic heads of every layer
 """
 from __future__ import annotations
 
@@ -33,6 +36,7 @@ FKV_MAX_HEADS, FKV_MAX_FRAMES, FKV_MAX_SEGMENTS = 64, 256, 4096
 
 EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_score_workspace_size", "fkv_score_segments", "fkv_select_compact",
+            "fkv_score_pooled_workspace_size", "fkv_score_pooled", "fkv_select_compact_pooled",
             "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_last_error")
 
 
@@ -85,6 +89,12 @@ def lib():
         L.fkv_score_segments.restype = ctypes.c_int
         L.fkv_select_compact.argtypes = [S, Hd, P, P, P, P, P, P, P, I32, P, P]
         L.fkv_select_compact.restype = ctypes.c_int
+        L.fkv_score_pooled_workspace_size.argtypes = [S, ctypes.POINTER(SZ)]
+        L.fkv_score_pooled_workspace_size.restype = ctypes.c_int
+        L.fkv_score_pooled.argtypes = [S, P, P, P, P, P, SZ, P]
+        L.fkv_score_pooled.restype = ctypes.c_int
+        L.fkv_select_compact_pooled.argtypes = [S, Hd, P, P, P, P, P, P, P, I32, P, P]
+        L.fkv_select_compact_pooled.restype = ctypes.c_int
         L.fkv_attention_workspace_size.argtypes = [S, ctypes.POINTER(SZ)]
         L.fkv_attention_workspace_size.restype = ctypes.c_int
         L.fkv_chunk_attention.argtypes = [S, P, P, P, I32, P, P, P, F, P, P, P, SZ, P]
@@ -218,12 +228,52 @@ def fkv_score_segments(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, score
     return workspace
 
 
-def fkv_select_compact(shape: fkv_shape, heads, scores, K_hist, V_hist, frame_slot, kept_seg,
-                       Kc, Vc, kv_len, stream=None):
+def fkv_score_pooled_workspace_size(shape: fkv_shape) -> int:
+    out = ctypes.c_size_t(0)
+    _raise(lib().fkv_score_pooled_workspace_size(ctypes.byref(shape), ctypes.byref(out)))
+    return int(out.value)
+
+
+def fkv_score_pooled(shape: fkv_shape, K_hist, frame_slot, K_cur, scores,
+                     workspace: Optional[torch.Tensor] = None, stream=None):
+    """One similarity row [n_seg] pooled over all heads (the first-block proxy).
+    If ``workspace`` is None a torch uint8 tensor of the required size is
+    allocated on the current device."""
     dt = _torch_dtype(shape)
     hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
     n_seg = fkv_num_segments(shape)
-    sc = _check(scores, "scores", torch.float32, (shape.n_heads, n_seg))
+    kh = _check(K_hist, "K_hist", dt, hist)
+    sl = _slots(frame_slot, shape.hist_frames)
+    kc = _check(K_cur, "K_cur", dt, (shape.n_heads, _lq(shape), shape.head_dim))
+    sc = _check(scores, "scores", torch.float32, (n_seg,))
+    need = fkv_score_pooled_workspace_size(shape)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=K_hist.device)
+    ws = _check(workspace, "workspace", torch.uint8)
+    _raise(lib().fkv_score_pooled(ctypes.byref(shape), kh, sl, kc, sc, ws, workspace.numel(),
+                                  _stream(stream)))
+    return workspace
+
+
+def fkv_select_compact_pooled(shape: fkv_shape, heads, scores, K_hist, V_hist, frame_slot,
+                              kept_seg, Kc, Vc, kv_len, stream=None):
+    """fkv_select_compact with one shared score row [n_seg]."""
+    _select_compact(shape, heads, scores, K_hist, V_hist, frame_slot, kept_seg, Kc, Vc, kv_len,
+                    stream, pooled=True)
+
+
+def fkv_select_compact(shape: fkv_shape, heads, scores, K_hist, V_hist, frame_slot, kept_seg,
+                       Kc, Vc, kv_len, stream=None):
+    _select_compact(shape, heads, scores, K_hist, V_hist, frame_slot, kept_seg, Kc, Vc, kv_len,
+                    stream, pooled=False)
+
+
+def _select_compact(shape, heads, scores, K_hist, V_hist, frame_slot, kept_seg, Kc, Vc, kv_len,
+                    stream, pooled):
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    n_seg = fkv_num_segments(shape)
+    sc = _check(scores, "scores", torch.float32, (n_seg,) if pooled else (shape.n_heads, n_seg))
     kh, vh = _check(K_hist, "K_hist", dt, hist), _check(V_hist, "V_hist", dt, hist)
     sl = _slots(frame_slot, shape.hist_frames)
     ks = _check(kept_seg, "kept_seg", torch.int32, (shape.n_heads, n_seg))
@@ -231,8 +281,8 @@ def fkv_select_compact(shape: fkv_shape, heads, scores, K_hist, V_hist, frame_sl
     comp = (shape.n_heads, slab, shape.head_dim)
     kc, vc = _check(Kc, "Kc", dt, comp), _check(Vc, "Vc", dt, comp)
     kl = _check(kv_len, "kv_len", torch.int32, (shape.n_heads,))
-    _raise(lib().fkv_select_compact(ctypes.byref(shape), heads, sc, kh, vh, sl, ks, kc, vc,
-                                    int(slab), kl, _stream(stream)))
+    fn = lib().fkv_select_compact_pooled if pooled else lib().fkv_select_compact
+    _raise(fn(ctypes.byref(shape), heads, sc, kh, vh, sl, ks, kc, vc, int(slab), kl, _stream(stream)))
 
 
 def fkv_attention_workspace_size(shape: fkv_shape) -> int:

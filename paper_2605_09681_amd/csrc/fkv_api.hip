@@ -185,6 +185,24 @@ fkv_status balanced_blocks(int *blocks) {
     return FKV_OK;
 }
 
+void score_geometry(const fkv_shape *s, int *unit_tokens, int *units, int64_t *unit_vecs,
+                           int *chunks) {
+    const int U = std::min(s->seg_tokens, s->frame_tokens);
+    *unit_tokens = U;
+    *units = s->frame_tokens / U;
+    *unit_vecs = (int64_t)U * s->head_dim * elem_size(s) / 16;
+    *chunks = (int)((*unit_vecs + fkv::kScoreThreads - 1) / fkv::kScoreThreads);
+}
+
+size_t score_bytes(const fkv_shape *shape, int n_list) {
+    if (n_list == 0 || shape->hist_frames == 0) return 0;
+    int U, units, chunks;
+    int64_t uv;
+    score_geometry(shape, &U, &units, &uv, &chunks);
+    const size_t b = fkv::score_workspace_doubles(n_list, shape->hist_frames, units, chunks) * sizeof(double);
+    return (b + 255) & ~(size_t)255;
+}
+
 }  // namespace
 
 extern "C" {
@@ -257,14 +275,6 @@ fkv_status fkv_compress_static(const fkv_shape *shape, const fkv_head *heads, co
                          "fkv_compress_static launch");
 }
 
-static void score_geometry(const fkv_shape *s, int *unit_tokens, int *units, int64_t *unit_vecs,
-                           int *chunks) {
-    const int U = std::min(s->seg_tokens, s->frame_tokens);
-    *unit_tokens = U;
-    *units = s->frame_tokens / U;
-    *unit_vecs = (int64_t)U * s->head_dim * elem_size(s) / 16;
-    *chunks = (int)((*unit_vecs + fkv::kScoreThreads - 1) / fkv::kScoreThreads);
-}
 
 fkv_status fkv_score_workspace_size(const fkv_shape *shape, const fkv_head *heads, size_t *bytes) {
     fkv_status st;
@@ -273,37 +283,22 @@ fkv_status fkv_score_workspace_size(const fkv_shape *shape, const fkv_head *head
     if (!bytes) return fail(FKV_ERR_ARG, "bytes is NULL");
     int n_dyn = 0;
     for (int h = 0; h < shape->n_heads; ++h) n_dyn += heads[h].type == FKV_DYNAMIC;
-    if (n_dyn == 0 || shape->hist_frames == 0) {
-        *bytes = 0;
-        return ok();
-    }
-    int U, units, chunks;
-    int64_t uv;
-    score_geometry(shape, &U, &units, &uv, &chunks);
-    const size_t b = fkv::score_workspace_doubles(n_dyn, shape->hist_frames, units, chunks) * sizeof(double);
-    *bytes = (b + 255) & ~(size_t)255;
+    *bytes = score_bytes(shape, n_dyn);
     return ok();
 }
 
-fkv_status fkv_score_segments(const fkv_shape *shape, const fkv_head *heads, const void *K_hist,
-                              const int32_t *frame_slot, const void *K_cur, float *scores,
-                              void *workspace, size_t workspace_bytes, void *stream) {
-    fkv_status st;
-    if ((st = check_shape(shape)) != FKV_OK) return st;
-    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
-    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
-    size_t need = 0;
-    if ((st = fkv_score_workspace_size(shape, heads, &need)) != FKV_OK) return st;
-    if (need == 0) return ok();  // no dynamic head, or nothing cached yet
-    if (!K_hist || !K_cur || !scores) return fail(FKV_ERR_ARG, "NULL tensor pointer");
-    if (!workspace) return fail(FKV_ERR_ARG, "workspace is NULL");
-    if (workspace_bytes < need)
-        return fail(FKV_ERR_CAPACITY, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+}  // extern "C"
 
+namespace {
+
+// Scoring of the heads in `list` (per head, or pooled into one row).
+fkv_status score_impl(const fkv_shape *shape, const fkv::HeadList &list, bool pooled, const void *K_hist,
+                      const int32_t *frame_slot, const void *K_cur, float *scores, void *workspace,
+                      void *stream, const char *what) {
     fkv::ScoreArgs a;
     memset(&a, 0, sizeof a);
-    for (int h = 0; h < shape->n_heads; ++h)
-        if (heads[h].type == FKV_DYNAMIC) a.heads.head[a.heads.n++] = h;
+    a.heads = list;
+    a.pooled = pooled ? 1 : 0;
     const size_t es = elem_size(shape);
     a.K_hist = (const uint8_t *)K_hist;
     a.K_cur = (const uint8_t *)K_cur;
@@ -321,14 +316,71 @@ fkv_status fkv_score_segments(const fkv_shape *shape, const fkv_head *heads, con
     score_geometry(shape, &a.unit_tokens, &a.units_per_frame, &a.unit_vecs, &a.chunks_per_unit);
     for (int t = 0; t < shape->hist_frames; ++t) a.slots.slot[t] = frame_slot[t];
     (void)hipGetLastError();
-    return device_status(fkv::launch_score(a, shape->dtype == FKV_F32, (hipStream_t)stream),
-                         "fkv_score_segments launch");
+    return device_status(fkv::launch_score(a, shape->dtype == FKV_F32, (hipStream_t)stream), what);
 }
 
-fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads, const float *scores,
-                              const void *K_hist, const void *V_hist, const int32_t *frame_slot,
-                              int32_t *kept_seg, void *Kc, void *Vc, int32_t slab, int32_t *kv_len,
-                              void *stream) {
+
+}  // namespace
+
+extern "C" {
+
+fkv_status fkv_score_segments(const fkv_shape *shape, const fkv_head *heads, const void *K_hist,
+                              const int32_t *frame_slot, const void *K_cur, float *scores,
+                              void *workspace, size_t workspace_bytes, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+    size_t need = 0;
+    if ((st = fkv_score_workspace_size(shape, heads, &need)) != FKV_OK) return st;
+    if (need == 0) return ok();  // no dynamic head, or nothing cached yet
+    if (!K_hist || !K_cur || !scores) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (!workspace) return fail(FKV_ERR_ARG, "workspace is NULL");
+    if (workspace_bytes < need)
+        return fail(FKV_ERR_CAPACITY, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    fkv::HeadList list;
+    memset(&list, 0, sizeof list);
+    for (int h = 0; h < shape->n_heads; ++h)
+        if (heads[h].type == FKV_DYNAMIC) list.head[list.n++] = h;
+    return score_impl(shape, list, false, K_hist, frame_slot, K_cur, scores, workspace, stream,
+                      "fkv_score_segments launch");
+}
+
+fkv_status fkv_score_pooled_workspace_size(const fkv_shape *shape, size_t *bytes) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if (!bytes) return fail(FKV_ERR_ARG, "bytes is NULL");
+    *bytes = score_bytes(shape, shape->n_heads);
+    return ok();
+}
+
+fkv_status fkv_score_pooled(const fkv_shape *shape, const void *K_hist, const int32_t *frame_slot,
+                            const void *K_cur, float *scores, void *workspace, size_t workspace_bytes,
+                            void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+    const size_t need = score_bytes(shape, shape->n_heads);
+    if (need == 0) return ok();  // nothing cached yet
+    if (!K_hist || !K_cur || !scores) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (!workspace) return fail(FKV_ERR_ARG, "workspace is NULL");
+    if (workspace_bytes < need)
+        return fail(FKV_ERR_CAPACITY, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    fkv::HeadList list;
+    memset(&list, 0, sizeof list);
+    for (int h = 0; h < shape->n_heads; ++h) list.head[list.n++] = h;
+    return score_impl(shape, list, true, K_hist, frame_slot, K_cur, scores, workspace, stream,
+                      "fkv_score_pooled launch");
+}
+
+}  // extern "C"
+
+namespace {
+
+fkv_status select_compact_impl(const fkv_shape *shape, const fkv_head *heads, const float *scores,
+                               bool shared_row, const void *K_hist, const void *V_hist,
+                               const int32_t *frame_slot, int32_t *kept_seg, void *Kc, void *Vc,
+                               int32_t slab, int32_t *kv_len, void *stream) {
     fkv_status st;
     if ((st = check_shape(shape)) != FKV_OK) return st;
     if ((st = check_heads(shape, heads)) != FKV_OK) return st;
@@ -361,6 +413,7 @@ fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads, con
     if (sa.heads.n == 0) return ok();
     (void)hipGetLastError();
     sa.scores = scores;
+    sa.score_stride = shared_row ? 0 : n_seg;
     sa.kept_seg = kept_seg;
     sa.kv_len = kv_len;
     sa.F = shape->frame_tokens;
@@ -394,6 +447,26 @@ fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads, con
     for (int t = 0; t < shape->hist_frames; ++t) ca.slots.slot[t] = frame_slot[t];
     return device_status(fkv::launch_dyn_copy(ca, max_pieces, (hipStream_t)stream),
                          "fkv_select_compact copy launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads, const float *scores,
+                              const void *K_hist, const void *V_hist, const int32_t *frame_slot,
+                              int32_t *kept_seg, void *Kc, void *Vc, int32_t slab, int32_t *kv_len,
+                              void *stream) {
+    return select_compact_impl(shape, heads, scores, false, K_hist, V_hist, frame_slot, kept_seg, Kc, Vc,
+                               slab, kv_len, stream);
+}
+
+fkv_status fkv_select_compact_pooled(const fkv_shape *shape, const fkv_head *heads, const float *scores,
+                                     const void *K_hist, const void *V_hist, const int32_t *frame_slot,
+                                     int32_t *kept_seg, void *Kc, void *Vc, int32_t slab,
+                                     int32_t *kv_len, void *stream) {
+    return select_compact_impl(shape, heads, scores, true, K_hist, V_hist, frame_slot, kept_seg, Kc, Vc,
+                               slab, kv_len, stream);
 }
 
 fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes) {

@@ -56,7 +56,8 @@ struct DynCopyArgs {
 
 // ---------------------------------------------------------------- selection
 struct SelectArgs {
-    const float *scores;            // [n_heads][n_seg]
+    const float *scores;            // head h's row at scores + h * score_stride
+    int64_t score_stride;           // n_seg, or 0 when all heads share one row
     int32_t *kept_seg;              // [n_heads][n_seg]
     int32_t *kv_len;                // [n_heads]
     int32_t F, L, H, n_seg;
@@ -78,6 +79,7 @@ struct ScoreArgs {
     int32_t units_per_frame;        // F / U
     int32_t chunks_per_unit;        // ceil(unit_vecs / 256)
     int32_t esize;
+    int32_t pooled;                 // 1: one score per segment over all listed heads, scores[n_seg]
     HeadList heads;
     SlotTable slots;
 };

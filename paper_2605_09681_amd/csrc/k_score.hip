@@ -1,5 +1,5 @@
 // k_score.hip -- segment-wise cosine similarity of adjacent frames for dynamic
-// heads (Sec. 4.3, Eq. 3).
+// heads (Sec. 4.3, Eq. 3), per head or pooled over all heads.
 //
 // Segment g of the history is compared with the same token range one frame
 // later.  Splitting every frame into units of U = min(L, F) tokens (a unit is
@@ -22,6 +22,10 @@
 // Pass 2 (score_finalize_kernel) sums the partials of each segment in a fixed
 // order, forms dot / sqrt(na*nb) in fp64 (0 when na*nb == 0) and rounds once
 // to fp32 (nearest even).  The result is deterministic run to run.
+//
+// The first-block proxy of Sec. 4.3 (scores pooled over heads) runs the same
+// two passes over every head and sums the partials of all heads of a segment
+// before the cosine.
 #include "fkv_internal.h"
 
 namespace fkv {
@@ -144,13 +148,13 @@ __global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
     }
 }
 
-// One workgroup per (segment, dynamic head): every thread sums a strided slice
-// of the segment's partials, then a fixed-order tree over the workgroup; the
-// result does not depend on timing.
+// One workgroup per (segment, listed head), or per segment when the score is
+// pooled over all listed heads: every thread sums a strided slice of the
+// segment's partials, then a fixed-order tree over the workgroup; the result
+// does not depend on timing.
 __global__ __launch_bounds__(kThreads) void score_finalize_kernel(ScoreArgs a) {
     __shared__ double red[3][kThreads];
-    const int g = blockIdx.x, li = blockIdx.y;
-    const int h = a.heads.head[li];
+    const int g = blockIdx.x;
     const int tid = threadIdx.x;
     const int nparts = a.chunks_per_unit * kWaves;
     int t0, t1, u;
@@ -164,10 +168,14 @@ __global__ __launch_bounds__(kThreads) void score_finalize_kernel(ScoreArgs a) {
         t1 = min(t0 + m, a.H);
         u = 0;
     }
-    const int n = (t1 - t0) * nparts;
+    const int li0 = a.pooled ? 0 : blockIdx.y;
+    const int nli = a.pooled ? a.heads.n : 1;
+    const int per_head = (t1 - t0) * nparts;
+    const int n = nli * per_head;
     double dot = 0.0, na = 0.0, nb = 0.0;
     for (int i = tid; i < n; i += kThreads) {
-        const int t = t0 + i / nparts, k = i % nparts;
+        const int li = li0 + i / per_head, j = i % per_head;
+        const int t = t0 + j / nparts, k = j % nparts;
         const double *pa = a.ws + ws_index(a, li, t, u, 0, 0) * 2;
         const double *pb = a.ws + ws_index(a, li, t + 1, u, 0, 0) * 2;
         na += pa[2 * k];
@@ -189,7 +197,8 @@ __global__ __launch_bounds__(kThreads) void score_finalize_kernel(ScoreArgs a) {
     if (tid == 0) {
         const double prod = red[1][0] * red[2][0];
         const double cosv = prod == 0.0 ? 0.0 : red[0][0] / sqrt(prod);
-        a.scores[(int64_t)h * a.n_seg + g] = (float)cosv;
+        const int64_t row = a.pooled ? 0 : (int64_t)a.heads.head[li0] * a.n_seg;
+        a.scores[row + g] = (float)cosv;
     }
 }
 
@@ -208,7 +217,7 @@ hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s) {
         hipLaunchKernelGGL(score_partials_kernel<false>, grid, dim3(kThreads), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(score_finalize_kernel, dim3(a.n_seg, a.heads.n), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(score_finalize_kernel, dim3(a.n_seg, a.pooled ? 1 : a.heads.n), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -43,7 +43,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
     const int segs_per_frame = per_frame ? a.F / a.L : 0;
 
     for (int g = tid; g < n; g += kThreads) {
-        s[g] = a.scores[(int64_t)h * n + g];
+        s[g] = a.scores[(int64_t)h * a.score_stride + g];
         const int64_t x0 = (int64_t)g * a.L;
         const int64_t x1 = x0 + a.L < HF ? x0 + a.L : HF;
         const int first = (int)(x0 / a.F), last = (int)((x1 - 1) / a.F);

@@ -123,6 +123,29 @@ def test_capacity_errors(fkv):
                                         need - 1, None) == 3
 
 
+def test_pooled_entry_point_errors(fkv):
+    """The first-block proxy path validates like the per-head path."""
+    shape = _shape(fkv)
+    heads = _heads(fkv)
+    L = fkv.lib()
+    sl = (ctypes.c_int32 * 4)(0, 1, 2, 3)
+    need = fkv.fkv_score_pooled_workspace_size(shape)
+    # all heads are pooled, so the workspace is larger than the per-head one (1 dynamic head)
+    assert need > fkv.fkv_score_workspace_size(shape, heads) and need % 256 == 0
+    assert L.fkv_score_pooled(ctypes.byref(shape), FAKE, sl, FAKE, FAKE, FAKE, need - 1, None) == 3
+    assert L.fkv_score_pooled(ctypes.byref(shape), FAKE, sl, FAKE, FAKE, None, need, None) == 1
+    assert L.fkv_score_pooled(ctypes.byref(shape), None, sl, FAKE, FAKE, FAKE, need, None) == 1
+    bad = (ctypes.c_int32 * 4)(0, 1, 4, 3)  # slot 4 is outside cap_frames = 4
+    assert L.fkv_score_pooled(ctypes.byref(shape), FAKE, bad, FAKE, FAKE, FAKE, need, None) == 1
+    empty = _shape(fkv, hist_frames=0)
+    assert fkv.fkv_score_pooled_workspace_size(empty) == 0
+    assert L.fkv_score_pooled(ctypes.byref(empty), None, None, None, None, None, 0, None) == 0
+    assert L.fkv_select_compact_pooled(ctypes.byref(shape), heads, FAKE, FAKE, FAKE, sl, FAKE, FAKE,
+                                       FAKE, 127, FAKE, None) == 3
+    assert L.fkv_select_compact_pooled(ctypes.byref(shape), heads, None, FAKE, FAKE, sl, FAKE, FAKE,
+                                       FAKE, 1 << 20, FAKE, None) == 1
+
+
 def test_attention_arg_errors(fkv):
     shape = _shape(fkv)
     L = fkv.lib()

@@ -285,3 +285,84 @@ def test_rollout_ring_buffer_sampled():
         _print_case("rollout", chunk=chunk, H=H)
         x = W.make_layer_inputs(cfg, seed=100 + chunk, frame_slot=slots, extra=(chunk, layer_idx))
         check_layer(cfg, x, rows=sample_rows(cfg.lq, 4, seed=chunk))
+
+
+# ---------------------------------------------------------------------------
+# the first-block proxy (Sec. 4.3): one similarity row pooled over all heads,
+# reused by the dynamic heads of another layer
+# ---------------------------------------------------------------------------
+def _pooled_gpu(cfg, x):
+    import paper_2605_09681_amd as fkv
+    shape = fkv.make_shape(cfg.n_heads, cfg.head_dim, cfg.frame_tokens, cfg.hist_frames,
+                           cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype)
+    d = dev_inputs(x)
+    scores = torch.full((fkv.fkv_num_segments(shape),), float("nan"), dtype=torch.float32, device="cuda")
+    fkv.fkv_score_pooled(shape, d["K_hist"], x.frame_slot, d["K_cur"], scores)
+    torch.cuda.synchronize()
+    return from_dev(scores)
+
+
+def test_pooled_scores_480p():
+    cfg = W.wan_layer_config("480p")
+    _print_case("pooled-480p", seed=13)
+    x = W.make_layer_inputs(cfg, seed=13)
+    got = _pooled_gpu(cfg, x)
+    want, _ = oracle.score_pooled(x.K_hist, x.frame_slot, x.K_cur, cfg.hist_frames, cfg.seg_tokens)
+    np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("F,L", [(100, 25), (100, 100), (100, 300)])
+def test_pooled_scores_small(dtype, F, L):
+    cfg = _small(F=F, L=L, d=64, dtype=dtype)
+    slot = np.array([3, 0, 8, 1, 5, 2, 7], np.int32)
+    _print_case("pooled-small", dtype=dtype, F=F, L=L)
+    x = W.make_layer_inputs(cfg, seed=L + 1, frame_slot=slot)
+    got = _pooled_gpu(cfg, x)
+    want, _ = oracle.score_pooled(x.K_hist, x.frame_slot, x.K_cur, cfg.hist_frames, L)
+    np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+def test_pooled_scores_reused_by_another_layer():
+    """Scores pooled from one layer's keys select the segments of a second
+    layer with other head types and budgets (fkv_select_compact_pooled):
+    kept ids, kv_len and compacted K/V bit-exact, then attention."""
+    import paper_2605_09681_amd as fkv
+    first = W.wan_layer_config("480p", seg_tokens=390)
+    _print_case("pooled-reuse")
+    x0 = W.make_layer_inputs(first, seed=14)
+    pooled = _pooled_gpu(first, x0)
+    heads = tuple(W.HeadBudget(W.DYNAMIC, 1, 0, 2, W.SCOPE_FRAME) if h % 3 else W.HeadBudget(W.STATIC, 1, 6)
+                  for h in range(12))
+    cfg = first.replace(heads=heads)
+    x = W.make_layer_inputs(cfg, seed=15)
+    layer = make_layer(cfg)
+    d = dev_inputs(x)
+    fkv.fkv_select_compact_pooled(layer.shape, layer.heads, torch.from_numpy(pooled).cuda(), d["K_hist"],
+                                  d["V_hist"], x.frame_slot, layer.kept_seg, layer.Kc, layer.Vc, layer.kv_len)
+    layer.compress_static(d["K_hist"], d["V_hist"], x.frame_slot)
+    O = torch.empty_like(d["Q"])
+    layer.attention(d["Q"], d["K_cur"], d["V_cur"], O)
+    torch.cuda.synchronize()
+    kept, kv = from_dev(layer.kept_seg), from_dev(layer.kv_len)
+    Kc, Vc = from_dev(layer.Kc), from_dev(layer.Vc)
+    H, F, L = cfg.hist_frames, cfg.frame_tokens, cfg.seg_tokens
+    rows = sample_rows(cfg.lq, 4, seed=15)
+    outs = []
+    for h, b in enumerate(heads):
+        if b.type == W.DYNAMIC:
+            want, cnt = oracle.select_head(pooled, H, F, L, b.sink_frames, b.recent_frames, b.keep_k, b.scope)
+            np.testing.assert_array_equal(kept[h], want, err_msg=f"head {h}")
+            kc = oracle.compact_head(x.K_hist[h], x.frame_slot, want[:cnt], H, L)
+            vc = oracle.compact_head(x.V_hist[h], x.frame_slot, want[:cnt], H, L)
+        else:
+            frames = oracle.static_frames(H, b.sink_frames, b.recent_frames)
+            kc = oracle.gather_frames(x.K_hist[h], x.frame_slot, frames)
+            vc = oracle.gather_frames(x.V_hist[h], x.frame_slot, frames)
+        assert int(kv[h]) == kc.shape[0]
+        np.testing.assert_array_equal(Kc[h, :kc.shape[0]], kc)
+        np.testing.assert_array_equal(Vc[h, :kc.shape[0]], vc)
+        outs.append(oracle.attention_rows(x.Q[h], kc, vc, x.K_cur[h], x.V_cur[h], 1 / math.sqrt(128), rows))
+    ref = oracle.LayerResult(None, None, None, None, None, None, rows,
+                             np.stack([o[0] for o in outs]), np.stack([o[1] for o in outs]))
+    assert_attention_close(O, ref, "bf16")
