@@ -46,6 +46,8 @@ def parse():
     p.add_argument("--cpu-rows", type=int, default=4680,
                    help="query rows per head in the CPU oracle sample (4680 = every row at 480P)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-extras", action="store_true",
+                   help="skip the extra measurements (pooled proxy scoring, uncompressed attention)")
     p.add_argument("--schedule", default="balanced", choices=["balanced", "per-item"],
                    help="attention work schedule (balanced needs the attention workspace)")
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "attention_traffic.json"),
@@ -172,6 +174,8 @@ def main():
 
     stage = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(4)] for e in events])  # ms
     score_ms, select_ms, static_ms, attn_ms = stage.mean(axis=0).tolist()
+    p10, p50, p90 = np.percentile(stage, [10, 50, 90], axis=0)
+    extras = None if args.no_extras else measure_extras(args, cfg, x, bufs, layers, stream)
 
     # algorithmic work per unit
     kv_len = layers[0].kv_len.cpu().numpy().astype(np.int64)
@@ -239,12 +243,71 @@ def main():
             "compress_static": round(static_copy_bytes / (static_ms * 1e-3) / 1e9, 1),
             "peak": PEAK_HBM_GBS,
         },
+        "breakdown_ms_p10_p50_p90": {
+            k: [round(float(p10[j]), 4), round(float(p50[j]), 4), round(float(p90[j]), 4)]
+            for j, k in enumerate(("score_segments", "select_compact", "compress_static", "chunk_attention"))},
         "attn_tflops": round(attn_tflops, 1),
         "ms_per_chunk_extrapolated_30layers_4steps": round(wall_ms * 120, 2),
     }
+    if extras is not None:
+        ua = extras["uncompressed_attention"]
+        ua["speedup_of_compressed"] = round(ua["ms"] / attn_ms, 3)
+        out["extras"] = extras
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, x, args.cpu_rows)
     print(json.dumps(out), flush=True)
+
+
+def _time_ms(fn, reps, stream):
+    """Mean ms of fn() over reps launches, HIP events on the launch stream."""
+    import torch
+    for _ in range(3):
+        fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def measure_extras(args, cfg, x, bufs, layers, stream):
+    """Measurements outside the step: the first-block proxy (scores pooled over
+    all heads, computed once per chunk and shared by every layer) and the same
+    attention kernel on the uncompressed cache (every head keeps all H frames),
+    for the kernel-level speedup of the compression."""
+    import numpy as np
+    import torch
+    import workloads as W
+    import paper_2605_09681_amd as fkv
+    from paper_2605_09681_amd.layer import CompressedLayer
+
+    d, F, H, Lq = cfg.head_dim, cfg.frame_tokens, cfg.hist_frames, cfg.lq
+    L0, b = layers[0], bufs[0]
+    pooled = torch.empty((L0.n_seg,), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(fkv.fkv_score_pooled_workspace_size(L0.shape), 1), dtype=torch.uint8, device="cuda")
+    pooled_ms = _time_ms(lambda: fkv.fkv_score_pooled(L0.shape, b["K_hist"], x.frame_slot, b["K_cur"], pooled, ws),
+                         20, stream)
+    pooled_bytes = cfg.n_heads * (H + 1) * F * d * 2
+
+    full_heads = tuple(W.HeadBudget(W.STATIC, 0, H) for _ in range(cfg.n_heads))
+    full = CompressedLayer(cfg.n_heads, d, F, H, cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype,
+                           full_heads, balanced=args.schedule == "balanced")
+    full.compress_static(b["K_hist"], b["V_hist"], x.frame_slot)
+    O = torch.empty_like(b["Q"])
+    full_ms = _time_ms(lambda: full.attention(b["Q"], b["K_cur"], b["V_cur"], O), 10, stream)
+    full_flop = 4.0 * Lq * d * cfg.n_heads * (H * F + Lq)
+    del full
+    return {
+        "pooled_proxy_score": {
+            "ms": round(pooled_ms, 4), "GB_s": round(pooled_bytes / (pooled_ms * 1e-3) / 1e9, 1),
+            "note": "all 12 heads pooled, once per AR step for all layers (not part of the step)"},
+        "uncompressed_attention": {
+            "ms": round(full_ms, 4), "TFLOP_s": round(full_flop / (full_ms * 1e-3) / 1e12, 1),
+            "kv_len": H * F},
+    }
 
 
 def _kernel_sha():
