@@ -159,6 +159,19 @@ fkv_status fkv_select_compact(const fkv_shape *shape, const fkv_head *heads,
                               int32_t *kept_seg, void *Kc, void *Vc, int32_t slab,
                               int32_t *kv_len, void *stream);
 
+/* Rolling cache write (the cache keeps a fixed window of past frames, the
+ * sink frame(s) pinned; Sec. 4): frame f of K_new / V_new, laid out
+ * [n_heads][n_frames*F][d] (a finished chunk's K_cur / V_cur with n_frames =
+ * C), is copied into physical slot dst_slot[f] of K_hist / V_hist for every
+ * head, overwriting that slot.  dst_slot is a HOST array of n_frames distinct
+ * slots in [0, cap_frames); 0 <= n_frames <= cap_frames.  The caller then
+ * describes the new logical order with frame_slot on the next calls (the
+ * write pointer advances; no cached frame moves). */
+fkv_status fkv_append_frames(const fkv_shape *shape, const void *K_new,
+                             const void *V_new, int32_t n_frames,
+                             const int32_t *dst_slot, void *K_hist, void *V_hist,
+                             void *stream);
+
 /* Device workspace fkv_score_pooled needs for `shape` (a multiple of 256
  * bytes; 0 when H = 0). */
 fkv_status fkv_score_pooled_workspace_size(const fkv_shape *shape, size_t *bytes);

@@ -62,6 +62,8 @@ def lib():
         L.fkvo_n_segments.restype = I
         L.fkvo_score_head.argtypes = [I, I, I, I, I, P, P, P, P, P]
         L.fkvo_score_head.restype = None
+        L.fkvo_append_frames.argtypes = [I, I, I, I, P, P, P]
+        L.fkvo_append_frames.restype = None
         L.fkvo_score_pooled.argtypes = [I, I, I, I, I, I, I, LG, P, P, P, P, P]
         L.fkvo_score_pooled.restype = None
         L.fkvo_select_head.argtypes = [I, I, I, I, I, I, I, P, P]
@@ -135,6 +137,19 @@ def score_head(hist_head: np.ndarray, frame_slot: np.ndarray, cur_head: np.ndarr
     lib().fkvo_score_head(_dt(hist_head), d, F, H, L, _ptr(hist_head), _ptr(slot),
                           _ptr(cur_head), _ptr(s32), _ptr(s64))
     return s32[:n].copy(), s64[:n].copy()
+
+
+def append_frames(hist_head: np.ndarray, new_frames: np.ndarray, dst_slot: np.ndarray) -> None:
+    """Rolling cache: writes new_frames[f] ([n][F][d]) into slot dst_slot[f] of
+    hist_head ([cap][F][d]) in place."""
+    assert hist_head.flags.c_contiguous and hist_head.flags.writeable
+    new_frames = _c(new_frames)
+    n, F, d = new_frames.shape
+    assert new_frames.dtype == hist_head.dtype and hist_head.shape[1:] == (F, d)
+    slot = _c(dst_slot, np.int32)
+    assert slot.shape == (n,) and ((slot >= 0) & (slot < hist_head.shape[0])).all()
+    lib().fkvo_append_frames(hist_head.dtype.itemsize, F, d, n, _ptr(new_frames), _ptr(slot),
+                             _ptr(hist_head))
 
 
 def score_pooled(hist: np.ndarray, frame_slot: np.ndarray, cur: np.ndarray, H: int, L: int):

@@ -116,6 +116,21 @@ void fkvo_score_head(int dtype, int d, int F, int H, int L, const void *hist,
 }
 
 /* ---------------------------------------------------------------------------
+ * Rolling cache (Sec. 4, the cache keeps a fixed window of past frames with
+ * the sink frames pinned): the frames of a finished chunk are written into
+ * the physical slots given for them, overwriting what those slots held.
+ * new_frames: [n_frames][F][d]; hist: [cap][F][d].
+ * ------------------------------------------------------------------------- */
+void fkvo_append_frames(int esize, int F, int d, int n_frames,
+                        const void *new_frames, const int32_t *dst_slot,
+                        void *hist) {
+    const size_t frame_bytes = (size_t)F * d * esize;
+    for (int f = 0; f < n_frames; ++f)
+        memcpy((char *)hist + (size_t)dst_slot[f] * frame_bytes,
+               (const char *)new_frames + (size_t)f * frame_bytes, frame_bytes);
+}
+
+/* ---------------------------------------------------------------------------
  * The first-block proxy of Sec. 4.3: the similarity is computed from the key
  * states of all attention heads together, i.e. the segment is the matrix
  * heads x tokens x head_dim and its cosine is taken over all of those

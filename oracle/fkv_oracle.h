@@ -53,6 +53,12 @@ void fkvo_score_head(int dtype, int d, int F, int H, int L, const void *hist,
                      const int32_t *frame_slot, const void *cur, float *s32,
                      double *s64);
 
+/* Rolling cache: writes frame f of new_frames ([n_frames][F][d]) into
+ * physical slot dst_slot[f] of hist ([cap][F][d]). */
+void fkvo_append_frames(int esize, int F, int d, int n_frames,
+                        const void *new_frames, const int32_t *dst_slot,
+                        void *hist);
+
 /* The first-block proxy of Sec. 4.3: one similarity per segment from the keys
  * of all heads together (the cosine over heads x tokens x head_dim elements).
  * hist: [n_heads][cap][F][d]; cur: [n_heads][lq][d]; s32/s64: [n_seg]. */

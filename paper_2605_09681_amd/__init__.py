@@ -13,6 +13,7 @@ Entry points (see ``include/fkv.h`` for the full contract):
 * :func:`fkv_score_segments`   -- segment similarity (Sec. 4.3, Eq. 3)
 * :func:`fkv_select_compact`   -- BottomK + compaction (Sec. 4.3, Eq. 3)
 * :func:`fkv_chunk_attention`  -- chunk attention (Eq. 2 / Eq. 4)
+* :func:`fkv_append_frames`    -- rolling-cache write of a finished chunk
 * :func:`fkv_score_pooled`, :func:`fkv_select_compact_pooled` -- the
   first-block proxy of Sec. 4.3: one similarity row pooled over all heads,
   shared by the dynamic heads of every layer
@@ -36,7 +37,8 @@ FKV_MAX_HEADS, FKV_MAX_FRAMES, FKV_MAX_SEGMENTS = 64, 256, 4096
 
 EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_score_workspace_size", "fkv_score_segments", "fkv_select_compact",
-            "fkv_score_pooled_workspace_size", "fkv_score_pooled", "fkv_select_compact_pooled",
+            "fkv_append_frames", "fkv_score_pooled_workspace_size", "fkv_score_pooled",
+            "fkv_select_compact_pooled",
             "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_last_error")
 
 
@@ -89,6 +91,8 @@ def lib():
         L.fkv_score_segments.restype = ctypes.c_int
         L.fkv_select_compact.argtypes = [S, Hd, P, P, P, P, P, P, P, I32, P, P]
         L.fkv_select_compact.restype = ctypes.c_int
+        L.fkv_append_frames.argtypes = [S, P, P, I32, P, P, P, P]
+        L.fkv_append_frames.restype = ctypes.c_int
         L.fkv_score_pooled_workspace_size.argtypes = [S, ctypes.POINTER(SZ)]
         L.fkv_score_pooled_workspace_size.restype = ctypes.c_int
         L.fkv_score_pooled.argtypes = [S, P, P, P, P, P, SZ, P]
@@ -226,6 +230,20 @@ def fkv_score_segments(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, score
     _raise(lib().fkv_score_segments(ctypes.byref(shape), heads, kh, sl, kc, sc, ws,
                                     workspace.numel(), _stream(stream)))
     return workspace
+
+
+def fkv_append_frames(shape: fkv_shape, K_new, V_new, dst_slot, K_hist, V_hist, stream=None):
+    """Writes the frames of K_new / V_new ([n_heads][n*F][d]) into the cache
+    slots dst_slot (host ints, one per frame)."""
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    slots = [int(v) for v in dst_slot]
+    n = len(slots)
+    new = (shape.n_heads, n * shape.frame_tokens, shape.head_dim)
+    kn, vn = _check(K_new, "K_new", dt, new), _check(V_new, "V_new", dt, new)
+    kh, vh = _check(K_hist, "K_hist", dt, hist), _check(V_hist, "V_hist", dt, hist)
+    arr = (ctypes.c_int32 * max(n, 1))(*slots)
+    _raise(lib().fkv_append_frames(ctypes.byref(shape), kn, vn, n, arr, kh, vh, _stream(stream)))
 
 
 def fkv_score_pooled_workspace_size(shape: fkv_shape) -> int:

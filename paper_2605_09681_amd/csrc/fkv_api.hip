@@ -469,6 +469,37 @@ fkv_status fkv_select_compact_pooled(const fkv_shape *shape, const fkv_head *hea
                                slab, kv_len, stream);
 }
 
+fkv_status fkv_append_frames(const fkv_shape *shape, const void *K_new, const void *V_new, int32_t n_frames,
+                             const int32_t *dst_slot, void *K_hist, void *V_hist, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if (n_frames < 0 || n_frames > shape->cap_frames)
+        return fail(FKV_ERR_ARG, "n_frames %d outside [0, cap_frames=%d]", n_frames, shape->cap_frames);
+    if (n_frames == 0) return ok();
+    if (!K_new || !V_new || !K_hist || !V_hist) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (!dst_slot) return fail(FKV_ERR_ARG, "dst_slot is NULL");
+    bool used[FKV_MAX_FRAMES] = {};
+    for (int f = 0; f < n_frames; ++f) {
+        const int sl = dst_slot[f];
+        if (sl < 0 || sl >= shape->cap_frames)
+            return fail(FKV_ERR_ARG, "dst_slot[%d] = %d outside [0, %d)", f, sl, shape->cap_frames);
+        if (used[sl]) return fail(FKV_ERR_ARG, "dst_slot[%d] = %d is given twice", f, sl);
+        used[sl] = true;
+    }
+    fkv::AppendArgs a;
+    memset(&a, 0, sizeof a);
+    a.K_new = (const uint8_t *)K_new;
+    a.V_new = (const uint8_t *)V_new;
+    a.K_hist = (uint8_t *)K_hist;
+    a.V_hist = (uint8_t *)V_hist;
+    a.frame_vecs = (int64_t)shape->frame_tokens * shape->head_dim * elem_size(shape) / 16;
+    a.n_frames = n_frames;
+    a.cap = shape->cap_frames;
+    for (int f = 0; f < n_frames; ++f) a.slots.slot[f] = dst_slot[f];
+    (void)hipGetLastError();
+    return device_status(fkv::launch_append(a, shape->n_heads, (hipStream_t)stream), "fkv_append_frames launch");
+}
+
 fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes) {
     fkv_status st;
     if ((st = check_shape(shape)) != FKV_OK) return st;

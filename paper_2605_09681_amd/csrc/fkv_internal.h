@@ -54,6 +54,15 @@ struct DynCopyArgs {
     SlotTable slots;
 };
 
+// ------------------------------------------------------------ cache append
+struct AppendArgs {
+    const uint8_t *K_new, *V_new;   // [n_heads][n_frames*F][d]
+    uint8_t *K_hist, *V_hist;       // [n_heads][cap][F][d]
+    int64_t frame_vecs;             // 16-byte vectors per frame
+    int32_t n_frames, cap;
+    SlotTable slots;                // destination slot of new frame f
+};
+
 // ---------------------------------------------------------------- selection
 struct SelectArgs {
     const float *scores;            // head h's row at scores + h * score_stride
@@ -110,6 +119,7 @@ size_t score_workspace_doubles(int n_dyn, int H, int units_per_frame, int chunks
 
 hipError_t launch_static_copy(const StaticCopyArgs &a, int max_kept, hipStream_t s);
 hipError_t launch_dyn_copy(const DynCopyArgs &a, int max_pieces, hipStream_t s);
+hipError_t launch_append(const AppendArgs &a, int n_heads, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, hipStream_t s);
 hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s);
 hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s);

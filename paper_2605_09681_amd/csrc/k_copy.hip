@@ -1,6 +1,7 @@
-// k_copy.hip -- structured frame gather for static heads (Sec. 4.2, Eq. 2) and
+// k_copy.hip -- structured frame gather for static heads (Sec. 4.2, Eq. 2),
 // kept-segment compaction for dynamic heads (Sec. 4.3: the compressed cache is
-// the union of the kept segments of every history frame).
+// the union of the kept segments of every history frame), and the write of a
+// finished chunk's frames into the rolling cache's slots.
 //
 // Both are pure HBM copies: each byte of a retained K/V row is read once and
 // written once with 16-byte vector accesses.  A workgroup moves one tile of one
@@ -84,6 +85,15 @@ __global__ __launch_bounds__(kThreads) void dyn_copy_kernel(DynCopyArgs a) {
               (int64_t)blockIdx.x * kTile + threadIdx.x);
 }
 
+// grid: x = tile within a frame, y = new frame f, z = head.
+__global__ __launch_bounds__(kThreads) void append_kernel(AppendArgs a) {
+    const int f = blockIdx.y, h = blockIdx.z;
+    const int64_t src = ((int64_t)h * a.n_frames + f) * a.frame_vecs;
+    const int64_t dst = ((int64_t)h * a.cap + a.slots.slot[f]) * a.frame_vecs;
+    copy_tile((const u32x4 *)a.K_new + src, (const u32x4 *)a.V_new + src, (u32x4 *)a.K_hist + dst,
+              (u32x4 *)a.V_hist + dst, a.frame_vecs, (int64_t)blockIdx.x * kTile + threadIdx.x);
+}
+
 }  // namespace
 
 hipError_t launch_static_copy(const StaticCopyArgs &a, int max_kept, hipStream_t s) {
@@ -100,6 +110,13 @@ hipError_t launch_dyn_copy(const DynCopyArgs &a, int max_pieces, hipStream_t s) 
     const int64_t tiles = (a.piece_vecs + kTile - 1) / kTile;
     dim3 grid((unsigned)tiles, (unsigned)max_pieces, (unsigned)a.heads.n);
     hipLaunchKernelGGL(dyn_copy_kernel, grid, dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_append(const AppendArgs &a, int n_heads, hipStream_t s) {
+    if (a.n_frames == 0) return hipSuccess;
+    const unsigned tiles = (unsigned)((a.frame_vecs + kTile - 1) / kTile);
+    hipLaunchKernelGGL(append_kernel, dim3(tiles, (unsigned)a.n_frames, (unsigned)n_heads), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -146,6 +146,22 @@ def test_pooled_entry_point_errors(fkv):
                                        FAKE, 1 << 20, FAKE, None) == 1
 
 
+def test_append_frames_errors(fkv):
+    shape = _shape(fkv)
+    L = fkv.lib()
+    def call(n, slots, p=FAKE):
+        arr = (ctypes.c_int32 * max(n, 1))(*slots) if slots is not None else None
+        return L.fkv_append_frames(ctypes.byref(shape), p, FAKE, n, arr, FAKE, FAKE, None)
+    assert call(0, None, p=None) == 0          # nothing to write
+    assert call(5, [0, 1, 2, 3, 0]) == 1        # more frames than cap_frames = 4
+    assert call(2, [1, 1]) == 1                 # a slot given twice
+    assert "twice" in fkv.fkv_last_error()
+    assert call(2, [1, 4]) == 1                 # outside [0, cap_frames)
+    assert call(2, [0, -1]) == 1
+    assert call(1, None) == 1                   # NULL dst_slot
+    assert call(1, [0], p=None) == 1            # NULL tensor
+
+
 def test_attention_arg_errors(fkv):
     shape = _shape(fkv)
     L = fkv.lib()

@@ -366,3 +366,113 @@ def test_pooled_scores_reused_by_another_layer():
     ref = oracle.LayerResult(None, None, None, None, None, None, rows,
                              np.stack([o[0] for o in outs]), np.stack([o[1] for o in outs]))
     assert_attention_close(O, ref, "bf16")
+
+
+# ---------------------------------------------------------------------------
+# rolling cache maintained on the GPU through fkv_append_frames
+# ---------------------------------------------------------------------------
+def test_append_frames_bit_exact():
+    import paper_2605_09681_amd as fkv
+    cfg = _small(H=5, cap=7, C=3, d=64)
+    _print_case("append")
+    x = W.make_layer_inputs(cfg, seed=31)
+    layer = make_layer(cfg)
+    d = dev_inputs(x)
+    dst = [6, 2, 4]
+    fkv.fkv_append_frames(layer.shape, d["K_cur"], d["V_cur"], dst, d["K_hist"], d["V_hist"])
+    torch.cuda.synchronize()
+    K, V = x.K_hist.copy(), x.V_hist.copy()
+    F = cfg.frame_tokens
+    for h in range(cfg.n_heads):
+        oracle.append_frames(K[h], x.K_cur[h].reshape(3, F, -1), np.array(dst, np.int32))
+        oracle.append_frames(V[h], x.V_cur[h].reshape(3, F, -1), np.array(dst, np.int32))
+    np.testing.assert_array_equal(from_dev(d["K_hist"]), K)
+    np.testing.assert_array_equal(from_dev(d["V_hist"]), V)
+
+
+def test_gpu_rollout_with_rolling_cache():
+    """Eight chunks of a streaming rollout (window 7 frames, sink pinned,
+    2-frame chunks): the cache lives on the GPU and is advanced by
+    fkv_append_frames; the oracle keeps its own copy through its own append.
+    Every chunk's step (compression bit-exact, attention on every row) is
+    checked, across the point where the ring starts to rotate."""
+    import paper_2605_09681_amd as fkv
+    window, C, F, d, nh = 7, 2, 64, 64, 4
+    n_chunks = 8
+    heads = (W.HeadBudget(W.STATIC, 1, 2), W.HeadBudget(W.DYNAMIC, 1, 0, 1, W.SCOPE_FRAME),
+             W.HeadBudget(W.DYNAMIC, 1, 0, 2, W.SCOPE_GLOBAL), W.HeadBudget(W.STATIC, 1, 1))
+    keys = W.ar1_key_frames(40, nh, n_chunks * C, F, d, 0.9, "bf16")       # [nh][frames][F][d]
+    vals = W.normal_tensor(40, 7, (nh, n_chunks * C, F, d), "bf16")
+    qs = W.normal_tensor(40, 8, (nh, n_chunks * C * F, d), "bf16")
+    K_o = np.zeros((nh, window, F, d), np.uint16)
+    V_o = np.zeros((nh, window, F, d), np.uint16)
+    K_g = torch.zeros((nh, window, F, d), dtype=torch.bfloat16, device="cuda")
+    V_g = torch.zeros_like(K_g)
+    for i in range(n_chunks):
+        slots = W.ring_frame_slots(i, C, window)
+        H = len(slots)
+        cfg = W.LayerConfig("roll", nh, d, F, H, window, C, 16, "bf16", heads, 0.9)
+        Kq = np.ascontiguousarray(keys[:, i * C:(i + 1) * C].reshape(nh, C * F, d))
+        Vq = np.ascontiguousarray(vals[:, i * C:(i + 1) * C].reshape(nh, C * F, d))
+        Q = np.ascontiguousarray(qs[:, i * C * F:(i + 1) * C * F])
+        x = W.LayerInputs(cfg, K_o.copy(), V_o.copy(), Kq, Vq, Q, slots)
+        _print_case("gpu-rollout", chunk=i, H=H)
+        layer = make_layer(cfg)
+        Kq_d, Vq_d, Q_d = to_dev(Kq, "bf16"), to_dev(Vq, "bf16"), to_dev(Q, "bf16")
+        O = torch.empty_like(Q_d)
+        lse = torch.empty((nh, C * F), dtype=torch.float32, device="cuda")
+        layer.step(K_g, V_g, slots, Q_d, Kq_d, Vq_d, O, lse)
+        torch.cuda.synchronize()
+        ref = oracle.run_layer(cfg, x, scale=1 / math.sqrt(d))
+        assert_compression_exact(cfg, layer, ref)
+        assert_attention_close(O, ref, "bf16", lse)
+        dst = W.chunk_write_slots(i, C, window)
+        fkv.fkv_append_frames(layer.shape, Kq_d, Vq_d, dst.tolist(), K_g, V_g)
+        for h in range(nh):
+            oracle.append_frames(K_o[h], Kq[h].reshape(C, F, d), dst)
+            oracle.append_frames(V_o[h], Vq[h].reshape(C, F, d), dst)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(from_dev(K_g), K_o)
+    np.testing.assert_array_equal(from_dev(V_g), V_o)
+
+
+# ---------------------------------------------------------------------------
+# comparison policies through the same kernels
+# ---------------------------------------------------------------------------
+def test_streaming_llm_budgets():
+    """3 sink + 4 recent frames on every head (frame-level StreamingLLM)."""
+    cfg = W.wan_layer_config("480p").replace(heads=W.streaming_llm_heads(12))
+    _print_case("streaming-llm")
+    layer, _, _, _ = check_layer(cfg, W.make_layer_inputs(cfg, seed=16), rows=sample_rows(cfg.lq, 8, seed=16))
+    assert (from_dev(layer.kv_len) == 7 * cfg.frame_tokens).all()
+
+
+@pytest.mark.parametrize("policy", ["random", "uniform"])
+def test_random_and_uniform_segment_pruning(policy):
+    """BottomK fed with seeded random scores (random pruning) or an evenly
+    spaced pattern (uniform pruning) instead of similarities."""
+    cfg = W.wan_layer_config("480p", seg_tokens=260, keep_fraction=0.7)   # 6 segments per frame
+    _print_case("pruning-policy", policy=policy)
+    x = W.make_layer_inputs(cfg, seed=17)
+    n_seg = cfg.hist_frames * 6
+    dyn = [h for h, b in enumerate(cfg.heads) if b.type == W.DYNAMIC]
+    k = cfg.heads[dyn[0]].keep_k
+    scores = (W.random_scores(17, 12, n_seg) if policy == "random"
+              else W.uniform_scores(12, cfg.hist_frames, cfg.frame_tokens, 260, k))
+    layer = make_layer(cfg)
+    d = dev_inputs(x)
+    layer.scores.copy_(torch.from_numpy(scores))
+    layer.select_compact(d["K_hist"], d["V_hist"], x.frame_slot)
+    torch.cuda.synchronize()
+    kept, kv, Kc = from_dev(layer.kept_seg), from_dev(layer.kv_len), from_dev(layer.Kc)
+    for h in dyn:
+        b = cfg.heads[h]
+        want, cnt = oracle.select_head(scores[h], cfg.hist_frames, cfg.frame_tokens, 260, b.sink_frames,
+                                       b.recent_frames, b.keep_k, b.scope)
+        np.testing.assert_array_equal(kept[h], want)
+        kc = oracle.compact_head(x.K_hist[h], x.frame_slot, want[:cnt], cfg.hist_frames, 260)
+        assert int(kv[h]) == kc.shape[0]
+        np.testing.assert_array_equal(Kc[h, :kc.shape[0]], kc)
+        if policy == "uniform":   # kept segments within every non-sink frame: 0, 1, 3, 4 of 6 (k = 4)
+            sel = want[:cnt]
+            assert sorted(set((sel[sel >= 6] % 6).tolist())) == sorted({(i * 6) // k for i in range(k)})

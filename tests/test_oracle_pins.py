@@ -259,6 +259,40 @@ def test_score_ar1_statistic(oracle_lib):
 
 
 # ---------------------------------------------------------------------------
+# rolling cache: chunk frames written through the ring write pointer
+# ---------------------------------------------------------------------------
+def test_append_frames_matches_assignment(oracle_lib):
+    rng = np.random.default_rng(4)
+    hist = rng.standard_normal((6, 3, 4), dtype=np.float32)
+    want = hist.copy()
+    new = rng.standard_normal((2, 3, 4), dtype=np.float32)
+    slot = np.array([4, 1], np.int32)
+    oracle.append_frames(hist, new, slot)
+    want[slot] = new
+    np.testing.assert_array_equal(hist, want)
+
+
+@pytest.mark.parametrize("window,C,pinned", [(7, 2, 1), (21, 3, 1), (6, 3, 0), (9, 3, 2)])
+def test_ring_cache_holds_sink_and_latest_frames(oracle_lib, window, C, pinned):
+    """Writing each finished chunk through the write pointer keeps, in the
+    logical order of ring_frame_slots, the pinned sink frames followed by the
+    most recent frames: frame v is stamped with the value v."""
+    F, d = 2, 3
+    hist = np.full((window, F, d), -1.0, np.float32)
+    for i in range(12):
+        slots = W.ring_frame_slots(i, C, window, pinned)
+        produced = i * C
+        H = len(slots)
+        if H:
+            got = hist[slots][:, 0, 0].astype(int).tolist()
+            n_sink = min(pinned, H)
+            expect = list(range(n_sink)) + list(range(produced - (H - n_sink), produced))
+            assert got == expect, (i, got, expect)
+        chunk = np.arange(produced, produced + C, dtype=np.float32)[:, None, None] * np.ones((1, F, d), np.float32)
+        oracle.append_frames(hist, chunk, W.chunk_write_slots(i, C, window, pinned))
+
+
+# ---------------------------------------------------------------------------
 # Sec. 4.3 first-block proxy: one similarity from the keys of all heads
 # ---------------------------------------------------------------------------
 def _tiny_heads(dtype, n_heads, H, F, d, C, seed, rho=0.7):

@@ -296,3 +296,48 @@ def ring_frame_slots(chunk_index: int, chunk_frames: int, window: int,
     for v in range(first, produced):
         slots.append(pinned_sink + (v - pinned_sink) % ring)
     return np.asarray(slots, dtype=np.int32)
+
+
+def ring_slot(v: int, window: int, pinned_sink: int = 1) -> int:
+    """Physical slot of video frame ``v`` in the ring-buffer cache of
+    ``ring_frame_slots``: the first ``pinned_sink`` frames keep their slots, the
+    others rotate through the remaining ``window - pinned_sink`` slots."""
+    if v < pinned_sink:
+        return v
+    return pinned_sink + (v - pinned_sink) % (window - pinned_sink)
+
+
+def chunk_write_slots(chunk_index: int, chunk_frames: int, window: int,
+                      pinned_sink: int = 1) -> np.ndarray:
+    """Slots that receive the frames of chunk ``chunk_index`` once it is done
+    (the write pointer of the ring buffer)."""
+    assert window - pinned_sink >= chunk_frames, "a chunk must fit in the rotating part"
+    v0 = chunk_index * chunk_frames
+    return np.array([ring_slot(v, window, pinned_sink) for v in range(v0, v0 + chunk_frames)],
+                    dtype=np.int32)
+
+
+# ---------------------------------------------------------------------------
+# comparison policies expressed through the same budgets and selection inputs
+# ---------------------------------------------------------------------------
+def streaming_llm_heads(n_heads: int, sink_frames: int = 3, recent_frames: int = 4):
+    """StreamingLLM-style frame-level cache: every head keeps the same sink
+    and recent frames (3 + 4 in the paper's baseline setting)."""
+    return tuple(HeadBudget(STATIC, sink_frames, recent_frames) for _ in range(n_heads))
+
+
+def random_scores(seed: int, n_heads: int, n_seg: int) -> np.ndarray:
+    """Scores that turn BottomK into random segment pruning: i.i.d. uniform
+    draws (a seeded input, so both sides select the same segments)."""
+    return _rng(seed, 9).random((n_heads, n_seg), dtype=np.float32)
+
+
+def uniform_scores(n_heads: int, H: int, F: int, L: int, keep_k: int) -> np.ndarray:
+    """Scores that turn per-frame BottomK (L < F) into uniform pruning: in every
+    frame the segments floor(i * n / k), i < k, score 0 and the others 1, so the
+    k kept segments are spread evenly over the frame."""
+    n = F // L
+    row = np.ones(n, np.float32)
+    for i in range(min(keep_k, n)):
+        row[(i * n) // max(keep_k, 1)] = 0.0
+    return np.tile(np.tile(row, H), (n_heads, 1)).astype(np.float32)
