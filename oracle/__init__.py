@@ -28,7 +28,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "fkv_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-BF16, F32 = 0, 1
+BF16, F32, F64 = 0, 1, 2
 STATIC, DYNAMIC = 0, 1
 
 
@@ -87,7 +87,9 @@ def _dt(arr: np.ndarray) -> int:
         return BF16
     if arr.dtype == np.float32:
         return F32
-    raise TypeError(f"oracle takes uint16 (bf16 bits) or float32 storage, got {arr.dtype}")
+    if arr.dtype == np.float64:
+        return F64
+    raise TypeError(f"oracle takes uint16 (bf16 bits), float32 or float64, got {arr.dtype}")
 
 
 def _c(a, dtype=None):

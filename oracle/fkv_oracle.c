@@ -26,6 +26,7 @@ static double load_elem(const void *base, int dtype, size_t i) {
         memcpy(&f, &u, sizeof f);
         return (double)f;
     }
+    if (dtype == FKVO_F64) return ((const double *)base)[i];
     return (double)((const float *)base)[i];
 }
 

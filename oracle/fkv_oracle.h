@@ -14,7 +14,8 @@
  *   Eq. 4 / Eq. 2      attention of the current chunk's queries over
  *                      [compressed history; current chunk].
  *
- * Element storage: FKVO_BF16 = uint16 bf16 bit patterns, FKVO_F32 = float.
+ * Element storage: FKVO_BF16 = uint16 bf16 bit patterns, FKVO_F32 = float,
+ * FKVO_F64 = double (attention inputs only).
  * All tensors are row-major with head_dim innermost.
  */
 #ifndef FKV_ORACLE_H
@@ -29,6 +30,7 @@ extern "C" {
 
 #define FKVO_BF16 0
 #define FKVO_F32 1
+#define FKVO_F64 2  /* attention inputs only (dequantized FP8 values) */
 
 /* Kept logical frames of a static head: [0, sink) U [H - recent, H), ascending,
  * each frame once.  Writes at most H entries; returns the count. */
