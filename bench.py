@@ -292,6 +292,12 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
                          20, stream)
     pooled_bytes = cfg.n_heads * (H + 1) * F * d * 2
 
+    O8 = torch.empty_like(b["Q"])
+    pack_ms = _time_ms(lambda: L0.pack_fp8(b["Q"], b["K_cur"], b["V_cur"]), 20, stream)
+    fp8_ms = _time_ms(lambda: L0.attention_fp8_packed(O8), 20, stream)
+    kv_len = L0.kv_len.cpu().numpy().astype(np.int64)
+    attn_flop = 4.0 * Lq * d * float(np.sum(kv_len + Lq))
+
     full_heads = tuple(W.HeadBudget(W.STATIC, 0, H) for _ in range(cfg.n_heads))
     full = CompressedLayer(cfg.n_heads, d, F, H, cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype,
                            full_heads, balanced=args.schedule == "balanced")
@@ -301,6 +307,10 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
     full_flop = 4.0 * Lq * d * cfg.n_heads * (H * F + Lq)
     del full
     return {
+        "fp8_attention": {
+            "attention_ms": round(fp8_ms, 4), "TFLOP_s": round(attn_flop / (fp8_ms * 1e-3) / 1e12, 1),
+            "peak_TFLOP_s": 5000.0, "pack_ms": round(pack_ms, 4),
+            "note": "E4M3 Q/K/V/P on gfx950 FP8 MFMA; pack = statistics + quantise + transpose"},
         "pooled_proxy_score": {
             "ms": round(pooled_ms, 4), "GB_s": round(pooled_bytes / (pooled_ms * 1e-3) / 1e9, 1),
             "note": "all 12 heads pooled, once per AR step for all layers (not part of the step)"},

@@ -236,6 +236,51 @@ fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q,
                                float *lse, void *workspace, size_t workspace_bytes,
                                void *stream);
 
+/* ---------------------------------------------------------------------------
+ * FP8 variant of the chunk attention (App. F: the method combined with FP8
+ * attention), for the FP8 matrix cores of gfx950.  Two steps:
+ *
+ * fkv_fp8_pack quantises one layer's attention inputs per head to OCP FP8
+ * E4M3 (round to nearest even): keys [Kc[0:kv_len]; K_cur] after subtracting
+ * their per-channel mean mu (fp64 sum, one rounding to fp32; softmax is
+ * unchanged by it), scaled by inv_k = 448 / amax|K - mu|; queries by
+ * inv_q = 448 / amax|Q|; values per channel by inv_v[c] = 448 / amax_c|V|
+ * (correctly rounded fp32; 0 for an all-zero tensor or channel).
+ *   Q8     uint8 [n_heads][C*F][d]
+ *   K8     uint8 [n_heads][rows][d], rows = round_up(slab + C*F, 64): row j of
+ *          head h is key j of [Kc[h][0:kv_len]; K_cur[h]], rows past it zero
+ *   V8T    uint8 [n_heads][rows/64][d][64]: each 64-key tile transposed, its
+ *          keys in the order the attention kernel consumes them
+ *   scales float [n_heads][4 + 3d]: s_q, s_k, inv_q, inv_k, s_v[d], inv_v[d],
+ *          mu[d], with s = amax / 448
+ * Inputs are bf16 (FKV_ERR_SHAPE for FKV_F32).  kv_len is read on the device.
+ * The workspace (fkv_fp8_sizes) holds statistics and needs no initialisation.
+ *
+ * fkv_chunk_attention_fp8 computes, from those buffers,
+ *   O[h][r] = softmax(scale * (s_q s_k) q8 . k8^T) . (v8 * s_v)
+ * with FP8 products accumulated in fp32, fp32 online softmax, and the
+ * probabilities themselves rounded to E4M3 (relative error <= 2^-4) before
+ * the value product; the normaliser sums the same rounded probabilities.
+ * O is bf16 [n_heads][C*F][d]; lse as in fkv_chunk_attention.  The workspace
+ * selects the balanced schedule exactly as in fkv_chunk_attention (same size
+ * query, fkv_attention_workspace_size). */
+fkv_status fkv_fp8_sizes(const fkv_shape *shape, int32_t slab, size_t *q_bytes,
+                         size_t *kv_bytes, size_t *scale_bytes,
+                         size_t *workspace_bytes);
+
+fkv_status fkv_fp8_pack(const fkv_shape *shape, const void *Q, const void *Kc,
+                        const void *Vc, int32_t slab, const int32_t *kv_len,
+                        const void *K_cur, const void *V_cur, void *Q8, void *K8,
+                        void *V8T, float *scales, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
+fkv_status fkv_chunk_attention_fp8(const fkv_shape *shape, const void *Q8,
+                                   const void *K8, const void *V8T, int32_t slab,
+                                   const int32_t *kv_len, const float *scales,
+                                   float scale, void *O, float *lse,
+                                   void *workspace, size_t workspace_bytes,
+                                   void *stream);
+
 /* Message describing the calling thread's last non-OK status ("" if none). */
 const char *fkv_last_error(void);
 

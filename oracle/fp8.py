@@ -88,6 +88,9 @@ class Fp8Head:
     s_k: np.float32
     mu_k: np.ndarray    # [d] float32
     s_v: np.ndarray     # [d] float32
+    inv_q: np.float32 = np.float32(0)
+    inv_k: np.float32 = np.float32(0)
+    inv_v: np.ndarray = None  # [d] float32
 
 
 def quantize_head(Q, K, V) -> Fp8Head:
@@ -105,7 +108,8 @@ def quantize_head(Q, K, V) -> Fp8Head:
     k8 = e4m3_encode((Kt * inv_k).astype(np.float32))
     q8 = e4m3_encode((Q * inv_q).astype(np.float32))
     v8 = e4m3_encode((V * inv_v[None, :]).astype(np.float32))
-    return Fp8Head(q8, k8, v8, np.float32(s_q), np.float32(s_k), mu, s_v.astype(np.float32))
+    return Fp8Head(q8, k8, v8, np.float32(s_q), np.float32(s_k), mu, s_v.astype(np.float32),
+                   np.float32(inv_q), np.float32(inv_k), inv_v.astype(np.float32))
 
 
 def dequantized(h: Fp8Head):
@@ -114,11 +118,15 @@ def dequantized(h: Fp8Head):
             e4m3_decode(h.v8) * h.s_v.astype(np.float64)[None, :])
 
 
-def p_rounding_sigma(q, k, v, scale: float, rows) -> np.ndarray:
+def p_rounding_sigma(q, k, v, scale: float, rows, p_bias_log2: float = 6.0) -> np.ndarray:
     """Standard deviation, per output element, of the error that rounding every
-    probability to E4M3 (relative error uniform in +-2^-4) adds to a softmax-
-    weighted average normalised by the same rounded probabilities:
-        sigma_d = 2^-4/sqrt(3) * sqrt(sum_k p_k^2 (v_kd - o_d)^2) / sum_k p_k.
+    probability to E4M3 adds to a softmax-weighted average normalised by the
+    same rounded probabilities.  The probabilities are taken as
+    p'_k = 2^p_bias_log2 * exp(z_k - max z) (the kernel's scaling, whose lagging
+    running maximum only makes its values larger, i.e. rounded more finely);
+    a normal E4M3 value has relative error within +-2^-4, a subnormal one
+    (below 2^-6) absolute error within +-2^-10, both taken as uniform:
+        sigma_d = sqrt(sum_k var_k (v_kd - o_d)^2) / sum_k p'_k.
     q: [Lq][d]; k, v: [n_keys][d] (float64, dequantised); returns [n_rows][d]."""
     q = np.asarray(q, np.float64)
     k = np.asarray(k, np.float64)
@@ -126,7 +134,13 @@ def p_rounding_sigma(q, k, v, scale: float, rows) -> np.ndarray:
     out = np.empty((len(rows), v.shape[1]))
     for i, r in enumerate(rows):
         z = scale * (k @ q[r])
-        p = np.exp(z - z.max())
+        p = np.exp(z - z.max()) * 2.0 ** p_bias_log2
         o = (p @ v) / p.sum()
-        out[i] = 2.0 ** -4 / np.sqrt(3.0) * np.sqrt((p[:, None] ** 2 * (v - o[None, :]) ** 2).sum(axis=0)) / p.sum()
+        out[i] = np.sqrt((p_rounding_var(p)[:, None] * (v - o[None, :]) ** 2).sum(axis=0)) / p.sum()
     return out
+
+
+def p_rounding_var(p) -> np.ndarray:
+    """Variance of the E4M3 rounding error of each (scaled) probability."""
+    p = np.asarray(p, np.float64)
+    return np.where(p >= 2.0 ** -6, (2.0 ** -4 * p) ** 2, (2.0 ** -10) ** 2) / 3.0

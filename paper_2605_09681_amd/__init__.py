@@ -14,6 +14,8 @@ Entry points (see ``include/fkv.h`` for the full contract):
 * :func:`fkv_select_compact`   -- BottomK + compaction (Sec. 4.3, Eq. 3)
 * :func:`fkv_chunk_attention`  -- chunk attention (Eq. 2 / Eq. 4)
 * :func:`fkv_append_frames`    -- rolling-cache write of a finished chunk
+* :func:`fkv_fp8_pack`, :func:`fkv_chunk_attention_fp8` -- the FP8 variant of
+  the chunk attention (App. F)
 * :func:`fkv_score_pooled`, :func:`fkv_select_compact_pooled` -- the
   first-block proxy of Sec. 4.3: one similarity row pooled over all heads,
   shared by the dynamic heads of every layer
@@ -39,7 +41,8 @@ EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_score_workspace_size", "fkv_score_segments", "fkv_select_compact",
             "fkv_append_frames", "fkv_score_pooled_workspace_size", "fkv_score_pooled",
             "fkv_select_compact_pooled",
-            "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_last_error")
+            "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_fp8_sizes", "fkv_fp8_pack",
+            "fkv_chunk_attention_fp8", "fkv_last_error")
 
 
 class FkvLibraryMissing(RuntimeError):
@@ -103,6 +106,12 @@ def lib():
         L.fkv_attention_workspace_size.restype = ctypes.c_int
         L.fkv_chunk_attention.argtypes = [S, P, P, P, I32, P, P, P, F, P, P, P, SZ, P]
         L.fkv_chunk_attention.restype = ctypes.c_int
+        L.fkv_fp8_sizes.argtypes = [S, I32] + [ctypes.POINTER(SZ)] * 4
+        L.fkv_fp8_sizes.restype = ctypes.c_int
+        L.fkv_fp8_pack.argtypes = [S, P, P, P, I32, P, P, P, P, P, P, P, P, SZ, P]
+        L.fkv_fp8_pack.restype = ctypes.c_int
+        L.fkv_chunk_attention_fp8.argtypes = [S, P, P, P, I32, P, P, F, P, P, P, SZ, P]
+        L.fkv_chunk_attention_fp8.restype = ctypes.c_int
         L.fkv_last_error.argtypes = []
         L.fkv_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -330,6 +339,54 @@ def fkv_chunk_attention(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, scale
         ws, nws = _check(workspace, "workspace", torch.uint8), workspace.numel()
     _raise(lib().fkv_chunk_attention(ctypes.byref(shape), q, kc, vc, int(slab), kl, kq, vq,
                                      ctypes.c_float(scale), o, ls, ws, nws, _stream(stream)))
+
+
+def fkv_fp8_sizes(shape: fkv_shape, slab: int):
+    """(q_bytes, kv_bytes, scale_bytes, workspace_bytes) of the FP8 buffers."""
+    out = [ctypes.c_size_t(0) for _ in range(4)]
+    _raise(lib().fkv_fp8_sizes(ctypes.byref(shape), int(slab), *[ctypes.byref(o) for o in out]))
+    return tuple(int(o.value) for o in out)
+
+
+def fkv_fp8_pack(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, Q8, K8, V8T, scales,
+                 workspace, stream=None):
+    dt = _torch_dtype(shape)
+    chunk = (shape.n_heads, _lq(shape), shape.head_dim)
+    slab = Kc.shape[1] if Kc.dim() == 3 else -1
+    comp = (shape.n_heads, slab, shape.head_dim)
+    qb, kvb, sb, wb = fkv_fp8_sizes(shape, slab)
+    args = [_check(Q, "Q", dt, chunk), _check(Kc, "Kc", dt, comp), _check(Vc, "Vc", dt, comp), int(slab),
+            _check(kv_len, "kv_len", torch.int32, (shape.n_heads,)), _check(K_cur, "K_cur", dt, chunk),
+            _check(V_cur, "V_cur", dt, chunk)]
+    for t, name, nb in ((Q8, "Q8", qb), (K8, "K8", kvb), (V8T, "V8T", kvb)):
+        args.append(_check(t, name, torch.uint8))
+        if t.numel() != nb:
+            raise ValueError(f"{name} holds {t.numel()} bytes, {nb} expected")
+    args.append(_check(scales, "scales", torch.float32))
+    if scales.numel() * 4 != sb:
+        raise ValueError(f"scales holds {scales.numel() * 4} bytes, {sb} expected")
+    args += [_check(workspace, "workspace", torch.uint8), workspace.numel(), _stream(stream)]
+    _raise(lib().fkv_fp8_pack(ctypes.byref(shape), *args))
+
+
+def fkv_chunk_attention_fp8(shape: fkv_shape, Q8, K8, V8T, slab: int, kv_len, scales, scale: float, O,
+                            lse: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                            stream=None):
+    chunk = (shape.n_heads, _lq(shape), shape.head_dim)
+    qb, kvb, sb, _ = fkv_fp8_sizes(shape, slab)
+    for t, name, nb in ((Q8, "Q8", qb), (K8, "K8", kvb), (V8T, "V8T", kvb)):
+        _check(t, name, torch.uint8)
+        if t.numel() != nb:
+            raise ValueError(f"{name} holds {t.numel()} bytes, {nb} expected")
+    ls = None if lse is None else _check(lse, "lse", torch.float32, (shape.n_heads, _lq(shape)))
+    ws, nws = None, 0
+    if workspace is not None:
+        ws, nws = _check(workspace, "workspace", torch.uint8), workspace.numel()
+    _raise(lib().fkv_chunk_attention_fp8(
+        ctypes.byref(shape), _check(Q8, "Q8", torch.uint8), _check(K8, "K8", torch.uint8),
+        _check(V8T, "V8T", torch.uint8), int(slab), _check(kv_len, "kv_len", torch.int32, (shape.n_heads,)),
+        _check(scales, "scales", torch.float32), ctypes.c_float(scale), _check(O, "O", torch.bfloat16, chunk),
+        ls, ws, nws, _stream(stream)))
 
 
 def fkv_last_error() -> str:

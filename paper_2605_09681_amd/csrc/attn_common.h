@@ -1,0 +1,69 @@
+// attn_common.h -- pieces shared by the bf16 and FP8 chunk-attention kernels:
+// tile sizes, the balanced work schedule and the partial-result slot format
+// that attn_merge_kernel combines.
+#pragma once
+
+#include "fkv_internal.h"
+
+namespace fkv {
+namespace attn {
+
+constexpr int BM = kAttnRowsBf16;  // query rows per workgroup (8 waves x 32)
+constexpr int BN = 64;             // keys per tile
+
+// Number of key tiles of head h: [Kc[h][0:kv_len]; K_cur[h]] in tiles of BN.
+__device__ __forceinline__ int head_kvl(const AttnArgs &a, int h) {
+    const int kvl = a.kv_len[h];
+    return kvl < 0 ? 0 : (kvl > a.slab ? (int)a.slab : kvl);
+}
+__device__ __forceinline__ int head_tiles(const AttnArgs &a, int h) {
+    return (head_kvl(a, h) + a.Lq + BN - 1) / BN;
+}
+
+// Balanced schedule.  Work item i = (head h, query tile qt), h-major, has
+// T_h key tiles; concatenating all items gives one sequence of `total` tiles,
+// which G = min(n_blocks, total) workgroups split into equal contiguous ranges:
+// workgroup r takes tiles [r*total/G, (r+1)*total/G).  An item cut by a range
+// boundary is computed in parts whose unnormalised results are combined by
+// attn_merge_kernel.  Both kernels derive the same schedule from kv_len.
+struct Schedule {
+    int64_t total;
+    int G;
+    __device__ __forceinline__ int64_t start(int r) const { return (int64_t)r * total / G; }
+    // workgroup whose range holds tile x: the largest r with start(r) <= x
+    __device__ __forceinline__ int owner(int64_t x) const { return (int)(((x + 1) * G - 1) / total); }
+};
+
+__device__ __forceinline__ Schedule make_schedule(const AttnArgs &a) {
+    int64_t total = 0;
+    for (int h = 0; h < a.n_heads; ++h) total += (int64_t)a.n_qtiles * head_tiles(a, h);
+    Schedule sc;
+    sc.total = total;
+    sc.G = (int)(total < a.n_blocks ? total : a.n_blocks);
+    return sc;
+}
+
+// Partial result of one part of an item, in a slot of BM*(D/2 + 2) floats:
+// the part's own normalised output o/l rounded to bf16, in the accumulator
+// layout of the waves (4 values per lane and uint2 index
+// ((wave*MB + mb)*4 + g)*64 + lane), then the running max m (log2 units) of
+// the BM rows, then their probability sums l.
+template <int D>
+__device__ __forceinline__ size_t slot_floats() { return (size_t)BM * (D / 2 + 2); }
+
+__device__ __forceinline__ uint2 pack_bf16x4(float x0, float x1, float x2, float x3) {
+    const uint32_t b0 = __builtin_bit_cast(uint16_t, (__bf16)x0), b1 = __builtin_bit_cast(uint16_t, (__bf16)x1);
+    const uint32_t b2 = __builtin_bit_cast(uint16_t, (__bf16)x2), b3 = __builtin_bit_cast(uint16_t, (__bf16)x3);
+    return make_uint2(b0 | (b1 << 16), b2 | (b3 << 16));
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
+
+}  // namespace attn
+
+// Combines the partial results of the items the balanced schedule split (a
+// second kernel on the same stream); shared by the bf16 and FP8 paths.
+hipError_t launch_attention_merge(const AttnArgs &a, int head_dim, hipStream_t s);
+
+}  // namespace fkv

@@ -558,6 +558,103 @@ fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q, const void
     return device_status(e, "fkv_chunk_attention launch");
 }
 
+fkv_status fkv_fp8_sizes(const fkv_shape *shape, int32_t slab, size_t *q_bytes, size_t *kv_bytes,
+                         size_t *scale_bytes, size_t *workspace_bytes) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if (shape->dtype != FKV_BF16) return fail(FKV_ERR_SHAPE, "the FP8 path takes bf16 inputs");
+    if (slab < 0) return fail(FKV_ERR_ARG, "slab %d < 0", slab);
+    if (!q_bytes || !kv_bytes || !scale_bytes || !workspace_bytes) return fail(FKV_ERR_ARG, "NULL size pointer");
+    const int64_t lq = (int64_t)shape->chunk_frames * shape->frame_tokens;
+    const int64_t rows = (slab + lq + 63) / 64 * 64;
+    const int d = shape->head_dim;
+    *q_bytes = (size_t)shape->n_heads * lq * d;
+    *kv_bytes = (size_t)shape->n_heads * rows * d;
+    *scale_bytes = (size_t)shape->n_heads * fkv::fp8_scale_floats(d) * sizeof(float);
+    const int chunks = (int)((slab + lq + fkv::kFp8ChunkRows - 1) / fkv::kFp8ChunkRows) +
+                       (int)((lq + fkv::kFp8ChunkRows - 1) / fkv::kFp8ChunkRows);
+    *workspace_bytes = (fkv::fp8_stats_doubles(shape->n_heads, chunks, d) * sizeof(double) + 255) & ~(size_t)255;
+    return ok();
+}
+
+fkv_status fkv_fp8_pack(const fkv_shape *shape, const void *Q, const void *Kc, const void *Vc, int32_t slab,
+                        const int32_t *kv_len, const void *K_cur, const void *V_cur, void *Q8, void *K8,
+                        void *V8T, float *scales, void *workspace, size_t workspace_bytes, void *stream) {
+    fkv_status st;
+    size_t qb, kvb, sb, wb;
+    if ((st = fkv_fp8_sizes(shape, slab, &qb, &kvb, &sb, &wb)) != FKV_OK) return st;
+    if (!Q || !K_cur || !V_cur || !kv_len || !Q8 || !K8 || !V8T || !scales)
+        return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (slab > 0 && (!Kc || !Vc)) return fail(FKV_ERR_ARG, "NULL Kc/Vc with slab %d", slab);
+    if (!workspace) return fail(FKV_ERR_ARG, "workspace is NULL");
+    if (workspace_bytes < wb)
+        return fail(FKV_ERR_CAPACITY, "workspace of %zu bytes, %zu needed", workspace_bytes, wb);
+    fkv::Fp8PackArgs a;
+    memset(&a, 0, sizeof a);
+    a.Q = (const uint16_t *)Q;
+    a.Kc = (const uint16_t *)(Kc ? Kc : K_cur);
+    a.Vc = (const uint16_t *)(Vc ? Vc : V_cur);
+    a.K_cur = (const uint16_t *)K_cur;
+    a.V_cur = (const uint16_t *)V_cur;
+    a.kv_len = kv_len;
+    a.slab = slab;
+    a.n_heads = shape->n_heads;
+    a.Lq = shape->chunk_frames * shape->frame_tokens;
+    a.d = shape->head_dim;
+    a.rows = (slab + a.Lq + 63) / 64 * 64;
+    a.Q8 = (uint8_t *)Q8;
+    a.K8 = (uint8_t *)K8;
+    a.V8T = (uint8_t *)V8T;
+    a.scales = scales;
+    a.ws = (double *)workspace;
+    a.chunk_rows = fkv::kFp8ChunkRows;
+    a.n_kchunks = (int)((slab + a.Lq + fkv::kFp8ChunkRows - 1) / fkv::kFp8ChunkRows);
+    a.n_qchunks = (a.Lq + fkv::kFp8ChunkRows - 1) / fkv::kFp8ChunkRows;
+    (void)hipGetLastError();
+    return device_status(fkv::launch_fp8_pack(a, (hipStream_t)stream), "fkv_fp8_pack launch");
+}
+
+fkv_status fkv_chunk_attention_fp8(const fkv_shape *shape, const void *Q8, const void *K8, const void *V8T,
+                                   int32_t slab, const int32_t *kv_len, const float *scales, float scale,
+                                   void *O, float *lse, void *workspace, size_t workspace_bytes,
+                                   void *stream) {
+    fkv_status st;
+    size_t qb, kvb, sb, wb;
+    if ((st = fkv_fp8_sizes(shape, slab, &qb, &kvb, &sb, &wb)) != FKV_OK) return st;
+    if (!Q8 || !K8 || !V8T || !kv_len || !scales || !O) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (!(scale > 0.f) || !isfinite(scale)) return fail(FKV_ERR_ARG, "scale %g must be positive and finite", (double)scale);
+    int blocks = 0;
+    if (workspace) {
+        if ((st = balanced_blocks(&blocks)) != FKV_OK) return st;
+        const size_t need = 2 * (size_t)blocks * fkv::attention_part_bytes(shape->head_dim);
+        if (workspace_bytes < need)
+            return fail(FKV_ERR_CAPACITY, "attention workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    }
+    fkv::AttnArgs a;
+    memset(&a, 0, sizeof a);
+    a.Q = Q8;
+    a.Kc = K8;
+    a.Vc = V8T;
+    a.O = O;
+    a.lse = lse;
+    a.kv_len = kv_len;
+    a.slab = slab;
+    a.n_heads = shape->n_heads;
+    a.Lq = shape->chunk_frames * shape->frame_tokens;
+    a.scale = scale;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.n_qtiles = (a.Lq + fkv::kAttnRowsBf16 - 1) / fkv::kAttnRowsBf16;
+    a.n_items = a.n_heads * a.n_qtiles;
+    a.items_per_xcd = (a.n_items + 7) / 8;
+    a.n_blocks = blocks;
+    a.part = (float *)workspace;
+    a.fp8_scales = scales;
+    a.fp8_rows = (slab + a.Lq + 63) / 64 * 64;
+    (void)hipGetLastError();
+    return device_status(fkv::launch_attention_fp8(a, shape->head_dim, (hipStream_t)stream),
+                         "fkv_chunk_attention_fp8 launch");
+}
+
 const char *fkv_last_error(void) { return g_err; }
 
 }  // extern "C"

@@ -106,8 +106,23 @@ struct AttnArgs {
     int32_t items_per_xcd;          // ceil(n_items / 8)
     int32_t n_blocks;               // balanced schedule: workgroups (multiple of 8); 0 = one per item
     float *part;                    // balanced schedule: 2 * n_blocks partial-result slots
+    const float *fp8_scales;        // FP8 path: per-head scale block (see k_fp8.hip)
+    int64_t fp8_rows;               // FP8 path: key rows per head of the packed K / V^T
     float scale;                    // softmax scale
     float scale_log2;               // scale * log2(e)
+};
+
+// ------------------------------------------------------------ FP8 packing
+struct Fp8PackArgs {
+    const uint16_t *Q, *Kc, *Vc, *K_cur, *V_cur;  // bf16 inputs
+    const int32_t *kv_len;
+    int64_t slab;
+    int32_t n_heads, Lq, d;
+    int64_t rows;                   // packed key rows per head (multiple of 64)
+    uint8_t *Q8, *K8, *V8T;
+    float *scales;                  // [n_heads][fp8_scale_floats(d)]
+    double *ws;                     // statistics partials
+    int32_t n_kchunks, n_qchunks, chunk_rows;
 };
 
 constexpr int kScoreThreads = 256;
@@ -124,6 +139,13 @@ hipError_t launch_select(const SelectArgs &a, hipStream_t s);
 hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s);
 hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s);
 size_t attention_part_bytes(int head_dim);  // bytes of one partial-result slot (bf16 kernel)
+
+// FP8 path (k_fp8.hip)
+constexpr int kFp8ChunkRows = 512;          // rows per statistics workgroup
+__host__ __device__ inline int fp8_scale_floats(int d) { return 4 + 3 * d; }
+inline size_t fp8_stats_doubles(int n_heads, int n_chunks, int d) { return (size_t)n_heads * n_chunks * d * 4; }
+hipError_t launch_fp8_pack(const Fp8PackArgs &a, hipStream_t s);
+hipError_t launch_attention_fp8(const AttnArgs &a, int head_dim, hipStream_t s);
 hipError_t launch_attention_f32(const AttnArgs &a, int head_dim, hipStream_t s);
 
 }  // namespace fkv

@@ -41,10 +41,12 @@
 // workgroup per CU and merges split items in a second kernel.  Heads with
 // longer caches make the per-item schedule uneven (at 480P a dynamic head has
 // 342 key tiles per query tile, a static head 245, on 228 items for 256 CUs).
-#include "fkv_internal.h"
+#include "attn_common.h"
 
 namespace fkv {
 namespace {
+
+using namespace attn;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
@@ -52,8 +54,6 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kThreads = 512;      // 8 waves: two groups of 4
 constexpr int kGroupThreads = 256; // one group stages a whole K or V tile
-constexpr int BM = kAttnRowsBf16;  // query rows per workgroup (128 per group)
-constexpr int BN = 64;             // keys per tile
 constexpr float kRescaleSlack = 8.f;  // log2 units the running max may lag behind
 constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw 32-bit buffer, range checked
 
@@ -171,55 +171,6 @@ __device__ __forceinline__ void mfma_block(const uint16_t *vs, const uint16_t *k
         if (st + kPrefetch < NSTEP) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
 }
-
-// Number of key tiles of head h: [Kc[h][0:kv_len]; K_cur[h]] in tiles of BN.
-__device__ __forceinline__ int head_kvl(const AttnArgs &a, int h) {
-    const int kvl = a.kv_len[h];
-    return kvl < 0 ? 0 : (kvl > a.slab ? (int)a.slab : kvl);
-}
-__device__ __forceinline__ int head_tiles(const AttnArgs &a, int h) {
-    return (head_kvl(a, h) + a.Lq + BN - 1) / BN;
-}
-
-// Balanced schedule.  Work item i = (head h, query tile qt), h-major, has
-// T_h key tiles; concatenating all items gives one sequence of `total` tiles,
-// which G = min(n_blocks, total) workgroups split into equal contiguous ranges:
-// workgroup r takes tiles [r*total/G, (r+1)*total/G).  An item cut by a range
-// boundary is computed in parts whose unnormalised results are combined by
-// attn_merge_kernel.  Both kernels derive the same schedule from kv_len.
-struct Schedule {
-    int64_t total;
-    int G;
-    __device__ __forceinline__ int64_t start(int r) const { return (int64_t)r * total / G; }
-    // workgroup whose range holds tile x: the largest r with start(r) <= x
-    __device__ __forceinline__ int owner(int64_t x) const { return (int)(((x + 1) * G - 1) / total); }
-};
-
-__device__ __forceinline__ Schedule make_schedule(const AttnArgs &a) {
-    int64_t total = 0;
-    for (int h = 0; h < a.n_heads; ++h) total += (int64_t)a.n_qtiles * head_tiles(a, h);
-    Schedule sc;
-    sc.total = total;
-    sc.G = (int)(total < a.n_blocks ? total : a.n_blocks);
-    return sc;
-}
-
-// Partial result of one part of an item, in a slot of BM*(D/2 + 2) floats:
-// the part's own normalised output o/l rounded to bf16, in the accumulator
-// layout of the waves (4 values per lane and uint2 index
-// ((wave*MB + mb)*4 + g)*64 + lane), then the running max m (log2 units) of
-// the BM rows, then their probability sums l.
-template <int D>
-__device__ __forceinline__ size_t slot_floats() { return (size_t)BM * (D / 2 + 2); }
-
-__device__ __forceinline__ uint2 pack_bf16x4(float x0, float x1, float x2, float x3) {
-    const uint32_t b0 = __builtin_bit_cast(uint16_t, (__bf16)x0), b1 = __builtin_bit_cast(uint16_t, (__bf16)x1);
-    const uint32_t b2 = __builtin_bit_cast(uint16_t, (__bf16)x2), b3 = __builtin_bit_cast(uint16_t, (__bf16)x3);
-    return make_uint2(b0 | (b1 << 16), b2 | (b3 << 16));
-}
-
-__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 
 // One segment: positions [t0, t1) of item (h, qt), where position j is key
 // tile (j + rot) mod T of the item's T tiles (the order of key tiles does not
@@ -564,16 +515,22 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 
 }  // namespace
 
+hipError_t launch_attention_merge(const AttnArgs &a, int head_dim, hipStream_t s) {
+    if (head_dim == 128)
+        hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(a.n_items, BM / 32), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(a.n_items, BM / 32), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
 hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s) {
     if (a.n_blocks > 0) {
-        if (head_dim == 128) {
+        if (head_dim == 128)
             hipLaunchKernelGGL((attn_bf16_kernel<128, true>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
-            hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(a.n_items, BM / 32), dim3(256), 0, s, a);
-        } else {
+        else
             hipLaunchKernelGGL((attn_bf16_kernel<64, true>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
-            hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(a.n_items, BM / 32), dim3(256), 0, s, a);
-        }
-        return hipGetLastError();
+        const hipError_t e = hipGetLastError();
+        return e != hipSuccess ? e : launch_attention_merge(a, head_dim, s);
     }
     const unsigned blocks = (unsigned)a.items_per_xcd * 8u;
     if (head_dim == 128)

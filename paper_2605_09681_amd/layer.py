@@ -20,9 +20,9 @@ from typing import Optional, Sequence
 import torch
 
 from . import (FKV_DYNAMIC, FKV_STATIC, fkv_attention_workspace_size, fkv_chunk_attention,
-               fkv_compress_static, fkv_num_segments, fkv_score_segments,
-               fkv_score_workspace_size, fkv_select_compact, make_heads, make_shape,
-               slab_tokens)
+               fkv_chunk_attention_fp8, fkv_compress_static, fkv_fp8_pack, fkv_fp8_sizes,
+               fkv_num_segments, fkv_score_segments, fkv_score_workspace_size,
+               fkv_select_compact, make_heads, make_shape, slab_tokens)
 
 
 class CompressedLayer:
@@ -73,6 +73,31 @@ class CompressedLayer:
     def attention(self, Q, K_cur, V_cur, O, lse=None, scale: Optional[float] = None):
         fkv_chunk_attention(self.shape, Q, self.Kc, self.Vc, self.kv_len, K_cur, V_cur,
                             self.scale if scale is None else scale, O, lse, self.attn_workspace)
+
+    def fp8_buffers(self):
+        """Packed FP8 inputs of the FP8 attention variant (allocated on first use)."""
+        if getattr(self, "_fp8", None) is None:
+            qb, kvb, sb, wb = fkv_fp8_sizes(self.shape, self.slab)
+            u8 = dict(dtype=torch.uint8, device=self.device)
+            self._fp8 = dict(Q8=torch.empty(qb, **u8), K8=torch.empty(kvb, **u8), V8T=torch.empty(kvb, **u8),
+                             scales=torch.empty(sb // 4, dtype=torch.float32, device=self.device),
+                             ws=torch.empty(max(wb, 1), **u8))
+        return self._fp8
+
+    def pack_fp8(self, Q, K_cur, V_cur):
+        b = self.fp8_buffers()
+        fkv_fp8_pack(self.shape, Q, self.Kc, self.Vc, self.kv_len, K_cur, V_cur, b["Q8"], b["K8"], b["V8T"],
+                     b["scales"], b["ws"])
+
+    def attention_fp8_packed(self, O, lse=None, scale: Optional[float] = None):
+        b = self.fp8_buffers()
+        fkv_chunk_attention_fp8(self.shape, b["Q8"], b["K8"], b["V8T"], self.slab, self.kv_len, b["scales"],
+                                self.scale if scale is None else scale, O, lse, self.attn_workspace)
+
+    def attention_fp8(self, Q, K_cur, V_cur, O, lse=None, scale: Optional[float] = None):
+        """FP8 variant of :meth:`attention`: pack, then the FP8 kernel."""
+        self.pack_fp8(Q, K_cur, V_cur)
+        self.attention_fp8_packed(O, lse, scale)
 
     # whole step --------------------------------------------------------------
     def compress(self, K_hist, V_hist, frame_slot, K_cur):

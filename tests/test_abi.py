@@ -29,7 +29,7 @@ def fkv():
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(fkv_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(fkv_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_declares_the_four_entry_points():

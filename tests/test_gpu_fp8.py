@@ -1,0 +1,183 @@
+"""GPU parity of the FP8 attention variant (App. F) through the C ABI.
+
+* Packing (fkv_fp8_pack) is byte-exact against the oracle's quantisation
+  (oracle/fp8.py): E4M3 codes of Q, K - mu and V, the key order of the packed
+  V^T tiles, and every scale bit.
+* The FP8 kernel's only rounding beyond the packed inputs is that of the
+  probabilities (E4M3: relative error within +-2^-4 for normal values,
+  absolute within +-2^-10 below 2^-6, in the kernel's scaling 2^6 exp(z - max)).  Against exact attention
+  of the dequantised inputs each output element must lie within 6 standard
+  deviations of that rounding's error (oracle.fp8.p_rounding_sigma) plus the
+  final bf16 rounding; the log-normaliser within 6 standard deviations of the
+  relative error of the rounded sum.
+* Against the exact bf16-input oracle (the quantisation included) the 480P
+  layer stays within the bf16 acceptance bound of 2e-2 max-abs.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import fp8
+import workloads as W
+from gpu_harness import dev_inputs, from_dev, make_layer, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2605_09681_amd as fkv
+    fkv.lib()
+    oracle.lib()
+
+
+def _case(name, **kw):
+    print(f"[gpu case] {name} " + " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
+
+
+def _key_of_position():
+    """Key (0..63) of each byte position of a packed V^T tile row."""
+    key = np.empty(64, np.int64)
+    for p in range(64):
+        hl, j = divmod(p, 32)
+        kb, i = divmod(j, 16)
+        key[p] = 32 * kb + 8 * (i // 4) + 4 * hl + (i % 4)
+    return key
+
+
+def run_fp8(cfg, x, balanced=True):
+    layer = make_layer(cfg, balanced=balanced)
+    d = dev_inputs(x)
+    layer.compress(d["K_hist"], d["V_hist"], x.frame_slot, d["K_cur"])
+    O = torch.empty_like(d["Q"])
+    lse = torch.empty((cfg.n_heads, cfg.lq), dtype=torch.float32, device="cuda")
+    layer.attention_fp8(d["Q"], d["K_cur"], d["V_cur"], O, lse)
+    torch.cuda.synchronize()
+    return layer, O, lse
+
+
+def check_pack(cfg, x, layer):
+    """Byte-exact packing; returns the oracle's per-head quantisation."""
+    ref = oracle.run_layer(cfg, x, attention=False)
+    b = layer.fp8_buffers()
+    nh, d, lq = cfg.n_heads, cfg.head_dim, cfg.lq
+    rows = b["K8"].numel() // (nh * d)
+    q8 = from_dev(b["Q8"]).reshape(nh, lq, d)
+    k8 = from_dev(b["K8"]).reshape(nh, rows, d)
+    vt = from_dev(b["V8T"]).reshape(nh, rows // 64, d, 64)
+    sc = from_dev(b["scales"]).reshape(nh, 4 + 3 * d)
+    key = _key_of_position()
+    heads = []
+    for h in range(nh):
+        kv = int(ref.kv_len[h])
+        f32 = lambda a: W.storage_to_f32(np.asarray(a), cfg.dtype)
+        K = np.concatenate([f32(ref.Kc[h]).reshape(-1, d), f32(x.K_cur[h])])
+        V = np.concatenate([f32(ref.Vc[h]).reshape(-1, d), f32(x.V_cur[h])])
+        hq = fp8.quantize_head(f32(x.Q[h]), K, V)
+        heads.append(hq)
+        n = kv + lq
+        v8 = np.zeros((rows, d), np.uint8)
+        for t in range(rows // 64):
+            v8[t * 64 + key] = vt[h, t].T
+        np.testing.assert_array_equal(q8[h], hq.q8, err_msg=f"Q8 head {h}")
+        np.testing.assert_array_equal(k8[h, :n], hq.k8, err_msg=f"K8 head {h}")
+        np.testing.assert_array_equal(v8[:n], hq.v8, err_msg=f"V8T head {h}")
+        tail = -(-n // 64) * 64
+        assert not k8[h, n:tail].any() and not v8[n:tail].any(), f"padding head {h}"
+        want = np.concatenate([[hq.s_q, hq.s_k, hq.inv_q, hq.inv_k], hq.s_v, hq.inv_v, hq.mu_k]).astype(np.float32)
+        np.testing.assert_array_equal(sc[h].view(np.uint32), want.view(np.uint32), err_msg=f"scales head {h}")
+    return ref, heads
+
+
+def check_attention(cfg, ref, heads, O, lse, rows, scale=None):
+    scale = 1 / math.sqrt(cfg.head_dim) if scale is None else scale
+    out = W.bf16_bits_to_f32(from_dev(O)).astype(np.float64)
+    ls = from_dev(lse).astype(np.float64)
+    worst = 0.0
+    for h, hq in enumerate(heads):
+        kv = int(ref.kv_len[h])
+        q, k, v = fp8.dequantized(hq)
+        o_ref, lse_ref = oracle.attention_rows(q, k[:kv], v[:kv], k[kv:], v[kv:], scale, rows)
+        sig = fp8.p_rounding_sigma(q, k, v, scale, rows)
+        err = np.abs(out[h, rows] - o_ref)
+        tol = 6 * sig + 2.0 ** -8 * np.abs(o_ref) + 1e-6
+        bad = err > tol
+        assert not bad.any(), (h, float(err[bad].max()), float(tol[bad].min()), int(bad.sum()))
+        worst = max(worst, float((err / tol).max()))
+        # the normaliser: relative error of a sum of rounded probabilities
+        z = scale * (q[rows] @ k.T)
+        p = np.exp(z - z.max(axis=1, keepdims=True)) * 64.0
+        rel = np.sqrt(fp8.p_rounding_var(p).sum(axis=1)) / p.sum(axis=1)
+        assert (np.abs(ls[h, rows] - lse_ref) <= 6 * rel + 1e-5).all(), h
+    return worst
+
+
+@pytest.mark.parametrize("balanced", [True, False])
+@pytest.mark.parametrize("d,L", [(128, 25), (128, 100), (64, 300)])
+def test_fp8_small_all_rows(balanced, d, L):
+    heads = (W.HeadBudget(W.STATIC, 1, 2), W.HeadBudget(W.DYNAMIC, 1, 0, 2, W.SCOPE_FRAME if L < 100 else W.SCOPE_GLOBAL),
+             W.HeadBudget(W.DYNAMIC, 0, 1, 3, W.SCOPE_GLOBAL), W.HeadBudget(W.STATIC, 2, 0))
+    cfg = W.LayerConfig("small", 4, d, 100, 7, 9, 2, L, "bf16", heads, 0.85)
+    slot = np.array([3, 0, 8, 1, 5, 2, 7], np.int32)
+    _case("fp8-small", d=d, L=L, balanced=balanced)
+    x = W.make_layer_inputs(cfg, seed=d + L, frame_slot=slot)
+    layer, O, lse = run_fp8(cfg, x, balanced)
+    ref, hq = check_pack(cfg, x, layer)
+    check_attention(cfg, ref, hq, O, lse, np.arange(cfg.lq, dtype=np.int32))
+
+
+def test_fp8_480p_layer():
+    cfg = W.wan_layer_config("480p")
+    _case("fp8-480p")
+    x = W.make_layer_inputs(cfg, seed=0)
+    layer, O, lse = run_fp8(cfg, x)
+    ref, hq = check_pack(cfg, x, layer)
+    rows = sample_rows(cfg.lq, 24)
+    worst = check_attention(cfg, ref, hq, O, lse, rows)
+    # against the exact (unquantised) attention of the bf16 inputs
+    exact = oracle.run_layer(cfg, x, rows=rows, scale=1 / math.sqrt(128))
+    out = W.bf16_bits_to_f32(from_dev(O)).astype(np.float64)[:, rows]
+    max_abs = float(np.abs(out - exact.O).max())
+    rel = float(np.linalg.norm(out - exact.O) / np.linalg.norm(exact.O))
+    print(f"fp8 480p: max_abs vs exact {max_abs:.2e}, rel_l2 {rel:.2e}, worst err/tol vs dequantised {worst:.2f}")
+    assert max_abs <= 2e-2 and rel <= 0.1
+
+
+def test_fp8_sharp_logits():
+    cfg = W.wan_layer_config("480p")
+    _case("fp8-sharp")
+    x = W.make_layer_inputs(cfg, seed=1, q_scale=6.0)
+    layer, O, lse = run_fp8(cfg, x)
+    ref, hq = check_pack(cfg, x, layer)
+    check_attention(cfg, ref, hq, O, lse, sample_rows(cfg.lq, 12, seed=1))
+
+
+def test_fp8_empty_history_and_budgets():
+    """H = 0 and zero budgets: attention over the chunk alone."""
+    heads = (W.HeadBudget(W.STATIC, 0, 0), W.HeadBudget(W.DYNAMIC, 0, 0, 0, W.SCOPE_GLOBAL),
+             W.HeadBudget(W.DYNAMIC, 0, 0, 0, W.SCOPE_FRAME), W.HeadBudget(W.STATIC, 1, 0))
+    for H in (0, 5):
+        cfg = W.LayerConfig("empty", 4, 128, 100, H, 6, 2, 25, "bf16", heads, 0.85)
+        _case("fp8-empty", H=H)
+        x = W.make_layer_inputs(cfg, seed=40 + H)
+        layer, O, lse = run_fp8(cfg, x)
+        ref, hq = check_pack(cfg, x, layer)
+        check_attention(cfg, ref, hq, O, lse, np.arange(cfg.lq, dtype=np.int32))
+
+
+def test_fp8_zero_queries():
+    """An all-zero Q packs to zeros with zero scales: uniform attention, the
+    mean of the dequantised values."""
+    cfg = W.LayerConfig("zeroq", 2, 128, 64, 3, 3, 1, 64, "bf16",
+                        (W.HeadBudget(W.STATIC, 1, 1), W.HeadBudget(W.STATIC, 0, 3)), 0.9)
+    x = W.make_layer_inputs(cfg, seed=41)
+    x.Q[:] = 0
+    _case("fp8-zero-q")
+    layer, O, lse = run_fp8(cfg, x)
+    ref, hq = check_pack(cfg, x, layer)
+    check_attention(cfg, ref, hq, O, lse, np.arange(cfg.lq, dtype=np.int32))

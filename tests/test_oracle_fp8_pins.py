@@ -112,7 +112,7 @@ def test_dequantized_attention_error_matches_rounding_model(oracle_lib):
     Kf, Vf = K.astype(np.float64), V.astype(np.float64)
     only_v = oracle.attention_rows(Q.astype(np.float64), Kf[:n], v[:n], Kf[n:], v[n:], 0.17)[0]
     exact = oracle.attention_rows(Q, K[:n], V[:n], K[n:], V[n:], 0.17)[0]
-    sig = fp8.p_rounding_sigma(Q, Kf, Vf, 0.17, rows)
+    sig = fp8.p_rounding_sigma(Q, Kf, Vf, 0.17, rows, p_bias_log2=12.0)   # all normal: relative model
     z = (only_v - exact) / sig
     assert 0.3 < np.sqrt((z ** 2).mean()) < 2.0 and np.abs(z).max() < 7
     deq = oracle.attention_rows(q, k[:n], v[:n], k[n:], v[n:], 0.17)[0]
