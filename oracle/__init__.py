@@ -72,6 +72,8 @@ def lib():
         L.fkvo_compact_head.restype = LG
         L.fkvo_attention_rows.argtypes = [I, I, LG, LG, P, P, P, P, P, D, P, I, P, P]
         L.fkvo_attention_rows.restype = None
+        L.fkvo_attention_mass.argtypes = [I, I, LG, LG, I, P, P, P, D, P]
+        L.fkvo_attention_mass.restype = None
         L.fkvo_max_threads.argtypes = []
         L.fkvo_max_threads.restype = I
         _lib = L
@@ -217,6 +219,39 @@ def attention_rows(Q: np.ndarray, Kc: np.ndarray, Vc: np.ndarray, K_cur: np.ndar
                               _ptr(K_cur), _ptr(V_cur), float(scale), _ptr(rows),
                               len(rows), _ptr(out), _ptr(lse))
     return out, lse
+
+
+def attention_mass(Q: np.ndarray, Kc: np.ndarray, K_cur: np.ndarray, F: int, scale: float) -> np.ndarray:
+    """Sec. 4.1 attention mass per block of F keys of [Kc; K_cur], summed over
+    all query rows (fp64).  Q/K_cur: [Lq][d]; Kc: [kv_len][d]."""
+    Q, K_cur, Kc = _c(Q), _c(K_cur), _c(Kc)
+    Lq, d = Q.shape
+    kv_len = Kc.shape[0]
+    n_bins = -(-(kv_len + Lq) // F)
+    out = np.empty(max(n_bins, 1), np.float64)
+    kc = Kc if kv_len else np.zeros((1, d), Q.dtype)
+    lib().fkvo_attention_mass(_dt(Q), d, kv_len, Lq, F, _ptr(Q), _ptr(kc), _ptr(K_cur), float(scale), _ptr(out))
+    return out[:n_bins].copy()
+
+
+def classify_heads(mass: np.ndarray, hist_frames: int, sink_frames: int, transition_frames: int,
+                   alpha: float) -> np.ndarray:
+    """Eq. 1: a head is static (0) when the mass on the generated chunk plus the
+    transition frame(s), over the mass of the whole window without the sink
+    frame(s), exceeds alpha; dynamic (1) otherwise.  mass: [n_heads][H + C]
+    (history frames in logical order, then the chunk's frames), summed in fp64."""
+    mass = np.asarray(mass, np.float64)
+    H = hist_frames
+    types = []
+    for row in mass:
+        total = row.sum()
+        generate = row[H:].sum()
+        transition = row[max(H - transition_frames, 0):H].sum()
+        sink = row[:min(sink_frames, H)].sum()
+        denom = total - sink
+        ratio = (generate + transition) / denom if denom > 0 else np.inf
+        types.append(STATIC if ratio > alpha else DYNAMIC)
+    return np.array(types, np.int32)
 
 
 # ---------------------------------------------------------------------------

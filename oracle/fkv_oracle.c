@@ -312,3 +312,45 @@ void fkvo_attention_rows(int dtype, int d, long kv_len, long Lq, const void *Q,
         free(q);
     }
 }
+
+/* ---------------------------------------------------------------------------
+ * Offline head profiling, Sec. 4.1 (Eq. 1 uses the attention mass a head puts
+ * on the generated chunk, the transition frame, the sink frames and the whole
+ * window).  Attention mass of key block b (keys [bF, bF + F) of the key
+ * sequence [Kc[0:kv_len]; Kcur]): the sum over every query row of the softmax
+ * probabilities of the block's keys.  Exact fp64 softmax per row.
+ * mass: [ceil((kv_len + Lq) / F)] fp64, overwritten.
+ * ------------------------------------------------------------------------- */
+void fkvo_attention_mass(int dtype, int d, long kv_len, long Lq, int F, const void *Q,
+                         const void *Kc, const void *Kcur, double scale, double *mass) {
+    const long Lk = kv_len + Lq;
+    const long n_bins = (Lk + F - 1) / F;
+    for (long b = 0; b < n_bins; ++b) mass[b] = 0.0;
+#pragma omp parallel
+    {
+        double *z = (double *)malloc(sizeof(double) * (size_t)(Lk > 0 ? Lk : 1));
+        double *q = (double *)malloc(sizeof(double) * (size_t)d);
+        double *acc = (double *)calloc((size_t)n_bins, sizeof(double));
+#pragma omp for schedule(dynamic, 4)
+        for (long r = 0; r < Lq; ++r) {
+            for (int c = 0; c < d; ++c) q[c] = load_elem(Q, dtype, (size_t)r * d + c);
+            double m = -INFINITY;
+            for (long j = 0; j < Lk; ++j) {
+                const void *kb = j < kv_len ? Kc : Kcur;
+                size_t kr = (size_t)(j < kv_len ? j : j - kv_len) * d;
+                double dot = 0.0;
+                for (int c = 0; c < d; ++c) dot += q[c] * load_elem(kb, dtype, kr + c);
+                z[j] = scale * dot;
+                if (z[j] > m) m = z[j];
+            }
+            double den = 0.0;
+            for (long j = 0; j < Lk; ++j) den += exp(z[j] - m);
+            for (long j = 0; j < Lk; ++j) acc[j / F] += exp(z[j] - m) / den;
+        }
+#pragma omp critical
+        for (long b = 0; b < n_bins; ++b) mass[b] += acc[b];
+        free(acc);
+        free(z);
+        free(q);
+    }
+}

@@ -91,6 +91,12 @@ void fkvo_attention_rows(int dtype, int d, long kv_len, long Lq, const void *Q,
                          const void *Vcur, double scale, const int32_t *rows,
                          int n_rows, double *out, double *lse);
 
+/* Offline head profiling (Sec. 4.1, Eq. 1): attention mass of every block of
+ * F keys of [Kc[0:kv_len]; Kcur], summed over all Lq query rows (exact fp64
+ * softmax per row).  mass: [ceil((kv_len + Lq) / F)]. */
+void fkvo_attention_mass(int dtype, int d, long kv_len, long Lq, int F, const void *Q,
+                         const void *Kc, const void *Kcur, double scale, double *mass);
+
 /* Number of OpenMP threads a parallel region would use. */
 int fkvo_max_threads(void);
 
