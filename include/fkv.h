@@ -237,6 +237,43 @@ fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q,
                                void *stream);
 
 /* ---------------------------------------------------------------------------
+ * Offline head profiling (Sec. 4.1, Eq. 1).  A profiling pass runs the layer
+ * on the uncompressed cache (every head static with recent_frames = H, so Kc
+ * holds the whole history in logical order), calls fkv_chunk_attention for
+ * the log-normaliser, then fkv_attention_mass, and finally classifies.
+ *
+ * fkv_attention_mass: for every head h and key block b (keys [bF, bF + F) of
+ * [Kc[h][0:kv_len]; K_cur[h]], F = frame_tokens -- with the full history,
+ * block t < H is logical frame t and blocks H .. H+C-1 are the chunk's frames):
+ *   mass[h][b] (=, or += when accumulate = 1) sum over every query row r of
+ *                exp(scale * Q[h][r] . k - lse[h][r])
+ * with the same bf16 score product as the attention kernel; fp32 sums in a
+ * fixed order (deterministic).  mass: float [n_heads][n_bins] (device),
+ * n_bins >= ceil((slab + C*F) / F) (FKV_ERR_CAPACITY otherwise).  bf16 only.
+ * The workspace needs no initialisation. */
+fkv_status fkv_attention_mass_workspace_size(const fkv_shape *shape, int32_t n_bins,
+                                             size_t *bytes);
+
+fkv_status fkv_attention_mass(const fkv_shape *shape, const void *Q, const void *Kc,
+                              int32_t slab, const int32_t *kv_len, const void *K_cur,
+                              const float *lse, float scale, int32_t n_bins,
+                              float *mass, int32_t accumulate, void *workspace,
+                              size_t workspace_bytes, void *stream);
+
+/* Eq. 1 on HOST data: mass float [n_heads][n_bins] with bins 0 .. H-1 the
+ * history frames (oldest first) and bins H .. n_bins-1 the generated chunk.
+ * With A_Total = all bins, A_Generate = bins >= H, A_Transition = the last
+ * transition_frames history frames (the paper's transition anchor frame is
+ * 1), A_Sink = the first sink_frames history frames, all summed in fp64:
+ *   head_type[h] = FKV_STATIC if (A_Generate + A_Transition) /
+ *                  (A_Total - A_Sink) > alpha, else FKV_DYNAMIC
+ * (FKV_STATIC when the denominator is 0).  head_type: HOST int32 [n_heads]. */
+fkv_status fkv_classify_heads(const float *mass, int32_t n_heads, int32_t n_bins,
+                              int32_t hist_frames, int32_t sink_frames,
+                              int32_t transition_frames, float alpha,
+                              int32_t *head_type);
+
+/* ---------------------------------------------------------------------------
  * FP8 variant of the chunk attention (App. F: the method combined with FP8
  * attention), for the FP8 matrix cores of gfx950.  Two steps:
  *

@@ -16,6 +16,8 @@ Entry points (see ``include/fkv.h`` for the full contract):
 * :func:`fkv_append_frames`    -- rolling-cache write of a finished chunk
 * :func:`fkv_fp8_pack`, :func:`fkv_chunk_attention_fp8` -- the FP8 variant of
   the chunk attention (App. F)
+* :func:`fkv_attention_mass`, :func:`fkv_classify_heads` -- offline head
+  profiling (Sec. 4.1, Eq. 1)
 * :func:`fkv_score_pooled`, :func:`fkv_select_compact_pooled` -- the
   first-block proxy of Sec. 4.3: one similarity row pooled over all heads,
   shared by the dynamic heads of every layer
@@ -42,7 +44,8 @@ EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_append_frames", "fkv_score_pooled_workspace_size", "fkv_score_pooled",
             "fkv_select_compact_pooled",
             "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_fp8_sizes", "fkv_fp8_pack",
-            "fkv_chunk_attention_fp8", "fkv_last_error")
+            "fkv_chunk_attention_fp8", "fkv_attention_mass_workspace_size", "fkv_attention_mass",
+            "fkv_classify_heads", "fkv_last_error")
 
 
 class FkvLibraryMissing(RuntimeError):
@@ -112,6 +115,12 @@ def lib():
         L.fkv_fp8_pack.restype = ctypes.c_int
         L.fkv_chunk_attention_fp8.argtypes = [S, P, P, P, I32, P, P, F, P, P, P, SZ, P]
         L.fkv_chunk_attention_fp8.restype = ctypes.c_int
+        L.fkv_attention_mass_workspace_size.argtypes = [S, I32, ctypes.POINTER(SZ)]
+        L.fkv_attention_mass_workspace_size.restype = ctypes.c_int
+        L.fkv_attention_mass.argtypes = [S, P, P, I32, P, P, P, F, I32, P, I32, P, SZ, P]
+        L.fkv_attention_mass.restype = ctypes.c_int
+        L.fkv_classify_heads.argtypes = [P, I32, I32, I32, I32, I32, F, P]
+        L.fkv_classify_heads.restype = ctypes.c_int
         L.fkv_last_error.argtypes = []
         L.fkv_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -387,6 +396,46 @@ def fkv_chunk_attention_fp8(shape: fkv_shape, Q8, K8, V8T, slab: int, kv_len, sc
         _check(V8T, "V8T", torch.uint8), int(slab), _check(kv_len, "kv_len", torch.int32, (shape.n_heads,)),
         _check(scales, "scales", torch.float32), ctypes.c_float(scale), _check(O, "O", torch.bfloat16, chunk),
         ls, ws, nws, _stream(stream)))
+
+
+def fkv_attention_mass_workspace_size(shape: fkv_shape, n_bins: int) -> int:
+    out = ctypes.c_size_t(0)
+    _raise(lib().fkv_attention_mass_workspace_size(ctypes.byref(shape), int(n_bins), ctypes.byref(out)))
+    return int(out.value)
+
+
+def fkv_attention_mass(shape: fkv_shape, Q, Kc, kv_len, K_cur, lse, scale: float, mass,
+                       accumulate: bool = False, workspace: Optional[torch.Tensor] = None, stream=None):
+    """Head-profiling attention mass per key block of F keys (see fkv.h)."""
+    dt = _torch_dtype(shape)
+    chunk = (shape.n_heads, _lq(shape), shape.head_dim)
+    slab = Kc.shape[1] if Kc.dim() == 3 else -1
+    m = _check(mass, "mass", torch.float32)
+    if mass.dim() != 2 or mass.shape[0] != shape.n_heads:
+        raise ValueError("mass must be [n_heads][n_bins]")
+    n_bins = mass.shape[1]
+    need = fkv_attention_mass_workspace_size(shape, n_bins)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=Q.device)
+    _raise(lib().fkv_attention_mass(
+        ctypes.byref(shape), _check(Q, "Q", dt, chunk), _check(Kc, "Kc", dt, (shape.n_heads, slab, shape.head_dim)),
+        int(slab), _check(kv_len, "kv_len", torch.int32, (shape.n_heads,)), _check(K_cur, "K_cur", dt, chunk),
+        _check(lse, "lse", torch.float32, (shape.n_heads, _lq(shape))), ctypes.c_float(scale), int(n_bins), m,
+        1 if accumulate else 0, _check(workspace, "workspace", torch.uint8), workspace.numel(), _stream(stream)))
+    return workspace
+
+
+def fkv_classify_heads(mass, hist_frames: int, sink_frames: int = 1, transition_frames: int = 1,
+                       alpha: float = 0.8):
+    """Eq. 1 on a host mass table [n_heads][n_bins] (numpy float32 or a CPU
+    tensor); returns a list of FKV_STATIC / FKV_DYNAMIC."""
+    import numpy as np
+    m = np.ascontiguousarray(mass.cpu().numpy() if isinstance(mass, torch.Tensor) else mass, dtype=np.float32)
+    n_heads, n_bins = m.shape
+    out = (ctypes.c_int32 * n_heads)()
+    _raise(lib().fkv_classify_heads(m.ctypes.data_as(ctypes.c_void_p), n_heads, n_bins, int(hist_frames),
+                                    int(sink_frames), int(transition_frames), ctypes.c_float(alpha), out))
+    return list(out)
 
 
 def fkv_last_error() -> str:

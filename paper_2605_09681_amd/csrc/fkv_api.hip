@@ -655,6 +655,84 @@ fkv_status fkv_chunk_attention_fp8(const fkv_shape *shape, const void *Q8, const
                          "fkv_chunk_attention_fp8 launch");
 }
 
+fkv_status fkv_attention_mass_workspace_size(const fkv_shape *shape, int32_t n_bins, size_t *bytes) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if (!bytes) return fail(FKV_ERR_ARG, "bytes is NULL");
+    if (n_bins < 1) return fail(FKV_ERR_ARG, "n_bins %d < 1", n_bins);
+    const int lq = shape->chunk_frames * shape->frame_tokens;
+    const size_t n_qtiles = (size_t)((lq + fkv::kAttnRowsBf16 - 1) / fkv::kAttnRowsBf16);
+    *bytes = ((size_t)shape->n_heads * n_qtiles * 8 * n_bins * sizeof(float) + 255) & ~(size_t)255;
+    return ok();
+}
+
+fkv_status fkv_attention_mass(const fkv_shape *shape, const void *Q, const void *Kc, int32_t slab,
+                              const int32_t *kv_len, const void *K_cur, const float *lse, float scale,
+                              int32_t n_bins, float *mass, int32_t accumulate, void *workspace,
+                              size_t workspace_bytes, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if (shape->dtype != FKV_BF16) return fail(FKV_ERR_SHAPE, "the attention mass takes bf16 inputs");
+    if (!Q || !K_cur || !kv_len || !lse || !mass) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (slab < 0) return fail(FKV_ERR_ARG, "slab %d < 0", slab);
+    if (slab > 0 && !Kc) return fail(FKV_ERR_ARG, "NULL Kc with slab %d", slab);
+    if (!(scale > 0.f) || !isfinite(scale)) return fail(FKV_ERR_ARG, "scale %g must be positive and finite", (double)scale);
+    if (accumulate != 0 && accumulate != 1) return fail(FKV_ERR_ARG, "accumulate must be 0 or 1");
+    const int64_t lq = (int64_t)shape->chunk_frames * shape->frame_tokens;
+    const int64_t need_bins = (slab + lq + shape->frame_tokens - 1) / shape->frame_tokens;
+    if (n_bins < need_bins)
+        return fail(FKV_ERR_CAPACITY, "n_bins %d below ceil((slab + C*F) / F) = %lld", n_bins, (long long)need_bins);
+    size_t need = 0;
+    if ((st = fkv_attention_mass_workspace_size(shape, n_bins, &need)) != FKV_OK) return st;
+    if (!workspace) return fail(FKV_ERR_ARG, "workspace is NULL");
+    if (workspace_bytes < need)
+        return fail(FKV_ERR_CAPACITY, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    fkv::AttnArgs a;
+    memset(&a, 0, sizeof a);
+    a.Q = Q;
+    a.Kc = Kc ? Kc : K_cur;
+    a.K_cur = K_cur;
+    a.kv_len = kv_len;
+    a.lse = (float *)lse;
+    a.slab = slab;
+    a.n_heads = shape->n_heads;
+    a.Lq = (int32_t)lq;
+    a.scale = scale;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.n_qtiles = (a.Lq + fkv::kAttnRowsBf16 - 1) / fkv::kAttnRowsBf16;
+    a.n_items = a.n_heads * a.n_qtiles;
+    a.part = (float *)workspace;
+    a.mass_F = shape->frame_tokens;
+    a.mass_bins = n_bins;
+    a.mass_acc = accumulate;
+    a.mass_out = mass;
+    (void)hipGetLastError();
+    return device_status(fkv::launch_attention_mass(a, shape->head_dim, (hipStream_t)stream),
+                         "fkv_attention_mass launch");
+}
+
+fkv_status fkv_classify_heads(const float *mass, int32_t n_heads, int32_t n_bins, int32_t hist_frames,
+                              int32_t sink_frames, int32_t transition_frames, float alpha, int32_t *head_type) {
+    if (!mass || !head_type) return fail(FKV_ERR_ARG, "NULL pointer");
+    if (n_heads < 1 || n_bins < 1) return fail(FKV_ERR_ARG, "n_heads %d, n_bins %d", n_heads, n_bins);
+    if (hist_frames < 0 || hist_frames > n_bins)
+        return fail(FKV_ERR_ARG, "hist_frames %d outside [0, n_bins=%d]", hist_frames, n_bins);
+    if (sink_frames < 0 || transition_frames < 0) return fail(FKV_ERR_ARG, "negative frame count");
+    if (!isfinite(alpha)) return fail(FKV_ERR_ARG, "alpha is not finite");
+    for (int h = 0; h < n_heads; ++h) {
+        const float *m = mass + (size_t)h * n_bins;
+        double total = 0.0, generate = 0.0, transition = 0.0, sink = 0.0;
+        for (int b = 0; b < n_bins; ++b) total += m[b];
+        for (int b = hist_frames; b < n_bins; ++b) generate += m[b];
+        for (int b = std::max(hist_frames - transition_frames, 0); b < hist_frames; ++b) transition += m[b];
+        for (int b = 0; b < std::min(sink_frames, hist_frames); ++b) sink += m[b];
+        const double denom = total - sink;
+        const bool is_static = denom > 0.0 ? (generate + transition) / denom > (double)alpha : true;
+        head_type[h] = is_static ? FKV_STATIC : FKV_DYNAMIC;
+    }
+    return ok();
+}
+
 const char *fkv_last_error(void) { return g_err; }
 
 }  // extern "C"

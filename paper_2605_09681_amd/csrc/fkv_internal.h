@@ -106,6 +106,10 @@ struct AttnArgs {
     int32_t items_per_xcd;          // ceil(n_items / 8)
     int32_t n_blocks;               // balanced schedule: workgroups (multiple of 8); 0 = one per item
     float *part;                    // balanced schedule: 2 * n_blocks partial-result slots
+    int32_t mass_F;                 // attention mass: keys per bin (frame tokens)
+    int32_t mass_bins;              // attention mass: bins per head
+    int32_t mass_acc;               // attention mass: 1 = add to mass_out, 0 = overwrite
+    float *mass_out;                // attention mass: [n_heads][mass_bins]
     const float *fp8_scales;        // FP8 path: per-head scale block (see k_fp8.hip)
     int64_t fp8_rows;               // FP8 path: key rows per head of the packed K / V^T
     float scale;                    // softmax scale
@@ -139,6 +143,10 @@ hipError_t launch_select(const SelectArgs &a, hipStream_t s);
 hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s);
 hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s);
 size_t attention_part_bytes(int head_dim);  // bytes of one partial-result slot (bf16 kernel)
+
+// attention mass per key block (head profiling), k_attn.hip; the workspace holds
+// n_heads * n_qtiles * 8 waves * mass_bins floats
+hipError_t launch_attention_mass(const AttnArgs &a, int head_dim, hipStream_t s);
 
 // FP8 path (k_fp8.hip)
 constexpr int kFp8ChunkRows = 512;          // rows per statistics workgroup

@@ -513,6 +513,101 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     }
 }
 
+// ------------------------------------------------------------ attention mass
+// Offline head profiling (Sec. 4.1, Eq. 1) needs, per head, the attention mass
+// each block of F keys of [Kc[0:kv_len]; K_cur] receives: the sum over all
+// query rows of the softmax probabilities exp(scale*q.k - lse_row), with lse
+// from fkv_chunk_attention over the same keys.  Workgroup = (256-row query
+// tile, head), 8 waves x 32 rows.  Per 64-key tile the waves compute S^T with
+// the attention kernel's score product (same MFMA sequence, so the same fp32
+// scores), form the probabilities, and for every key block the tile touches
+// reduce their sum across the wave with a fixed butterfly; lane 0 adds it to
+// the wave's own bin array in the workspace, so the result is deterministic.
+__device__ __forceinline__ float wave_sum_f(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_mass_kernel(AttnArgs a) {
+    using C = Cfg<D>;
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[C::TILE];
+    const int qt = blockIdx.x, h = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l32 = lane & 31, hl = lane >> 5;
+    const int Lq = a.Lq;
+    float *bins = a.part + (((size_t)h * a.n_qtiles + qt) * 8 + wave) * a.mass_bins;
+    for (int b = lane; b < a.mass_bins; b += 64) bins[b] = 0.f;
+
+    const int qrow = qt * BM + wave * 32 + l32;
+    const bool qok = qrow < Lq;
+    const uint16_t *Qh = (const uint16_t *)a.Q + (size_t)h * Lq * D;
+    bf16x8_t qf[C::KS];
+#pragma unroll
+    for (int kk = 0; kk < C::KS; ++kk) {
+        const u32x4 v = qok ? *(const u32x4 *)(Qh + (size_t)qrow * D + kk * 16 + hl * 8) : u32x4{0, 0, 0, 0};
+        qf[kk] = __builtin_bit_cast(bf16x8_t, v);
+    }
+    // rows past Lq contribute nothing: their bias is -inf
+    const float bias = qok ? -a.lse[(size_t)h * Lq + qrow] * 1.4426950408889634f : -__builtin_inff();
+    const float c2 = a.scale_log2;
+
+    const int kvl = head_kvl(a, h);
+    const int Lk = kvl + Lq;
+    const uint16_t *Kc = (const uint16_t *)a.Kc + (size_t)h * a.slab * D;
+    const uint16_t *Kq = (const uint16_t *)a.K_cur + (size_t)h * Lq * D;
+    // staging geometry: all 512 threads, rows r0 + RPP2*i
+    constexpr int RPP2 = kThreads / C::CPR;
+    constexpr int NV2 = BN / RPP2;
+    const int c = tid % C::CPR, r0 = tid / C::CPR;
+    const uint32_t voff = (uint32_t)(r0 * D + c * 8) * 2u;
+    const int wofs = r0 * C::RSE + c * 8;
+    const int kbase = l32 * C::RSE + hl * 8;
+    const int vbase = 0;
+
+    f32x16_t o[C::MB];
+    f32x16_t s[2];
+    bf16x8_t pb[4];
+    const int T = (Lk + BN - 1) / BN;
+    for (int t = 0; t < T; ++t) {
+        const int j0 = t * BN;
+        u32x4 stage[4];
+        load_tile<D, NV2>(Kc, Kq, j0, kvl, Lk, Lq, stage, voff, RPP2 * D * 2);
+        __syncthreads();  // the previous tile's reads are done
+#pragma unroll
+        for (int i = 0; i < NV2; ++i) *(u32x4 *)(Ks + wofs + i * RPP2 * C::RSE) = stage[i];
+        __syncthreads();
+        mfma_block<D, false, true>(nullptr, Ks, vbase, kbase, pb, qf, o, s);
+        // keys of this lane: j0 + 32kb + 8(i/4) + 4hl + i%4
+        const int b_first = j0 / a.mass_F, b_last = (min(j0 + BN, Lk) - 1) / a.mass_F;
+        for (int b = b_first; b <= b_last; ++b) {
+            const int lo = b * a.mass_F, hi = min(lo + a.mass_F, Lk);
+            float v = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int key = j0 + kb * 32 + 8 * (i >> 2) + 4 * hl + (i & 3);
+                    if (key >= lo && key < hi) v += __builtin_amdgcn_exp2f(fmaf(s[kb][i], c2, bias));
+                }
+            v = wave_sum_f(v);
+            if (lane == 0) bins[b] += v;
+        }
+    }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void attn_mass_finalize_kernel(AttnArgs a) {
+    const int h = blockIdx.x;
+    for (int b = threadIdx.x; b < a.mass_bins; b += 256) {
+        float v = 0.f;
+        for (int k = 0; k < a.n_qtiles * 8; ++k) v += a.part[((size_t)h * a.n_qtiles * 8 + k) * a.mass_bins + b];
+        float *out = a.mass_out + (size_t)h * a.mass_bins + b;
+        *out = a.mass_acc ? *out + v : v;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_attention_merge(const AttnArgs &a, int head_dim, hipStream_t s) {
@@ -537,6 +632,18 @@ hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s)
         hipLaunchKernelGGL((attn_bf16_kernel<128, false>), dim3(blocks), dim3(kThreads), 0, s, a);
     else
         hipLaunchKernelGGL((attn_bf16_kernel<64, false>), dim3(blocks), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_attention_mass(const AttnArgs &a, int head_dim, hipStream_t s) {
+    const dim3 grid((unsigned)a.n_qtiles, (unsigned)a.n_heads);
+    if (head_dim == 128) {
+        hipLaunchKernelGGL(attn_mass_kernel<128>, grid, dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(attn_mass_finalize_kernel<128>, dim3(a.n_heads), dim3(256), 0, s, a);
+    } else {
+        hipLaunchKernelGGL(attn_mass_kernel<64>, grid, dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(attn_mass_finalize_kernel<64>, dim3(a.n_heads), dim3(256), 0, s, a);
+    }
     return hipGetLastError();
 }
 

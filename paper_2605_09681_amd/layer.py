@@ -19,7 +19,8 @@ from typing import Optional, Sequence
 
 import torch
 
-from . import (FKV_DYNAMIC, FKV_STATIC, fkv_attention_workspace_size, fkv_chunk_attention,
+from . import (FKV_DYNAMIC, FKV_STATIC, fkv_attention_mass, fkv_attention_workspace_size,
+               fkv_chunk_attention, fkv_classify_heads,
                fkv_chunk_attention_fp8, fkv_compress_static, fkv_fp8_pack, fkv_fp8_sizes,
                fkv_num_segments, fkv_score_segments, fkv_score_workspace_size,
                fkv_select_compact, make_heads, make_shape, slab_tokens)
@@ -110,3 +111,38 @@ class CompressedLayer:
     def step(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse=None):
         self.compress(K_hist, V_hist, frame_slot, K_cur)
         self.attention(Q, K_cur, V_cur, O, lse)
+
+
+class HeadProfiler:
+    """Offline head profiling (Sec. 4.1, Eq. 1) of one layer.
+
+    Each :meth:`observe` call attends the chunk's queries over the uncompressed
+    cache (every head keeps the whole history, gathered with the static-head
+    kernel) and adds the attention mass of every history frame and chunk frame
+    to ``mass`` [n_heads][H + C] on the device.  :meth:`classify` applies Eq. 1
+    to the accumulated table."""
+
+    def __init__(self, n_heads: int, head_dim: int, frame_tokens: int, hist_frames: int,
+                 cap_frames: int, chunk_frames: int, device="cuda"):
+        self.H, self.C = hist_frames, chunk_frames
+        budgets = [type("B", (), dict(type=FKV_STATIC, sink_frames=0, recent_frames=hist_frames,
+                                      keep_k=0, scope=0))() for _ in range(n_heads)]
+        self.layer = CompressedLayer(n_heads, head_dim, frame_tokens, hist_frames, cap_frames,
+                                     chunk_frames, frame_tokens, "bf16", budgets, device=device)
+        dev = self.layer.device
+        self.mass = torch.zeros((n_heads, hist_frames + chunk_frames), dtype=torch.float32, device=dev)
+        self.lse = torch.empty((n_heads, self.layer.lq), dtype=torch.float32, device=dev)
+        self.O = torch.empty((n_heads, self.layer.lq, head_dim), dtype=torch.bfloat16, device=dev)
+        self.workspace = None
+        self.observed = 0
+
+    def observe(self, Q, K_hist, V_hist, frame_slot, K_cur, V_cur):
+        L = self.layer
+        L.compress_static(K_hist, V_hist, frame_slot)
+        L.attention(Q, K_cur, V_cur, self.O, self.lse)
+        self.workspace = fkv_attention_mass(L.shape, Q, L.Kc, L.kv_len, K_cur, self.lse, L.scale, self.mass,
+                                            accumulate=self.observed > 0, workspace=self.workspace)
+        self.observed += 1
+
+    def classify(self, alpha: float = 0.8, sink_frames: int = 1, transition_frames: int = 1):
+        return fkv_classify_heads(self.mass.cpu(), self.H, sink_frames, transition_frames, alpha)

@@ -162,6 +162,42 @@ def test_append_frames_errors(fkv):
     assert call(1, [0], p=None) == 1            # NULL tensor
 
 
+def test_classify_heads_matches_oracle(fkv):
+    """The library's Eq. 1 (host code) against the oracle on random mass tables,
+    including exact ties with alpha and zero sink / transition windows."""
+    rng = np.random.default_rng(5)
+    for trial in range(200):
+        H, C = int(rng.integers(0, 8)), int(rng.integers(1, 4))
+        mass = rng.random((6, H + C)).astype(np.float32) * rng.integers(1, 5, (6, H + C)).astype(np.float32)
+        sink, trans = int(rng.integers(0, 3)), int(rng.integers(0, 3))
+        alpha = float(rng.choice([0.5, 0.8, 0.9]))
+        want = oracle.classify_heads(mass.astype(np.float64), H, sink, trans, alpha).tolist()
+        assert fkv.fkv_classify_heads(mass, H, sink, trans, alpha) == want
+    tie = np.array([[0.0, 1.0, 0.0, 1.0, 3.0, 0.0]], np.float32)   # ratio exactly 0.8
+    assert fkv.fkv_classify_heads(tie, 4, 1, 1, 0.8) == [W.DYNAMIC]
+    L = fkv.lib()
+    out = (ctypes.c_int32 * 1)()
+    assert L.fkv_classify_heads(None, 1, 2, 1, 1, 1, ctypes.c_float(0.8), out) == 1
+    m = np.zeros((1, 2), np.float32)
+    assert L.fkv_classify_heads(m.ctypes.data_as(ctypes.c_void_p), 1, 2, 3, 1, 1, ctypes.c_float(0.8), out) == 1
+
+
+def test_attention_mass_arg_errors(fkv):
+    shape = _shape(fkv)              # F = 64, C = 1, slab must fit ceil((slab + 64) / 64) bins
+    L = fkv.lib()
+    need = fkv.fkv_attention_mass_workspace_size(shape, 5)
+    assert need > 0 and need % 256 == 0
+    call = lambda slab, bins, ws=need, acc=0: L.fkv_attention_mass(
+        ctypes.byref(shape), FAKE, FAKE, slab, FAKE, FAKE, FAKE, ctypes.c_float(0.1), bins, FAKE, acc, FAKE, ws, None)
+    assert call(256, 4) == 3          # 256 + 64 keys need 5 bins
+    assert call(256, 5, ws=need - 1) == 3
+    assert call(256, 5, acc=2) == 1
+    assert call(-1, 5) == 1
+    f32 = fkv.make_shape(2, 128, 64, 4, 4, 1, 64, "f32")
+    assert L.fkv_attention_mass(ctypes.byref(f32), FAKE, FAKE, 256, FAKE, FAKE, FAKE, ctypes.c_float(0.1), 5, FAKE,
+                                0, FAKE, need, None) == 2
+
+
 def test_attention_arg_errors(fkv):
     shape = _shape(fkv)
     L = fkv.lib()
