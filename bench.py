@@ -221,7 +221,7 @@ def main():
             "attention_schedule": args.schedule,
         },
         "roofline": {
-            "kernel": "attn_bf16_kernel<128> (fkv_chunk_attention)",
+            "kernel": "fkv_chunk_attention: attn_bf16_kernel<128, balanced> + attn_merge_kernel<128>",
             "bound": "mfma",
             "achieved": round(attn_tflops, 1),
             "peak": PEAK_BF16_TFLOPS,
