@@ -48,11 +48,14 @@ _lib = None
 
 
 def lib():
+    """The compiled oracle.  FKV_ORACLE_LIB may name another build of the same
+    source (the mutation tests load deliberately broken copies that way)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
+        path = os.environ.get("FKV_ORACLE_LIB", _LIB)
+        if path == _LIB and not os.path.exists(_LIB):
             build()
-        L = ctypes.CDLL(_LIB)
+        L = ctypes.CDLL(path)
         P, I, LG, D = ctypes.c_void_p, ctypes.c_int, ctypes.c_long, ctypes.c_double
         L.fkvo_static_frames.argtypes = [I, I, I, P]
         L.fkvo_static_frames.restype = I
