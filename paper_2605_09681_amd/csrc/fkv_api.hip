@@ -420,11 +420,6 @@ fkv_status select_compact_impl(const fkv_shape *shape, const fkv_head *heads, co
     sa.L = shape->seg_tokens;
     sa.H = shape->hist_frames;
     sa.n_seg = n_seg;
-    // With nothing cached (H = 0, the first AR step) the selection kernel only
-    // writes kv_len = 0 and there is nothing to copy.
-    fkv_status rs = device_status(fkv::launch_select(sa, (hipStream_t)stream), "fkv_select_compact select launch");
-    if (rs != FKV_OK || n_seg == 0) return rs;
-
     fkv::DynCopyArgs ca;
     memset(&ca, 0, sizeof ca);
     const size_t es = elem_size(shape);
@@ -445,6 +440,19 @@ fkv_status select_compact_impl(const fkv_shape *shape, const fkv_head *heads, co
     ca.n_seg = n_seg;
     ca.heads = sa.heads;
     for (int t = 0; t < shape->hist_frames; ++t) ca.slots.slot[t] = frame_slot[t];
+    // One launch when every copy workgroup can re-derive its head's keep set;
+    // otherwise the selection kernel, then the copy.  With nothing cached
+    // (H = 0, the first AR step) or nothing kept, only the selection kernel
+    // runs: it writes kv_len = 0 and the -1 padding of kept_seg.
+    if (n_seg > 0 && n_seg <= fkv::kFusedSelectMaxSeg && max_pieces > 0) {
+        fkv::SelectCopyArgs sc;
+        sc.sel = sa;
+        sc.copy = ca;
+        return device_status(fkv::launch_select_copy(sc, max_pieces, (hipStream_t)stream),
+                             "fkv_select_compact launch");
+    }
+    fkv_status rs = device_status(fkv::launch_select(sa, (hipStream_t)stream), "fkv_select_compact select launch");
+    if (rs != FKV_OK || n_seg == 0) return rs;
     return device_status(fkv::launch_dyn_copy(ca, max_pieces, (hipStream_t)stream),
                          "fkv_select_compact copy launch");
 }

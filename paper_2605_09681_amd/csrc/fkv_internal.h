@@ -75,6 +75,14 @@ struct SelectArgs {
     int32_t k[FKV_MAX_HEADS];       // kk = min(keep_k, |group|) per head
 };
 
+// Fused selection + compaction: used when a head has at most kFusedSelectMaxSeg
+// segments, so that every copy workgroup can re-derive its head's keep set.
+constexpr int kFusedSelectMaxSeg = 128;
+struct SelectCopyArgs {
+    SelectArgs sel;
+    DynCopyArgs copy;
+};
+
 // ------------------------------------------------------------------ scoring
 struct ScoreArgs {
     const uint8_t *K_hist, *K_cur;
@@ -140,6 +148,7 @@ hipError_t launch_static_copy(const StaticCopyArgs &a, int max_kept, hipStream_t
 hipError_t launch_dyn_copy(const DynCopyArgs &a, int max_pieces, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_heads, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, hipStream_t s);
+hipError_t launch_select_copy(const SelectCopyArgs &a, int max_pieces, hipStream_t s);
 hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s);
 hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s);
 size_t attention_part_bytes(int head_dim);  // bytes of one partial-result slot (bf16 kernel)

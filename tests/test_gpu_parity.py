@@ -142,6 +142,17 @@ def test_480p_sweep(L, frac):
     check_layer(cfg, x, rows=sample_rows(cfg.lq, 8, seed=L))
 
 
+def test_480p_many_segments():
+    """168 segments per head (an eighth of a frame each, per-frame groups): more
+    than the fused select + compact kernel takes, so the selection kernel and
+    the copy kernel run separately."""
+    cfg = W.wan_layer_config("480p", keep_fraction=0.5, seg_tokens=195)
+    assert cfg.hist_frames * cfg.frame_tokens // cfg.seg_tokens == 168
+    _print_case("480p-168-segments")
+    x = W.make_layer_inputs(cfg, seed=15)
+    check_layer(cfg, x, rows=sample_rows(cfg.lq, 8, seed=15))
+
+
 def test_480p_no_pruning_equals_full_attention():
     """Keep everything (dynamic f = 1, static recent = H): both head types
     reduce to full attention over the uncompressed cache."""
@@ -210,10 +221,12 @@ def test_empty_budgets():
     assert from_dev(layer.kv_len).tolist() == [0, 0, 0, 100]
 
 
-def test_select_crafted_scores():
-    """fkv_select_compact on crafted scores: ties, signed zeros and NaNs."""
-    import paper_2605_09681_amd as fkv
-    F, L, H = 64, 16, 6
+@pytest.mark.parametrize("F,L,H", [(64, 16, 6), (64, 4, 10)])
+def test_select_crafted_scores(F, L, H):
+    """fkv_select_compact on crafted scores: ties, signed zeros and NaNs, with
+    24 segments (selection inside the compaction kernel) and 160 segments
+    (separate selection kernel)."""
+    _print_case("crafted", F=F, L=L, H=H)
     heads = (W.HeadBudget(W.DYNAMIC, 0, 0, 5, W.SCOPE_GLOBAL), W.HeadBudget(W.DYNAMIC, 1, 1, 2, W.SCOPE_FRAME),
              W.HeadBudget(W.DYNAMIC, 0, 0, 7, W.SCOPE_GLOBAL), W.HeadBudget(W.DYNAMIC, 0, 2, 3, W.SCOPE_GLOBAL))
     cfg = W.LayerConfig("crafted", 4, 64, F, H, H, 1, L, "bf16", heads)
