@@ -10,7 +10,11 @@ of one layer:
 3. ``fkv_compress_static`` (static heads, Eq. 2)
 4. ``fkv_chunk_attention`` (all heads, Eq. 2 / Eq. 4)
 
-All four enqueue on the current torch stream; nothing synchronises.
+Steps 1-2 and step 3 touch disjoint heads, so :meth:`CompressedLayer.compress`
+runs the static gather on a second stream (default priority) alongside the
+dynamic heads' scoring and compaction; both are HBM-bound and neither fills
+the memory system alone.  Attention waits for both.  The individual stages
+enqueue on the current torch stream; nothing synchronises with the host.
 """
 from __future__ import annotations
 
@@ -30,7 +34,7 @@ class CompressedLayer:
     def __init__(self, n_heads: int, head_dim: int, frame_tokens: int, hist_frames: int,
                  cap_frames: int, chunk_frames: int, seg_tokens: int, dtype: str,
                  budgets: Sequence, device="cuda", slab: Optional[int] = None,
-                 balanced: bool = True):
+                 balanced: bool = True, overlap: bool = True):
         self.shape = make_shape(n_heads, head_dim, frame_tokens, hist_frames, cap_frames,
                                 chunk_frames, seg_tokens, dtype)
         self.heads = make_heads(budgets)
@@ -57,6 +61,9 @@ class CompressedLayer:
         self.scale = 1.0 / math.sqrt(head_dim)
         self.has_static = FKV_STATIC in self.types
         self.has_dynamic = FKV_DYNAMIC in self.types
+        # side stream for the static gather (only when both head types exist)
+        self.side = (torch.cuda.Stream(device=dev) if overlap and self.has_static and self.has_dynamic
+                     else None)
 
     # individual stages -------------------------------------------------------
     def score(self, K_hist, frame_slot, K_cur):
@@ -102,6 +109,17 @@ class CompressedLayer:
 
     # whole step --------------------------------------------------------------
     def compress(self, K_hist, V_hist, frame_slot, K_cur):
+        if self.side is not None:
+            main = torch.cuda.current_stream(self.device)
+            self.side.wait_stream(main)             # inputs written on the main stream
+            with torch.cuda.stream(self.side):
+                self.compress_static(K_hist, V_hist, frame_slot)
+            for t in (K_hist, V_hist):              # read on the side stream too
+                t.record_stream(self.side)
+            self.score(K_hist, frame_slot, K_cur)
+            self.select_compact(K_hist, V_hist, frame_slot)
+            main.wait_stream(self.side)             # attention reads every head's Kc/Vc/kv_len
+            return
         if self.has_dynamic:
             self.score(K_hist, frame_slot, K_cur)
             self.select_compact(K_hist, V_hist, frame_slot)
