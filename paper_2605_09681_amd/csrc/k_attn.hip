@@ -12,7 +12,8 @@
 // of 64.  Per wave and tile, with v_mfma_f32_32x32x16_bf16:
 //   S^T = K . Q^T   (A = K rows from LDS, B = the wave's Q rows, held in VGPRs),
 //                   2 x (d/16) MFMAs;
-//   online softmax in fp32 (exp2 with the scale folded into log2 units);
+//   online softmax in fp32 (exp2 with the scale folded into log2 units; the
+//                   row sum adds the bf16-rounded probabilities with v_dot2);
 //   O^T += V^T . P^T (A = rows of a V^T tile in LDS, B = P taken straight from
 //                    the S^T accumulators, rounded to bf16), 4 x (d/32) MFMAs.
 // Computing S transposed makes each lane own one query column, so P needs no
@@ -49,6 +50,7 @@ namespace {
 using namespace attn;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
@@ -56,6 +58,7 @@ constexpr int kThreads = 512;      // 8 waves: two groups of 4
 constexpr int kGroupThreads = 256; // one group stages a whole K or V tile
 constexpr float kRescaleSlack = 8.f;  // log2 units the running max may lag behind
 constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw 32-bit buffer, range checked
+constexpr bf16x2_t kOnes2 = {(__bf16)1.f, (__bf16)1.f};
 
 template <int D>
 struct Cfg {
@@ -301,11 +304,21 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
 #pragma unroll
         for (int t = 0; t < 4; ++t)
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const float p = __builtin_amdgcn_exp2f(fmaf(s[t >> 1][8 * (t & 1) + j], c2, -m_run));
-                l_run += p;
-                pb[t][j] = (__bf16)p;
+            for (int j = 0; j < 8; ++j)
+                pb[t][j] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[t >> 1][8 * (t & 1) + j], c2, -m_run));
+        // The row sum adds the bf16-rounded probabilities -- exactly the P the
+        // value product consumes -- two at a time (v_dot2 against (1, 1)),
+        // in two chains: half the VALU instructions of fp32 adds.
+        float l2 = 0.f;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const bf16x2_t pr = {pb[t][2 * j], pb[t][2 * j + 1]};
+                if (t & 1) l2 = __builtin_amdgcn_fdot2_f32_bf16(pr, kOnes2, l2, false);
+                else l_run = __builtin_amdgcn_fdot2_f32_bf16(pr, kOnes2, l_run, false);
             }
+        l_run += l2;
     };
 
     // Prologue: group 0 copies K(0) and K(1) into LDS, group 1 copies V(0);

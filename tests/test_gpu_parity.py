@@ -120,7 +120,16 @@ def test_schedules_agree_480p():
     ou = W.bf16_bits_to_f32(from_dev(Ou)).astype(np.float64)
     tol = np.abs(ou) * 2.0 ** -7 + 2e-4
     assert (np.abs(ob - ou) <= tol).all(), float(np.abs(ob - ou).max())
-    np.testing.assert_allclose(from_dev(lb), from_dev(lu), rtol=0, atol=1e-4)
+    # Each schedule's normaliser sums probabilities rounded to bf16 against its
+    # own running maxima: each is within a relative 2^-9 of the exact sum, so
+    # the two lse differ by at most 2 * -log(1 - 2^-9) (+1e-4 for the score
+    # accumulation order).  With independent roundings of n_eff >= 1000
+    # effective terms, each sum's relative error has standard deviation at most
+    # 2^-9 / sqrt(3 * 1000) = 3.6e-5, so the RMS difference stays below 1e-4.
+    dl = from_dev(lb).astype(np.float64) - from_dev(lu).astype(np.float64)
+    bound = -2 * math.log1p(-2.0 ** -9) + 1e-4
+    rms = float(np.sqrt(np.mean(dl ** 2)))
+    assert float(np.abs(dl).max()) <= bound and rms <= 1e-4, (float(np.abs(dl).max()), rms)
 
 
 def test_small_fp32_multitile():
