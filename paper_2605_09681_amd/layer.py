@@ -23,11 +23,12 @@ from typing import Optional, Sequence
 
 import torch
 
-from . import (FKV_DYNAMIC, FKV_STATIC, fkv_attention_mass, fkv_attention_workspace_size,
-               fkv_chunk_attention, fkv_classify_heads,
+from . import (FKV_DYNAMIC, FKV_STATIC, fkv_append_frames, fkv_attention_mass,
+               fkv_attention_workspace_size, fkv_chunk_attention, fkv_classify_heads,
                fkv_chunk_attention_fp8, fkv_compress_static, fkv_fp8_pack, fkv_fp8_sizes,
-               fkv_num_segments, fkv_score_segments, fkv_score_workspace_size,
-               fkv_select_compact, make_heads, make_shape, slab_tokens)
+               fkv_num_segments, fkv_score_pooled, fkv_score_pooled_workspace_size,
+               fkv_score_segments, fkv_score_workspace_size, fkv_select_compact,
+               fkv_select_compact_pooled, make_heads, make_shape, slab_tokens)
 
 
 class CompressedLayer:
@@ -164,3 +165,128 @@ class HeadProfiler:
 
     def classify(self, alpha: float = 0.8, sink_frames: int = 1, transition_frames: int = 1):
         return fkv_classify_heads(self.mass.cpu(), self.H, sink_frames, transition_frames, alpha)
+
+
+class RolloutStack:
+    """A stack of attention layers in a streaming AR rollout.
+
+    Every layer owns a rolling K/V cache of ``window`` frame slots
+    ([n_heads][window][F][d]); the caller maps logical history frames to slots
+    (``frame_slot``, sink pinned, the others rotating) and writes each finished
+    chunk's frames back with :meth:`append`.  Layers run one after another, so
+    they share one set of compressed-cache buffers, sized for a full window;
+    the history length H = len(frame_slot) may grow from chunk to chunk (0 on
+    the first one).  Per layer and AR step :meth:`run_layer` makes the four
+    C-ABI calls (the static gather on a side stream next to the dynamic heads'
+    scoring and compaction), or -- with a shared score row from
+    :meth:`score_pooled` -- the first-block proxy of Sec. 4.3: one similarity
+    row computed from one layer's keys pooled over all heads and reused by the
+    dynamic heads of every layer.  ``budgets`` are per-head objects with
+    type/sink_frames/recent_frames/keep_k/scope for the given H."""
+
+    def __init__(self, n_layers: int, n_heads: int, head_dim: int, frame_tokens: int, window: int,
+                 chunk_frames: int, seg_tokens: int, dtype: str = "bf16", device="cuda",
+                 overlap: bool = True):
+        self.n_layers, self.n_heads, self.d = n_layers, n_heads, head_dim
+        self.F, self.window, self.C, self.L = frame_tokens, window, chunk_frames, seg_tokens
+        self.dtype_name = dtype
+        self.dtype = torch.bfloat16 if dtype in ("bf16", 0) else torch.float32
+        self.device = torch.device(device)
+        dev, dt = self.device, self.dtype
+        hist = (n_heads, window, frame_tokens, head_dim)
+        self.K_hist = [torch.zeros(hist, dtype=dt, device=dev) for _ in range(n_layers)]
+        self.V_hist = [torch.zeros(hist, dtype=dt, device=dev) for _ in range(n_layers)]
+        full = self._shape(window)
+        self.n_seg_max = fkv_num_segments(full)
+        self.slab = window * frame_tokens
+        self.Kc = torch.zeros((n_heads, self.slab, head_dim), dtype=dt, device=dev)
+        self.Vc = torch.zeros_like(self.Kc)
+        self.kv_len = torch.zeros((n_heads,), dtype=torch.int32, device=dev)
+        self._scores = torch.zeros((n_heads * max(self.n_seg_max, 1),), dtype=torch.float32, device=dev)
+        self._kept = torch.full((n_heads * max(self.n_seg_max, 1),), -1, dtype=torch.int32, device=dev)
+        self.pooled_row = torch.zeros((max(self.n_seg_max, 1),), dtype=torch.float32, device=dev)
+        # workspaces: the largest history with every head dynamic bounds the scoring workspace
+        all_dyn = make_heads([_Budget(FKV_DYNAMIC, 0, 0, 0, 1)] * n_heads)
+        self.score_ws = torch.empty(max(fkv_score_workspace_size(full, all_dyn), 1), dtype=torch.uint8, device=dev)
+        self.pooled_ws = torch.empty(max(fkv_score_pooled_workspace_size(full), 1), dtype=torch.uint8, device=dev)
+        with torch.cuda.device(dev):
+            n = fkv_attention_workspace_size(full)
+        self.attn_ws = torch.empty(max(n, 1), dtype=torch.uint8, device=dev) if n > 0 else None
+        self.scale = 1.0 / math.sqrt(head_dim)
+        self.side = torch.cuda.Stream(device=dev) if overlap else None
+        self._shapes, self._heads = {}, {}
+
+    def _shape(self, H: int):
+        return make_shape(self.n_heads, self.d, self.F, H, self.window, self.C, self.L, self.dtype_name)
+
+    def shape(self, H: int):
+        if H not in self._shapes:
+            self._shapes[H] = self._shape(H)
+        return self._shapes[H]
+
+    def _budget_array(self, budgets):
+        key = tuple((int(b.type), int(b.sink_frames), int(b.recent_frames), int(b.keep_k), int(b.scope))
+                    for b in budgets)
+        if key not in self._heads:
+            self._heads[key] = make_heads(budgets)
+        return self._heads[key], key
+
+    def views(self, H: int):
+        """scores and kept_seg of the current history length, as [n_heads][n_seg] tensors."""
+        n_seg = fkv_num_segments(self.shape(H))
+        k = self.n_heads * n_seg
+        return self._scores[:k].view(self.n_heads, n_seg), self._kept[:k].view(self.n_heads, n_seg)
+
+    def score_pooled(self, layer: int, frame_slot, K_cur):
+        """The first-block proxy: one score row pooled over all heads of ``layer``."""
+        H = len(frame_slot)
+        if H == 0:
+            return self.pooled_row[:0]
+        shape = self.shape(H)
+        row = self.pooled_row[:fkv_num_segments(shape)]
+        fkv_score_pooled(shape, self.K_hist[layer], frame_slot, K_cur, row, self.pooled_ws)
+        return row
+
+    def run_layer(self, layer: int, budgets, frame_slot, Q, K_cur, V_cur, O, lse=None, pooled=None):
+        """One AR step of one layer: compress its cache, then chunk attention
+        into O.  ``pooled`` (a row from :meth:`score_pooled`) replaces the
+        layer's own per-head scoring."""
+        H = len(frame_slot)
+        shape = self.shape(H)
+        heads, key = self._budget_array(budgets)
+        types = [b[0] for b in key]
+        Kh, Vh = self.K_hist[layer], self.V_hist[layer]
+        scores, kept = self.views(H)
+        has_static, has_dynamic = FKV_STATIC in types, FKV_DYNAMIC in types
+        main = torch.cuda.current_stream(self.device)
+        side = self.side if (self.side is not None and has_static and has_dynamic) else None
+        if side is not None:
+            side.wait_stream(main)
+            with torch.cuda.stream(side):
+                fkv_compress_static(shape, heads, Kh, Vh, frame_slot, self.Kc, self.Vc, self.kv_len)
+            for t in (Kh, Vh):
+                t.record_stream(side)
+        elif has_static:
+            fkv_compress_static(shape, heads, Kh, Vh, frame_slot, self.Kc, self.Vc, self.kv_len)
+        if has_dynamic:
+            if pooled is not None:
+                fkv_select_compact_pooled(shape, heads, pooled, Kh, Vh, frame_slot, kept, self.Kc, self.Vc,
+                                          self.kv_len)
+            else:
+                fkv_score_segments(shape, heads, Kh, frame_slot, K_cur, scores, self.score_ws)
+                fkv_select_compact(shape, heads, scores, Kh, Vh, frame_slot, kept, self.Kc, self.Vc,
+                                   self.kv_len)
+        if side is not None:
+            main.wait_stream(side)
+        fkv_chunk_attention(shape, Q, self.Kc, self.Vc, self.kv_len, K_cur, V_cur, self.scale, O, lse,
+                            self.attn_ws)
+
+    def append(self, layer: int, K_new, V_new, dst_slots):
+        """Write a finished chunk's frames ([n_heads][n*F][d]) into the layer's cache slots."""
+        fkv_append_frames(self.shape(0), K_new, V_new, dst_slots, self.K_hist[layer], self.V_hist[layer])
+
+
+class _Budget:
+    def __init__(self, type, sink_frames, recent_frames, keep_k, scope):
+        self.type, self.sink_frames, self.recent_frames, self.keep_k, self.scope = \
+            type, sink_frames, recent_frames, keep_k, scope

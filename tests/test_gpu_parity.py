@@ -498,3 +498,99 @@ def test_random_and_uniform_segment_pruning(policy):
         if policy == "uniform":   # kept segments within every non-sink frame: 0, 1, 3, 4 of 6 (k = 4)
             sel = want[:cnt]
             assert sorted(set((sel[sel >= 6] % 6).tolist())) == sorted({(i * 6) // k for i in range(k)})
+
+
+# ---------------------------------------------------------------------------
+# the layer-stack rollout driver
+# ---------------------------------------------------------------------------
+def _stack_budgets(mask_row, H, F, L):
+    """Per-head budgets of one layer for history length H: static heads keep the
+    sink and the last two frames, dynamic heads the sink plus half of the
+    candidate segments (one global group)."""
+    n_seg = (H * F + L - 1) // L
+    k = max((n_seg - (F + L - 1) // L) // 2, 0)
+    return tuple(W.HeadBudget(W.DYNAMIC, 1, 0, k, W.SCOPE_GLOBAL) if m == W.DYNAMIC else
+                 W.HeadBudget(W.STATIC, 1, 2) for m in mask_row)
+
+
+@pytest.mark.parametrize("pooled", [False, True])
+def test_rollout_stack(pooled):
+    """RolloutStack: 3 layers with their own head masks and rolling caches
+    (window 7, sink pinned, 2-frame chunks) over 6 chunks of 2 AR steps, across
+    the ring wrap, sharing one set of compressed buffers.  Every layer's step is
+    checked against the oracle (compression bit-exact, attention on every row);
+    with pooled=True the dynamic heads of every layer select with the score row
+    pooled over all heads of layer 0 (the first-block proxy)."""
+    import paper_2605_09681_amd as fkv
+    from paper_2605_09681_amd.layer import RolloutStack
+    from types import SimpleNamespace
+    n_layers, nh, d, F, window, C, L = 3, 4, 64, 64, 7, 2, 32
+    n_chunks, n_steps = 6, 2
+    masks = W.rollout_head_masks(21, n_layers=n_layers, n_heads=nh, n_dynamic=2)
+    stack = RolloutStack(n_layers, nh, d, F, window, C, L)
+    K_o = np.zeros((n_layers, nh, window, F, d), np.uint16)
+    V_o = np.zeros_like(K_o)
+    for i in range(n_chunks):
+        slots = W.ring_frame_slots(i, C, window)
+        H = len(slots)
+        for step in range(n_steps):
+            ex = (i, step)
+            Kq = W.normal_tensor(22, 1, (nh, C * F, d), "bf16", extra=ex)
+            Vq = W.normal_tensor(22, 2, (nh, C * F, d), "bf16", extra=ex)
+            Q = W.normal_tensor(22, 3, (nh, C * F, d), "bf16", extra=ex)
+            Kq_d, Vq_d, Q_d = to_dev(Kq, "bf16"), to_dev(Vq, "bf16"), to_dev(Q, "bf16")
+            row = None
+            if pooled and H > 0:
+                row_d = stack.score_pooled(0, slots, Kq_d)
+                row_want, _ = oracle.score_pooled(K_o[0], slots, Kq, H, L)
+                torch.cuda.synchronize()
+                np.testing.assert_array_equal(from_dev(row_d).view(np.uint32), row_want.view(np.uint32))
+                row = row_d
+            for layer in range(n_layers):
+                _print_case("rollout-stack", pooled=pooled, chunk=i, step=step, layer=layer)
+                heads = _stack_budgets(masks[layer], H, F, L)
+                O = torch.empty_like(Q_d)
+                lse = torch.empty((nh, C * F), dtype=torch.float32, device="cuda")
+                stack.run_layer(layer, heads, slots, Q_d, Kq_d, Vq_d, O, lse, pooled=row)
+                torch.cuda.synchronize()
+                cfg = W.LayerConfig("stack", nh, d, F, H, window, C, L, "bf16", heads)
+                x = W.LayerInputs(cfg, K_o[layer], V_o[layer], Kq, Vq, Q, slots)
+                scores, kept = stack.views(H)
+                got = SimpleNamespace(kv_len=stack.kv_len, scores=scores, kept_seg=kept, Kc=stack.Kc, Vc=stack.Vc)
+                if row is None:
+                    ref = oracle.run_layer(cfg, x, scale=1 / math.sqrt(d))
+                    assert_compression_exact(cfg, got, ref)
+                else:
+                    ref = oracle.run_layer(cfg, x, scale=1 / math.sqrt(d), attention=False)
+                    kept_d, kv_d = from_dev(kept), from_dev(stack.kv_len)
+                    Kc_d, Vc_d = from_dev(stack.Kc), from_dev(stack.Vc)
+                    for h, b in enumerate(heads):
+                        if b.type == W.DYNAMIC:
+                            want, cnt = oracle.select_head(row_want, H, F, L, b.sink_frames, b.recent_frames,
+                                                           b.keep_k, b.scope)
+                            np.testing.assert_array_equal(kept_d[h], want)
+                            kc = oracle.compact_head(K_o[layer][h], slots, want[:cnt], H, L)
+                            vc = oracle.compact_head(V_o[layer][h], slots, want[:cnt], H, L)
+                        else:
+                            kc, vc = ref.Kc[h], ref.Vc[h]
+                        assert int(kv_d[h]) == kc.shape[0]
+                        np.testing.assert_array_equal(Kc_d[h, :kc.shape[0]], kc)
+                        np.testing.assert_array_equal(Vc_d[h, :vc.shape[0]], vc)
+                    rows = np.arange(C * F, dtype=np.int32)
+                    Kc_l = [Kc_d[h, :int(kv_d[h])] for h in range(nh)]
+                    Vc_l = [Vc_d[h, :int(kv_d[h])] for h in range(nh)]
+                    att = [oracle.attention_rows(Q[h], Kc_l[h], Vc_l[h], Kq[h], Vq[h], 1 / math.sqrt(d), rows)
+                           for h in range(nh)]
+                    ref = oracle.LayerResult(None, None, None, None, None, None, rows,
+                                             np.stack([a[0] for a in att]), np.stack([a[1] for a in att]))
+                assert_attention_close(O, ref, "bf16", lse)
+        dst = W.chunk_write_slots(i, C, window)
+        for layer in range(n_layers):
+            stack.append(layer, Kq_d, Vq_d, dst.tolist())
+            for h in range(nh):
+                oracle.append_frames(K_o[layer][h], Kq[h].reshape(C, F, d), dst)
+                oracle.append_frames(V_o[layer][h], Vq[h].reshape(C, F, d), dst)
+    torch.cuda.synchronize()
+    for layer in range(n_layers):
+        np.testing.assert_array_equal(from_dev(stack.K_hist[layer]), K_o[layer])
+        np.testing.assert_array_equal(from_dev(stack.V_hist[layer]), V_o[layer])
