@@ -14,8 +14,9 @@ layers of a real rollout would), so a step never finds its cache in the
 
 Prints ONE JSON line (see the keys below).  `value` is the wall-clock ms per
 step over the timed steps (lower is better); in the timed step the static
-heads' gather runs on a side stream next to the dynamic heads' scoring and
-compaction (they touch disjoint heads).  The per-stage breakdown comes from a
+heads' gather and attention run on a side stream while the dynamic heads are
+scored, compacted and attended on the main stream (they touch disjoint
+heads).  The per-stage breakdown comes from a
 second pass that runs the four calls one after another with HIP events
 between them.  `roofline` covers the dominant
 kernel (chunk attention, MFMA-bound) timed with HIP events on the stream the
@@ -150,12 +151,11 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step(i):
-        """The timed step: compression (the static gather on a side stream,
-        overlapped with the dynamic heads' scoring and compaction), then
-        attention over every head's compressed cache."""
+        """The timed step (CompressedLayer.step): the static heads' gather and
+        attention on a side stream while the dynamic heads are scored,
+        compacted and attended on the main stream."""
         L, b = layers[i % len(layers)], bufs[i % len(layers)]
-        L.compress(b["K_hist"], b["V_hist"], slots, b["K_cur"])
-        L.attention(b["Q"], b["K_cur"], b["V_cur"], b["O"])
+        L.step(b["K_hist"], b["V_hist"], slots, b["Q"], b["K_cur"], b["V_cur"], b["O"])
 
     def staged(i, ev):
         """The same four calls one after another on one stream, with HIP
@@ -235,7 +235,7 @@ def main():
             "kv_len": kv_len.tolist(),
             "rotating_copies": args.copies,
             "attention_schedule": args.schedule,
-            "step": "static gather on a side stream, overlapped with scoring + select/compact",
+            "step": "static heads (gather + attention) on a side stream, dynamic heads (score + select/compact + attention) on the main stream",
         },
         "roofline": {
             "kernel": "fkv_chunk_attention: attn_bf16_kernel<128, balanced> + attn_merge_kernel<128>",

@@ -236,6 +236,23 @@ fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q,
                                float *lse, void *workspace, size_t workspace_bytes,
                                void *stream);
 
+/* fkv_chunk_attention restricted to the heads head_list[0..n_list) (host
+ * int32 array; distinct indices in [0, n_heads)): only those heads' rows of O
+ * and lse are written, every other byte is left as it was.  Arguments,
+ * layouts, schedule and workspace are as in fkv_chunk_attention; the balanced
+ * schedule spreads the listed heads' work over all compute units.  This lets a
+ * caller attend the heads whose compressed cache is ready (the static heads
+ * after fkv_compress_static) while other heads are still being compressed on
+ * another stream -- each concurrent call needs its own workspace.  n_list = 0
+ * enqueues nothing.  FKV_ERR_ARG for a bad list (out of range, repeated,
+ * NULL with n_list > 0). */
+fkv_status fkv_chunk_attention_heads(const fkv_shape *shape, const int32_t *head_list,
+                                     int32_t n_list, const void *Q, const void *Kc,
+                                     const void *Vc, int32_t slab, const int32_t *kv_len,
+                                     const void *K_cur, const void *V_cur, float scale,
+                                     void *O, float *lse, void *workspace,
+                                     size_t workspace_bytes, void *stream);
+
 /* ---------------------------------------------------------------------------
  * Offline head profiling (Sec. 4.1, Eq. 1).  A profiling pass runs the layer
  * on the uncompressed cache (every head static with recent_frames = H, so Kc

@@ -13,6 +13,7 @@ Entry points (see ``include/fkv.h`` for the full contract):
 * :func:`fkv_score_segments`   -- segment similarity (Sec. 4.3, Eq. 3)
 * :func:`fkv_select_compact`   -- BottomK + compaction (Sec. 4.3, Eq. 3)
 * :func:`fkv_chunk_attention`  -- chunk attention (Eq. 2 / Eq. 4)
+* :func:`fkv_chunk_attention_heads` -- the same for a subset of heads
 * :func:`fkv_append_frames`    -- rolling-cache write of a finished chunk
 * :func:`fkv_fp8_pack`, :func:`fkv_chunk_attention_fp8` -- the FP8 variant of
   the chunk attention (App. F)
@@ -43,7 +44,8 @@ EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_score_workspace_size", "fkv_score_segments", "fkv_select_compact",
             "fkv_append_frames", "fkv_score_pooled_workspace_size", "fkv_score_pooled",
             "fkv_select_compact_pooled",
-            "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_fp8_sizes", "fkv_fp8_pack",
+            "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_chunk_attention_heads",
+            "fkv_fp8_sizes", "fkv_fp8_pack",
             "fkv_chunk_attention_fp8", "fkv_attention_mass_workspace_size", "fkv_attention_mass",
             "fkv_classify_heads", "fkv_last_error")
 
@@ -109,6 +111,8 @@ def lib():
         L.fkv_attention_workspace_size.restype = ctypes.c_int
         L.fkv_chunk_attention.argtypes = [S, P, P, P, I32, P, P, P, F, P, P, P, SZ, P]
         L.fkv_chunk_attention.restype = ctypes.c_int
+        L.fkv_chunk_attention_heads.argtypes = [S, P, I32, P, P, P, I32, P, P, P, F, P, P, P, SZ, P]
+        L.fkv_chunk_attention_heads.restype = ctypes.c_int
         L.fkv_fp8_sizes.argtypes = [S, I32] + [ctypes.POINTER(SZ)] * 4
         L.fkv_fp8_sizes.restype = ctypes.c_int
         L.fkv_fp8_pack.argtypes = [S, P, P, P, I32, P, P, P, P, P, P, P, P, SZ, P]
@@ -328,11 +332,7 @@ def fkv_attention_workspace_size(shape: fkv_shape) -> int:
     return int(out.value)
 
 
-def fkv_chunk_attention(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, scale: float, O,
-                        lse: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
-                        stream=None):
-    """``workspace`` (uint8 device tensor of fkv_attention_workspace_size bytes)
-    selects the balanced schedule; None runs one workgroup per query tile."""
+def _attention_args(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, O, lse, workspace):
     dt = _torch_dtype(shape)
     chunk = (shape.n_heads, _lq(shape), shape.head_dim)
     slab = Kc.shape[1] if Kc.dim() == 3 else -1
@@ -346,8 +346,31 @@ def fkv_chunk_attention(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, scale
     ws, nws = None, 0
     if workspace is not None:
         ws, nws = _check(workspace, "workspace", torch.uint8), workspace.numel()
-    _raise(lib().fkv_chunk_attention(ctypes.byref(shape), q, kc, vc, int(slab), kl, kq, vq,
+    return q, kc, vc, int(slab), kl, kq, vq, o, ls, ws, nws
+
+
+def fkv_chunk_attention(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, scale: float, O,
+                        lse: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                        stream=None):
+    """``workspace`` (uint8 device tensor of fkv_attention_workspace_size bytes)
+    selects the balanced schedule; None runs one workgroup per query tile."""
+    q, kc, vc, slab, kl, kq, vq, o, ls, ws, nws = _attention_args(shape, Q, Kc, Vc, kv_len, K_cur, V_cur, O,
+                                                                  lse, workspace)
+    _raise(lib().fkv_chunk_attention(ctypes.byref(shape), q, kc, vc, slab, kl, kq, vq,
                                      ctypes.c_float(scale), o, ls, ws, nws, _stream(stream)))
+
+
+def fkv_chunk_attention_heads(shape: fkv_shape, heads: Sequence[int], Q, Kc, Vc, kv_len, K_cur, V_cur,
+                              scale: float, O, lse: Optional[torch.Tensor] = None,
+                              workspace: Optional[torch.Tensor] = None, stream=None):
+    """fkv_chunk_attention for the listed heads only (host ints); the other
+    heads' rows of O and lse are left untouched."""
+    q, kc, vc, slab, kl, kq, vq, o, ls, ws, nws = _attention_args(shape, Q, Kc, Vc, kv_len, K_cur, V_cur, O,
+                                                                  lse, workspace)
+    ids = [int(h) for h in heads]
+    arr = (ctypes.c_int32 * max(len(ids), 1))(*ids)
+    _raise(lib().fkv_chunk_attention_heads(ctypes.byref(shape), arr, len(ids), q, kc, vc, slab, kl, kq, vq,
+                                           ctypes.c_float(scale), o, ls, ws, nws, _stream(stream)))
 
 
 def fkv_fp8_sizes(shape: fkv_shape, slab: int):

@@ -20,6 +20,9 @@ __device__ __forceinline__ int head_tiles(const AttnArgs &a, int h) {
     return (head_kvl(a, h) + a.Lq + BN - 1) / BN;
 }
 
+// Work items are (entry li of the launch's head list, query tile qt),
+// li-major; the head is h = heads.head[li].
+//
 // Balanced schedule.  Work item i = (head h, query tile qt), h-major, has
 // T_h key tiles; concatenating all items gives one sequence of `total` tiles,
 // which G = min(n_blocks, total) workgroups split into equal contiguous ranges:
@@ -34,9 +37,26 @@ struct Schedule {
     __device__ __forceinline__ int owner(int64_t x) const { return (int)(((x + 1) * G - 1) / total); }
 };
 
+// The item holding tile x of the concatenated sequence: list entry li, its
+// query tile qt, the item's first tile ibase and its tile count T.
+struct ItemPos {
+    int li, qt, T;
+    int64_t ibase;
+};
+__device__ __forceinline__ ItemPos locate(const AttnArgs &a, int64_t x) {
+    int li = 0, T = head_tiles(a, a.heads.head[0]);
+    int64_t base = 0;
+    while (x >= base + (int64_t)a.n_qtiles * T) {
+        base += (int64_t)a.n_qtiles * T;
+        T = head_tiles(a, a.heads.head[++li]);
+    }
+    const int qt = (int)((x - base) / T);
+    return ItemPos{li, qt, T, base + (int64_t)qt * T};
+}
+
 __device__ __forceinline__ Schedule make_schedule(const AttnArgs &a) {
     int64_t total = 0;
-    for (int h = 0; h < a.n_heads; ++h) total += (int64_t)a.n_qtiles * head_tiles(a, h);
+    for (int li = 0; li < a.heads.n; ++li) total += (int64_t)a.n_qtiles * head_tiles(a, a.heads.head[li]);
     Schedule sc;
     sc.total = total;
     sc.G = (int)(total < a.n_blocks ? total : a.n_blocks);

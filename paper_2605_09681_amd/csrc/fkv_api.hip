@@ -520,12 +520,24 @@ fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes) {
     return ok();
 }
 
-fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q, const void *Kc, const void *Vc,
-                               int32_t slab, const int32_t *kv_len, const void *K_cur,
-                               const void *V_cur, float scale, void *O, float *lse, void *workspace,
-                               size_t workspace_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Identity head list (every head of the shape, in order).
+fkv::HeadList all_heads(int n_heads) {
+    fkv::HeadList l;
+    memset(&l, 0, sizeof l);
+    l.n = n_heads;
+    for (int h = 0; h < n_heads; ++h) l.head[h] = h;
+    return l;
+}
+
+fkv_status chunk_attention_impl(const fkv_shape *shape, const fkv::HeadList &list, const void *Q,
+                                const void *Kc, const void *Vc, int32_t slab, const int32_t *kv_len,
+                                const void *K_cur, const void *V_cur, float scale, void *O, float *lse,
+                                void *workspace, size_t workspace_bytes, void *stream) {
     fkv_status st;
-    if ((st = check_shape(shape)) != FKV_OK) return st;
     if (!Q || !K_cur || !V_cur || !O || !kv_len) return fail(FKV_ERR_ARG, "NULL tensor pointer");
     if (slab < 0) return fail(FKV_ERR_ARG, "slab %d < 0", slab);
     if (slab > 0 && (!Kc || !Vc)) return fail(FKV_ERR_ARG, "NULL Kc/Vc with slab %d", slab);
@@ -538,6 +550,7 @@ fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q, const void
         if (workspace_bytes < need)
             return fail(FKV_ERR_CAPACITY, "attention workspace of %zu bytes, %zu needed", workspace_bytes, need);
     }
+    if (list.n == 0) return ok();
 
     fkv::AttnArgs a;
     memset(&a, 0, sizeof a);
@@ -551,12 +564,13 @@ fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q, const void
     a.kv_len = kv_len;
     a.slab = slab;
     a.n_heads = shape->n_heads;
+    a.heads = list;
     a.Lq = shape->chunk_frames * shape->frame_tokens;
     a.scale = scale;
     a.scale_log2 = scale * 1.4426950408889634f;
     const int rows = bf16 ? fkv::kAttnRowsBf16 : fkv::kAttnRowsF32;
     a.n_qtiles = (a.Lq + rows - 1) / rows;
-    a.n_items = a.n_heads * a.n_qtiles;
+    a.n_items = list.n * a.n_qtiles;
     a.items_per_xcd = (a.n_items + 7) / 8;
     a.n_blocks = blocks;
     a.part = (float *)workspace;
@@ -564,6 +578,43 @@ fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q, const void
     hipError_t e = bf16 ? fkv::launch_attention_bf16(a, shape->head_dim, (hipStream_t)stream)
                         : fkv::launch_attention_f32(a, shape->head_dim, (hipStream_t)stream);
     return device_status(e, "fkv_chunk_attention launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q, const void *Kc, const void *Vc,
+                               int32_t slab, const int32_t *kv_len, const void *K_cur,
+                               const void *V_cur, float scale, void *O, float *lse, void *workspace,
+                               size_t workspace_bytes, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    return chunk_attention_impl(shape, all_heads(shape->n_heads), Q, Kc, Vc, slab, kv_len, K_cur, V_cur,
+                                scale, O, lse, workspace, workspace_bytes, stream);
+}
+
+fkv_status fkv_chunk_attention_heads(const fkv_shape *shape, const int32_t *head_list, int32_t n_list,
+                                     const void *Q, const void *Kc, const void *Vc, int32_t slab,
+                                     const int32_t *kv_len, const void *K_cur, const void *V_cur,
+                                     float scale, void *O, float *lse, void *workspace,
+                                     size_t workspace_bytes, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if (n_list < 0 || n_list > shape->n_heads) return fail(FKV_ERR_ARG, "n_list %d outside [0, %d]", n_list, shape->n_heads);
+    if (n_list > 0 && !head_list) return fail(FKV_ERR_ARG, "head_list is NULL");
+    fkv::HeadList list;
+    memset(&list, 0, sizeof list);
+    bool seen[FKV_MAX_HEADS] = {};
+    for (int i = 0; i < n_list; ++i) {
+        const int h = head_list[i];
+        if (h < 0 || h >= shape->n_heads) return fail(FKV_ERR_ARG, "head_list[%d] = %d outside [0, %d)", i, h, shape->n_heads);
+        if (seen[h]) return fail(FKV_ERR_ARG, "head %d listed twice", h);
+        seen[h] = true;
+        list.head[list.n++] = h;
+    }
+    return chunk_attention_impl(shape, list, Q, Kc, Vc, slab, kv_len, K_cur, V_cur, scale, O, lse,
+                                workspace, workspace_bytes, stream);
 }
 
 fkv_status fkv_fp8_sizes(const fkv_shape *shape, int32_t slab, size_t *q_bytes, size_t *kv_bytes,
@@ -648,6 +699,7 @@ fkv_status fkv_chunk_attention_fp8(const fkv_shape *shape, const void *Q8, const
     a.kv_len = kv_len;
     a.slab = slab;
     a.n_heads = shape->n_heads;
+    a.heads = all_heads(shape->n_heads);
     a.Lq = shape->chunk_frames * shape->frame_tokens;
     a.scale = scale;
     a.scale_log2 = scale * 1.4426950408889634f;
@@ -704,6 +756,7 @@ fkv_status fkv_attention_mass(const fkv_shape *shape, const void *Q, const void 
     a.lse = (float *)lse;
     a.slab = slab;
     a.n_heads = shape->n_heads;
+    a.heads = all_heads(shape->n_heads);
     a.Lq = (int32_t)lq;
     a.scale = scale;
     a.scale_log2 = scale * 1.4426950408889634f;

@@ -110,7 +110,8 @@ struct AttnArgs {
     int64_t slab;
     int32_t n_heads, Lq;
     int32_t n_qtiles;               // ceil(Lq / BM)
-    int32_t n_items;                // n_heads * n_qtiles
+    int32_t n_items;                // heads.n * n_qtiles (work item = (list entry, query tile))
+    HeadList heads;                 // the heads this launch computes, in schedule order
     int32_t items_per_xcd;          // ceil(n_items / 8)
     int32_t n_blocks;               // balanced schedule: workgroups (multiple of 8); 0 = one per item
     float *part;                    // balanced schedule: 2 * n_blocks partial-result slots

@@ -425,8 +425,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     if (!BAL) {
         const int item = (blockIdx.x & 7) * a.items_per_xcd + (blockIdx.x >> 3);
         if (item >= a.n_items) return;
-        const int h = item / a.n_qtiles;
-        attn_segment<D>(a, Ks, Vs, h, item - h * a.n_qtiles, 0, head_tiles(a, h), 0, nullptr);
+        const int li = item / a.n_qtiles;
+        const int h = a.heads.head[li];
+        attn_segment<D>(a, Ks, Vs, h, item - li * a.n_qtiles, 0, head_tiles(a, h), 0, nullptr);
         return;
     }
     const Schedule sc = make_schedule(a);
@@ -437,14 +438,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     bool first = true;
     while (cur < end) {
         // locate the item holding tile `cur`
-        int h = 0, T = head_tiles(a, 0);
-        int64_t base = 0;
-        while (cur >= base + (int64_t)a.n_qtiles * T) {
-            base += (int64_t)a.n_qtiles * T;
-            T = head_tiles(a, ++h);
-        }
-        const int qt = (int)((cur - base) / T);
-        const int64_t ibase = base + (int64_t)qt * T;
+        const ItemPos ip = locate(a, cur);
+        const int h = a.heads.head[ip.li], qt = ip.qt, T = ip.T;
+        const int64_t ibase = ip.ibase;
         const int t0 = (int)(cur - ibase);
         const int t1 = (int)((end < ibase + T ? end : ibase + T) - ibase);
         float *slot = (t0 == 0 && t1 == T)
@@ -472,10 +468,11 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     using C = Cfg<D>;
     constexpr int kML = BM * D / 2;  // float offset of m within a slot
     const int item = blockIdx.x, w = blockIdx.y;
-    const int h = item / a.n_qtiles, qt = item - h * a.n_qtiles;
+    const int li = item / a.n_qtiles, qt = item - li * a.n_qtiles;
+    const int h = a.heads.head[li];
     const Schedule sc = make_schedule(a);
     int64_t P = 0;
-    for (int hh = 0; hh < h; ++hh) P += (int64_t)a.n_qtiles * head_tiles(a, hh);
+    for (int l = 0; l < li; ++l) P += (int64_t)a.n_qtiles * head_tiles(a, a.heads.head[l]);
     const int T = head_tiles(a, h);
     P += (int64_t)qt * T;
     const int b0 = sc.owner(P), b1 = sc.owner(P + T - 1);

@@ -25,8 +25,9 @@ __global__ __launch_bounds__(kThreads) void attn_f32_kernel(AttnArgs a) {
 
     const int item = blockIdx.x;
     if (item >= a.n_items) return;
-    const int h = item / a.n_qtiles;
-    const int qt = item - h * a.n_qtiles;
+    const int li = item / a.n_qtiles;
+    const int h = a.heads.head[li];
+    const int qt = item - li * a.n_qtiles;
     const int tid = threadIdx.x;
     const int r = tid / TPR, sub = tid % TPR;
     const int Lq = a.Lq;

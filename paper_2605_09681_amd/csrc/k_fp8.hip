@@ -631,8 +631,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fp8_kernel(AttnArgs a) {
     if (!BAL) {
         const int item = (blockIdx.x & 7) * a.items_per_xcd + (blockIdx.x >> 3);
         if (item >= a.n_items) return;
-        const int h = item / a.n_qtiles;
-        fp8_segment<D>(a, Ks, Vs, h, item - h * a.n_qtiles, 0, head_tiles(a, h), 0, nullptr);
+        const int li = item / a.n_qtiles;
+        const int h = a.heads.head[li];
+        fp8_segment<D>(a, Ks, Vs, h, item - li * a.n_qtiles, 0, head_tiles(a, h), 0, nullptr);
         return;
     }
     const Schedule sc = make_schedule(a);
@@ -642,14 +643,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fp8_kernel(AttnArgs a) {
     int64_t cur = sc.start(r);
     bool first = true;
     while (cur < end) {
-        int h = 0, T = head_tiles(a, 0);
-        int64_t base = 0;
-        while (cur >= base + (int64_t)a.n_qtiles * T) {
-            base += (int64_t)a.n_qtiles * T;
-            T = head_tiles(a, ++h);
-        }
-        const int qt = (int)((cur - base) / T);
-        const int64_t ibase = base + (int64_t)qt * T;
+        const ItemPos ip = locate(a, cur);
+        const int h = a.heads.head[ip.li], qt = ip.qt, T = ip.T;
+        const int64_t ibase = ip.ibase;
         const int t0 = (int)(cur - ibase);
         const int t1 = (int)((end < ibase + T ? end : ibase + T) - ibase);
         float *slot = (t0 == 0 && t1 == T) ? nullptr

@@ -10,11 +10,15 @@ of one layer:
 3. ``fkv_compress_static`` (static heads, Eq. 2)
 4. ``fkv_chunk_attention`` (all heads, Eq. 2 / Eq. 4)
 
-Steps 1-2 and step 3 touch disjoint heads, so :meth:`CompressedLayer.compress`
-runs the static gather on a second stream (default priority) alongside the
-dynamic heads' scoring and compaction; both are HBM-bound and neither fills
-the memory system alone.  Attention waits for both.  The individual stages
-enqueue on the current torch stream; nothing synchronises with the host.
+Steps 1-2 and step 3 touch disjoint heads.  :meth:`CompressedLayer.step`
+therefore runs, on a second stream (default priority), the static gather and
+then attention over the static heads (``fkv_chunk_attention_heads``), while
+the current stream scores and compacts the dynamic heads and then attends
+them: the HBM-bound compression of the dynamic heads runs under the
+MFMA-bound attention of the static heads.  :meth:`CompressedLayer.compress`
+alone overlaps the static gather with the dynamic compression the same way.
+The individual stages enqueue on the current torch stream; nothing
+synchronises with the host.
 """
 from __future__ import annotations
 
@@ -24,7 +28,8 @@ from typing import Optional, Sequence
 import torch
 
 from . import (FKV_DYNAMIC, FKV_STATIC, fkv_append_frames, fkv_attention_mass,
-               fkv_attention_workspace_size, fkv_chunk_attention, fkv_classify_heads,
+               fkv_attention_workspace_size, fkv_chunk_attention, fkv_chunk_attention_heads,
+               fkv_classify_heads,
                fkv_chunk_attention_fp8, fkv_compress_static, fkv_fp8_pack, fkv_fp8_sizes,
                fkv_num_segments, fkv_score_pooled, fkv_score_pooled_workspace_size,
                fkv_score_segments, fkv_score_workspace_size, fkv_select_compact,
@@ -53,7 +58,7 @@ class CompressedLayer:
         self.kv_len = torch.zeros((n_heads,), dtype=torch.int32, device=dev)
         self.ws_bytes = fkv_score_workspace_size(self.shape, self.heads)
         self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
-        self.attn_workspace = None
+        self.attn_workspace = self.attn_workspace2 = None
         if balanced:
             with torch.cuda.device(dev):
                 n = fkv_attention_workspace_size(self.shape)
@@ -62,9 +67,13 @@ class CompressedLayer:
         self.scale = 1.0 / math.sqrt(head_dim)
         self.has_static = FKV_STATIC in self.types
         self.has_dynamic = FKV_DYNAMIC in self.types
-        # side stream for the static gather (only when both head types exist)
+        # side stream for the static heads (only when both head types exist)
         self.side = (torch.cuda.Stream(device=dev) if overlap and self.has_static and self.has_dynamic
                      else None)
+        self.static_heads = [h for h, t in enumerate(self.types) if t == FKV_STATIC]
+        self.dynamic_heads = [h for h, t in enumerate(self.types) if t == FKV_DYNAMIC]
+        if self.side is not None and self.attn_workspace is not None:
+            self.attn_workspace2 = torch.empty_like(self.attn_workspace)
 
     # individual stages -------------------------------------------------------
     def score(self, K_hist, frame_slot, K_cur):
@@ -128,8 +137,24 @@ class CompressedLayer:
             self.compress_static(K_hist, V_hist, frame_slot)
 
     def step(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse=None):
-        self.compress(K_hist, V_hist, frame_slot, K_cur)
-        self.attention(Q, K_cur, V_cur, O, lse)
+        if self.side is None:
+            self.compress(K_hist, V_hist, frame_slot, K_cur)
+            self.attention(Q, K_cur, V_cur, O, lse)
+            return
+        main = torch.cuda.current_stream(self.device)
+        args = (self.Kc, self.Vc, self.kv_len, K_cur, V_cur, self.scale, O, lse)
+        self.side.wait_stream(main)
+        with torch.cuda.stream(self.side):
+            self.compress_static(K_hist, V_hist, frame_slot)
+            fkv_chunk_attention_heads(self.shape, self.static_heads, Q, *args[:7], lse=lse,
+                                      workspace=self.attn_workspace2)
+        for t in (K_hist, V_hist, Q, K_cur, V_cur, O) + ((lse,) if lse is not None else ()):
+            t.record_stream(self.side)
+        self.score(K_hist, frame_slot, K_cur)
+        self.select_compact(K_hist, V_hist, frame_slot)
+        fkv_chunk_attention_heads(self.shape, self.dynamic_heads, Q, *args[:7], lse=lse,
+                                  workspace=self.attn_workspace)
+        main.wait_stream(self.side)
 
 
 class HeadProfiler:
@@ -212,6 +237,7 @@ class RolloutStack:
         with torch.cuda.device(dev):
             n = fkv_attention_workspace_size(full)
         self.attn_ws = torch.empty(max(n, 1), dtype=torch.uint8, device=dev) if n > 0 else None
+        self.attn_ws2 = torch.empty_like(self.attn_ws) if (n > 0 and overlap) else None
         self.scale = 1.0 / math.sqrt(head_dim)
         self.side = torch.cuda.Stream(device=dev) if overlap else None
         self._shapes, self._heads = {}, {}
@@ -249,8 +275,10 @@ class RolloutStack:
 
     def run_layer(self, layer: int, budgets, frame_slot, Q, K_cur, V_cur, O, lse=None, pooled=None):
         """One AR step of one layer: compress its cache, then chunk attention
-        into O.  ``pooled`` (a row from :meth:`score_pooled`) replaces the
-        layer's own per-head scoring."""
+        into O -- the static heads (gather, then their attention) on the side
+        stream while the dynamic heads are scored, compacted and attended on
+        the current stream.  ``pooled`` (a row from :meth:`score_pooled`)
+        replaces the layer's own per-head scoring."""
         H = len(frame_slot)
         shape = self.shape(H)
         heads, key = self._budget_array(budgets)
@@ -260,11 +288,14 @@ class RolloutStack:
         has_static, has_dynamic = FKV_STATIC in types, FKV_DYNAMIC in types
         main = torch.cuda.current_stream(self.device)
         side = self.side if (self.side is not None and has_static and has_dynamic) else None
+        att = (self.Kc, self.Vc, self.kv_len, K_cur, V_cur, self.scale, O)
         if side is not None:
+            static_ids = [h for h, t in enumerate(types) if t == FKV_STATIC]
             side.wait_stream(main)
             with torch.cuda.stream(side):
                 fkv_compress_static(shape, heads, Kh, Vh, frame_slot, self.Kc, self.Vc, self.kv_len)
-            for t in (Kh, Vh):
+                fkv_chunk_attention_heads(shape, static_ids, Q, *att, lse=lse, workspace=self.attn_ws2)
+            for t in (Kh, Vh, Q, K_cur, V_cur, O) + ((lse,) if lse is not None else ()):
                 t.record_stream(side)
         elif has_static:
             fkv_compress_static(shape, heads, Kh, Vh, frame_slot, self.Kc, self.Vc, self.kv_len)
@@ -277,9 +308,11 @@ class RolloutStack:
                 fkv_select_compact(shape, heads, scores, Kh, Vh, frame_slot, kept, self.Kc, self.Vc,
                                    self.kv_len)
         if side is not None:
+            dynamic_ids = [h for h, t in enumerate(types) if t == FKV_DYNAMIC]
+            fkv_chunk_attention_heads(shape, dynamic_ids, Q, *att, lse=lse, workspace=self.attn_ws)
             main.wait_stream(side)
-        fkv_chunk_attention(shape, Q, self.Kc, self.Vc, self.kv_len, K_cur, V_cur, self.scale, O, lse,
-                            self.attn_ws)
+        else:
+            fkv_chunk_attention(shape, Q, *att, lse, self.attn_ws)
 
     def append(self, layer: int, K_new, V_new, dst_slots):
         """Write a finished chunk's frames ([n_heads][n*F][d]) into the layer's cache slots."""

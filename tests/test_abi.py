@@ -217,6 +217,26 @@ def test_attention_arg_errors(fkv):
     assert L.fkv_attention_workspace_size(ctypes.byref(f32), ctypes.byref(out)) == 0 and out.value == 0
 
 
+def test_attention_heads_arg_errors(fkv):
+    """fkv_chunk_attention_heads validates its head list before anything else;
+    an empty list enqueues nothing (returns OK without touching the device)."""
+    shape = _shape(fkv)
+    L = fkv.lib()
+
+    def call(ids, n=None, scale=0.1, null_list=False):
+        arr = (ctypes.c_int32 * max(len(ids), 1))(*ids)
+        return L.fkv_chunk_attention_heads(ctypes.byref(shape), None if null_list else arr,
+                                           len(ids) if n is None else n, FAKE, FAKE, FAKE, 10, FAKE,
+                                           FAKE, FAKE, ctypes.c_float(scale), FAKE, None, None, 0, None)
+    assert call([0], n=-1) == 1
+    assert call([0, 1, 0], n=3) == 1          # more entries than heads
+    assert call([1], null_list=True) == 1
+    assert call([2]) == 1 and call([-1]) == 1  # out of range
+    assert call([1, 1]) == 1                   # repeated
+    assert call([1], scale=0.0) == 1           # the other arguments as in fkv_chunk_attention
+    assert call([]) == 0
+
+
 def test_segment_count(fkv):
     for H, F, L in [(21, 1560, 1560), (21, 1560, 390), (21, 1560, 4680), (20, 1560, 4680), (0, 64, 64)]:
         assert fkv.fkv_num_segments(_shape(fkv, frame_tokens=F, hist_frames=H, cap_frames=max(H, 1),

@@ -162,6 +162,60 @@ def test_480p_many_segments():
     check_layer(cfg, x, rows=sample_rows(cfg.lq, 8, seed=15))
 
 
+@pytest.mark.parametrize("case", ["small", "480p"])
+def test_pipelined_step(case):
+    """CompressedLayer.step: the static heads' gather and attention on a side
+    stream while the dynamic heads are scored, compacted and attended on the
+    main stream (fkv_chunk_attention_heads twice, each with its own workspace).
+    Same parity bar as the serial path; the small case interleaves head types."""
+    if case == "small":
+        cfg = _small(F=100, L=25, d=128)
+        x = W.make_layer_inputs(cfg, seed=30, frame_slot=np.array([3, 0, 8, 1, 5, 2, 7], np.int32))
+        rows = None
+    else:
+        cfg = W.wan_layer_config("480p")
+        x = W.make_layer_inputs(cfg, seed=31)
+        rows = sample_rows(cfg.lq, 8, seed=31)
+    _print_case("pipelined-step", case=case)
+    layer = make_layer(cfg)
+    assert layer.side is not None and layer.attn_workspace2 is not None
+    d = dev_inputs(x)
+    O = torch.empty_like(d["Q"])
+    lse = torch.empty((cfg.n_heads, cfg.lq), dtype=torch.float32, device="cuda")
+    layer.step(d["K_hist"], d["V_hist"], x.frame_slot, d["Q"], d["K_cur"], d["V_cur"], O, lse)
+    torch.cuda.synchronize()
+    ref = oracle.run_layer(cfg, x, rows=rows, scale=1 / math.sqrt(cfg.head_dim))
+    assert_compression_exact(cfg, layer, ref)
+    assert_attention_close(O, ref, cfg.dtype, lse)
+
+
+@pytest.mark.parametrize("balanced", [True, False])
+def test_attention_heads_subset(balanced):
+    """fkv_chunk_attention_heads computes exactly the listed heads (in any
+    order) and leaves every other head's rows of O and lse as they were."""
+    import paper_2605_09681_amd as fkv
+    cfg = _small(F=100, L=25, d=64)
+    x = W.make_layer_inputs(cfg, seed=32, frame_slot=np.array([3, 0, 8, 1, 5, 2, 7], np.int32))
+    _print_case("attention-heads", balanced=balanced)
+    layer = make_layer(cfg, balanced=balanced)
+    d = dev_inputs(x)
+    layer.compress(d["K_hist"], d["V_hist"], x.frame_slot, d["K_cur"])
+    O = torch.full_like(d["Q"], 7.0)
+    lse = torch.full((cfg.n_heads, cfg.lq), -3.0, dtype=torch.float32, device="cuda")
+    listed = [3, 1]
+    fkv.fkv_chunk_attention_heads(layer.shape, listed, d["Q"], layer.Kc, layer.Vc, layer.kv_len, d["K_cur"],
+                                  d["V_cur"], layer.scale, O, lse, layer.attn_workspace)
+    torch.cuda.synchronize()
+    ref = oracle.run_layer(cfg, x, scale=layer.scale)
+    Of, lf = from_dev(O), from_dev(lse)
+    for h in range(cfg.n_heads):
+        if h in listed:
+            one = oracle.LayerResult(None, None, None, None, None, None, ref.rows, ref.O[h:h + 1], ref.lse[h:h + 1])
+            assert_attention_close(O[h:h + 1], one, "bf16", lse[h:h + 1])
+        else:
+            assert (W.bf16_bits_to_f32(Of[h]) == 7.0).all() and (lf[h] == -3.0).all(), h
+
+
 def test_480p_no_pruning_equals_full_attention():
     """Keep everything (dynamic f = 1, static recent = H): both head types
     reduce to full attention over the uncompressed cache."""
