@@ -51,6 +51,9 @@ def parse():
     p.add_argument("--cpu-rows", type=int, default=4680,
                    help="query rows per head in the CPU oracle sample (4680 = every row at 480P)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--step", default="pipelined", choices=["pipelined", "serial"],
+                   help="timed step: pipelined (static heads on a side stream) or the four calls "
+                        "one after another on one stream")
     p.add_argument("--no-rollout", action="store_true",
                    help="skip the measured 30-layer x 4-step x 10-chunk rollout")
     p.add_argument("--no-extras", action="store_true",
@@ -171,12 +174,20 @@ def main():
         L.attention(b["Q"], b["K_cur"], b["V_cur"], b["O"])
         ev[4].record(stream)
 
+    def serial(i):
+        L, b = layers[i % len(layers)], bufs[i % len(layers)]
+        L.score(b["K_hist"], slots, b["K_cur"])
+        L.select_compact(b["K_hist"], b["V_hist"], slots)
+        L.compress_static(b["K_hist"], b["V_hist"], slots)
+        L.attention(b["Q"], b["K_cur"], b["V_cur"], b["O"])
+
+    timed = step if args.step == "pipelined" else serial
     for i in range(args.warmup):
-        step(i)
+        timed(i)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(i)
+        timed(i)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
 
@@ -235,7 +246,9 @@ def main():
             "kv_len": kv_len.tolist(),
             "rotating_copies": args.copies,
             "attention_schedule": args.schedule,
-            "step": "static heads (gather + attention) on a side stream, dynamic heads (score + select/compact + attention) on the main stream",
+            "step": ("static heads (gather + attention) on a side stream, dynamic heads (score + select/compact "
+                     "+ attention) on the main stream" if args.step == "pipelined" else
+                     "the four calls one after another on one stream"),
         },
         "roofline": {
             "kernel": "fkv_chunk_attention: attn_bf16_kernel<128, balanced> + attn_merge_kernel<128>",
