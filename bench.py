@@ -329,6 +329,13 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
     pooled_ms = _time_ms(lambda: fkv.fkv_score_pooled(L0.shape, b["K_hist"], x.frame_slot, b["K_cur"], pooled, ws),
                          20, stream)
     pooled_bytes = cfg.n_heads * (H + 1) * F * d * 2
+    stats = torch.empty(fkv.fkv_score_stats_size(L0.shape, L0.heads) // 8, dtype=torch.float64, device="cuda")
+    hist_ms = _time_ms(lambda: fkv.fkv_score_history(L0.shape, L0.heads, b["K_hist"], x.frame_slot, stats,
+                                                     L0.workspace), 20, stream)
+    cached_ms = _time_ms(lambda: fkv.fkv_score_segments_cached(L0.shape, L0.heads, b["K_hist"], x.frame_slot,
+                                                               b["K_cur"], stats, L0.scores, L0.workspace), 20,
+                         stream)
+    n_dyn = sum(1 for t in L0.types if t == W.DYNAMIC)
 
     O8 = torch.empty_like(b["Q"])
     pack_ms = _time_ms(lambda: L0.pack_fp8(b["Q"], b["K_cur"], b["V_cur"]), 20, stream)
@@ -371,6 +378,10 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
             "attention_ms": round(fp8_ms, 4), "TFLOP_s": round(attn_flop / (fp8_ms * 1e-3) / 1e12, 1),
             "peak_TFLOP_s": 5000.0, "pack_ms": round(pack_ms, 4),
             "note": "E4M3 Q/K/V/P on gfx950 FP8 MFMA; pack = statistics + quantise + transpose"},
+        "incremental_score": {"history_ms": round(hist_ms, 4), "step_ms": round(cached_ms, 4),
+                              "step_GB_s": round(n_dyn * 2 * F * d * 2 / (cached_ms * 1e-3) / 1e9, 1),
+                              "note": "history statistics once per chunk, then per AR step the scores from "
+                                      "them plus frames H-1 and H (2 of the 22 frames per dynamic head)"},
         "pooled_proxy_score": {
             "ms": round(pooled_ms, 4), "GB_s": round(pooled_bytes / (pooled_ms * 1e-3) / 1e9, 1),
             "note": "all 12 heads pooled, once per AR step for all layers (not part of the step)"},
@@ -380,14 +391,17 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
     }
 
 
-def measure_rollout(pooled: bool, n_chunks: int = 10, n_steps: int = 4, n_layers: int = 30):
+def measure_rollout(pooled: bool, n_chunks: int = 10, n_steps: int = 4, n_layers: int = 30,
+                    incremental: bool = False):
     """The metric measured rather than extrapolated: the 30-layer stack of the
     480P layer, 4 denoising steps per chunk, 10 chunks, each layer with its own
     rolling 21-frame cache (sink pinned, 3-frame chunks written back after
     each chunk) and its own seeded head mask (6 of 12 heads dynamic).  Every
     step re-scores and compacts every layer (pooled=False), or scores once per
     step from the first layer's keys pooled over all heads and reuses that row
-    in every layer (pooled=True, the first-block proxy).  Inputs are
+    in every layer (pooled=True, the first-block proxy); incremental=True
+    computes each layer's history statistics once per chunk and then scores
+    each step from them plus the pair touching the chunk.  Inputs are
     device-generated N(0,1) tensors (values do not change the work)."""
     import numpy as np
     import torch
@@ -409,11 +423,17 @@ def measure_rollout(pooled: bool, n_chunks: int = 10, n_steps: int = 4, n_layers
     def chunk(i):
         slots = W.ring_frame_slots(i, C, window)
         H = len(slots)
+        if incremental and H > 0:
+            if pooled:
+                stack.history(0, None, slots, pooled=True)
+            else:
+                for layer in range(n_layers):
+                    stack.history(layer, budgets(layer, H), slots)
         for step in range(n_steps):
             Q, Kq, Vq = sets[step % 2]
-            row = stack.score_pooled(0, slots, Kq) if pooled and H > 0 else None
+            row = stack.score_pooled(0, slots, Kq, incremental=incremental) if pooled and H > 0 else None
             for layer in range(n_layers):
-                stack.run_layer(layer, budgets(layer, H), slots, Q, Kq, Vq, O, pooled=row)
+                stack.run_layer(layer, budgets(layer, H), slots, Q, Kq, Vq, O, pooled=row, incremental=incremental)
         dst = W.chunk_write_slots(i, C, window).tolist()
         for layer in range(n_layers):
             stack.append(layer, Kq, Vq, dst)

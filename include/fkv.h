@@ -190,6 +190,37 @@ fkv_status fkv_score_pooled(const fkv_shape *shape, const void *K_hist,
                             float *scores, void *workspace, size_t workspace_bytes,
                             void *stream);
 
+/* Incremental rescoring (the per-step cost of Sec. 4.3's scoring).  Across the
+ * AR steps of one chunk the history does not change, only K_cur does, and of
+ * all Eq. 3 terms only the pair (frame H-1, first frame of K_cur) depends on
+ * it.  fkv_score_history streams the history once and stores, per listed head,
+ * unit u (a segment, or a frame when segments span frames) and frame t < H,
+ * the fp64 sums SQ(t) = sum K_t^2 and DOT(t) = sum K_t * K_{t+1} (t < H-1) in
+ * `stats`, a caller-owned device buffer of fkv_score_stats_size bytes.
+ * fkv_score_segments_cached then streams frames H-1 and H only and writes the
+ * same scores fkv_score_segments (pooled = 0) or fkv_score_pooled (pooled = 1)
+ * would: per listed head [n_heads][n_seg] (rows of static heads untouched),
+ * or one row [n_seg].  Sums are fp64 in a fixed order and the cosine is rounded
+ * once to fp32; only the grouping of the fp64 sums differs from the full pass.
+ * pooled = 0 lists the dynamic heads of `heads`; pooled = 1 lists every head
+ * and `heads` may be NULL.  stats stays valid until the history (K_hist
+ * contents or frame_slot) changes; the caller runs fkv_score_history again
+ * then (once per chunk).  `workspace` is the scoring workspace
+ * (fkv_score_workspace_size, or fkv_score_pooled_workspace_size when pooled).
+ * Nothing is enqueued when there is no listed head or H = 0.  Errors as in
+ * fkv_score_segments; FKV_ERR_CAPACITY also for a short stats buffer. */
+fkv_status fkv_score_stats_size(const fkv_shape *shape, const fkv_head *heads, int32_t pooled,
+                                size_t *bytes);
+fkv_status fkv_score_history(const fkv_shape *shape, const fkv_head *heads, int32_t pooled,
+                             const void *K_hist, const int32_t *frame_slot, double *stats,
+                             size_t stats_bytes, void *workspace, size_t workspace_bytes,
+                             void *stream);
+fkv_status fkv_score_segments_cached(const fkv_shape *shape, const fkv_head *heads,
+                                     int32_t pooled, const void *K_hist,
+                                     const int32_t *frame_slot, const void *K_cur,
+                                     const double *stats, size_t stats_bytes, float *scores,
+                                     void *workspace, size_t workspace_bytes, void *stream);
+
 /* fkv_select_compact with one score row shared by every dynamic head: scores
  * is float [n_seg] (as fkv_score_pooled writes it) instead of
  * [n_heads][n_seg].  Everything else, outputs and errors included, is as in

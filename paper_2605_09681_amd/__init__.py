@@ -43,7 +43,8 @@ FKV_MAX_HEADS, FKV_MAX_FRAMES, FKV_MAX_SEGMENTS = 64, 256, 4096
 EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_score_workspace_size", "fkv_score_segments", "fkv_select_compact",
             "fkv_append_frames", "fkv_score_pooled_workspace_size", "fkv_score_pooled",
-            "fkv_select_compact_pooled",
+            "fkv_select_compact_pooled", "fkv_score_stats_size", "fkv_score_history",
+            "fkv_score_segments_cached",
             "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_chunk_attention_heads",
             "fkv_fp8_sizes", "fkv_fp8_pack",
             "fkv_chunk_attention_fp8", "fkv_attention_mass_workspace_size", "fkv_attention_mass",
@@ -111,6 +112,12 @@ def lib():
         L.fkv_attention_workspace_size.restype = ctypes.c_int
         L.fkv_chunk_attention.argtypes = [S, P, P, P, I32, P, P, P, F, P, P, P, SZ, P]
         L.fkv_chunk_attention.restype = ctypes.c_int
+        L.fkv_score_stats_size.argtypes = [S, Hd, I32, ctypes.POINTER(SZ)]
+        L.fkv_score_stats_size.restype = ctypes.c_int
+        L.fkv_score_history.argtypes = [S, Hd, I32, P, P, P, SZ, P, SZ, P]
+        L.fkv_score_history.restype = ctypes.c_int
+        L.fkv_score_segments_cached.argtypes = [S, Hd, I32, P, P, P, P, SZ, P, P, SZ, P]
+        L.fkv_score_segments_cached.restype = ctypes.c_int
         L.fkv_chunk_attention_heads.argtypes = [S, P, I32, P, P, P, I32, P, P, P, F, P, P, P, SZ, P]
         L.fkv_chunk_attention_heads.restype = ctypes.c_int
         L.fkv_fp8_sizes.argtypes = [S, I32] + [ctypes.POINTER(SZ)] * 4
@@ -252,6 +259,44 @@ def fkv_score_segments(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, score
     _raise(lib().fkv_score_segments(ctypes.byref(shape), heads, kh, sl, kc, sc, ws,
                                     workspace.numel(), _stream(stream)))
     return workspace
+
+
+def fkv_score_stats_size(shape: fkv_shape, heads, pooled: bool = False) -> int:
+    """Bytes of the per-frame statistics buffer of incremental rescoring."""
+    out = ctypes.c_size_t(0)
+    _raise(lib().fkv_score_stats_size(ctypes.byref(shape), heads, int(pooled), ctypes.byref(out)))
+    return int(out.value)
+
+
+def fkv_score_history(shape: fkv_shape, heads, K_hist, frame_slot, stats, workspace, pooled: bool = False,
+                      stream=None):
+    """Per-frame statistics of the history into ``stats`` (float64 device
+    tensor of fkv_score_stats_size bytes), once per chunk."""
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    kh = _check(K_hist, "K_hist", dt, hist)
+    st = _check(stats, "stats", torch.float64)
+    ws = _check(workspace, "workspace", torch.uint8)
+    _raise(lib().fkv_score_history(ctypes.byref(shape), heads, int(pooled), kh, _slots(frame_slot, shape.hist_frames),
+                                   st, stats.numel() * 8, ws, workspace.numel(), _stream(stream)))
+
+
+def fkv_score_segments_cached(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, stats, scores, workspace,
+                              pooled: bool = False, stream=None):
+    """Scores of one AR step from the history statistics plus the pair
+    (frame H-1, first frame of K_cur): the result of fkv_score_segments
+    (or fkv_score_pooled when pooled) with two frames read per head."""
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    n_seg = fkv_num_segments(shape)
+    kh = _check(K_hist, "K_hist", dt, hist)
+    kc = _check(K_cur, "K_cur", dt, (shape.n_heads, _lq(shape), shape.head_dim))
+    sc = _check(scores, "scores", torch.float32, (n_seg,) if pooled else (shape.n_heads, n_seg))
+    st = _check(stats, "stats", torch.float64)
+    ws = _check(workspace, "workspace", torch.uint8)
+    _raise(lib().fkv_score_segments_cached(ctypes.byref(shape), heads, int(pooled), kh,
+                                           _slots(frame_slot, shape.hist_frames), kc, st, stats.numel() * 8, sc,
+                                           ws, workspace.numel(), _stream(stream)))
 
 
 def fkv_append_frames(shape: fkv_shape, K_new, V_new, dst_slot, K_hist, V_hist, stream=None):

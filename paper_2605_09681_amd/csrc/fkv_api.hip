@@ -292,13 +292,16 @@ fkv_status fkv_score_workspace_size(const fkv_shape *shape, const fkv_head *head
 namespace {
 
 // Scoring of the heads in `list` (per head, or pooled into one row).
+enum ScoreMode { kScoreFull, kScoreHistory, kScoreCached };
+
 fkv_status score_impl(const fkv_shape *shape, const fkv::HeadList &list, bool pooled, const void *K_hist,
                       const int32_t *frame_slot, const void *K_cur, float *scores, void *workspace,
-                      void *stream, const char *what) {
+                      void *stream, const char *what, ScoreMode mode = kScoreFull, double *stats = nullptr) {
     fkv::ScoreArgs a;
     memset(&a, 0, sizeof a);
     a.heads = list;
     a.pooled = pooled ? 1 : 0;
+    a.stats = stats;
     const size_t es = elem_size(shape);
     a.K_hist = (const uint8_t *)K_hist;
     a.K_cur = (const uint8_t *)K_cur;
@@ -316,7 +319,51 @@ fkv_status score_impl(const fkv_shape *shape, const fkv::HeadList &list, bool po
     score_geometry(shape, &a.unit_tokens, &a.units_per_frame, &a.unit_vecs, &a.chunks_per_unit);
     for (int t = 0; t < shape->hist_frames; ++t) a.slots.slot[t] = frame_slot[t];
     (void)hipGetLastError();
-    return device_status(fkv::launch_score(a, shape->dtype == FKV_F32, (hipStream_t)stream), what);
+    const bool f32 = shape->dtype == FKV_F32;
+    const hipStream_t st = (hipStream_t)stream;
+    hipError_t e = mode == kScoreHistory ? fkv::launch_score_history(a, f32, st)
+                 : mode == kScoreCached  ? fkv::launch_score_cached(a, f32, st)
+                                         : fkv::launch_score(a, f32, st);
+    return device_status(e, what);
+}
+
+// Heads of an incremental-rescoring call: every dynamic head, or every head
+// when the score is pooled (heads may then be NULL).
+fkv_status stats_heads(const fkv_shape *shape, const fkv_head *heads, int32_t pooled, fkv::HeadList *list) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if (pooled != 0 && pooled != 1) return fail(FKV_ERR_ARG, "pooled %d is neither 0 nor 1", pooled);
+    if (!pooled && (st = check_heads(shape, heads)) != FKV_OK) return st;
+    memset(list, 0, sizeof *list);
+    for (int h = 0; h < shape->n_heads; ++h)
+        if (pooled || heads[h].type == FKV_DYNAMIC) list->head[list->n++] = h;
+    return FKV_OK;
+}
+
+size_t stats_bytes(const fkv_shape *shape, int n_list) {
+    int U, units, chunks;
+    int64_t uv;
+    score_geometry(shape, &U, &units, &uv, &chunks);
+    return (size_t)n_list * shape->hist_frames * units * 2 * sizeof(double);
+}
+
+// Shared checks of the two incremental calls; need = 0 means there is nothing
+// to do (no listed head, or no history yet).
+fkv_status stats_call_checks(const fkv_shape *shape, const fkv::HeadList &list, const int32_t *frame_slot,
+                             const void *K_hist, const double *stats, size_t stats_size, void *workspace,
+                             size_t workspace_bytes, size_t *need) {
+    fkv_status st;
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+    *need = score_bytes(shape, list.n);
+    if (*need == 0) return FKV_OK;
+    if (!K_hist) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (!stats) return fail(FKV_ERR_ARG, "stats is NULL");
+    const size_t sb = stats_bytes(shape, list.n);
+    if (stats_size < sb) return fail(FKV_ERR_CAPACITY, "stats of %zu bytes, %zu needed", stats_size, sb);
+    if (!workspace) return fail(FKV_ERR_ARG, "workspace is NULL");
+    if (workspace_bytes < *need)
+        return fail(FKV_ERR_CAPACITY, "workspace of %zu bytes, %zu needed", workspace_bytes, *need);
+    return FKV_OK;
 }
 
 
@@ -344,6 +391,47 @@ fkv_status fkv_score_segments(const fkv_shape *shape, const fkv_head *heads, con
         if (heads[h].type == FKV_DYNAMIC) list.head[list.n++] = h;
     return score_impl(shape, list, false, K_hist, frame_slot, K_cur, scores, workspace, stream,
                       "fkv_score_segments launch");
+}
+
+fkv_status fkv_score_stats_size(const fkv_shape *shape, const fkv_head *heads, int32_t pooled, size_t *bytes) {
+    fkv::HeadList list;
+    fkv_status st;
+    if ((st = stats_heads(shape, heads, pooled, &list)) != FKV_OK) return st;
+    if (!bytes) return fail(FKV_ERR_ARG, "bytes is NULL");
+    *bytes = stats_bytes(shape, list.n);
+    return ok();
+}
+
+fkv_status fkv_score_history(const fkv_shape *shape, const fkv_head *heads, int32_t pooled, const void *K_hist,
+                             const int32_t *frame_slot, double *stats, size_t stats_size, void *workspace,
+                             size_t workspace_bytes, void *stream) {
+    fkv::HeadList list;
+    fkv_status st;
+    if ((st = stats_heads(shape, heads, pooled, &list)) != FKV_OK) return st;
+    size_t need = 0;
+    if ((st = stats_call_checks(shape, list, frame_slot, K_hist, stats, stats_size, workspace, workspace_bytes,
+                                &need)) != FKV_OK)
+        return st;
+    if (need == 0) return ok();
+    return score_impl(shape, list, pooled, K_hist, frame_slot, K_hist, nullptr, workspace, stream,
+                      "fkv_score_history launch", kScoreHistory, stats);
+}
+
+fkv_status fkv_score_segments_cached(const fkv_shape *shape, const fkv_head *heads, int32_t pooled,
+                                     const void *K_hist, const int32_t *frame_slot, const void *K_cur,
+                                     const double *stats, size_t stats_size, float *scores, void *workspace,
+                                     size_t workspace_bytes, void *stream) {
+    fkv::HeadList list;
+    fkv_status st;
+    if ((st = stats_heads(shape, heads, pooled, &list)) != FKV_OK) return st;
+    size_t need = 0;
+    if ((st = stats_call_checks(shape, list, frame_slot, K_hist, stats, stats_size, workspace, workspace_bytes,
+                                &need)) != FKV_OK)
+        return st;
+    if (need == 0) return ok();
+    if (!K_cur || !scores) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    return score_impl(shape, list, pooled, K_hist, frame_slot, K_cur, scores, workspace, stream,
+                      "fkv_score_segments_cached launch", kScoreCached, const_cast<double *>(stats));
 }
 
 fkv_status fkv_score_pooled_workspace_size(const fkv_shape *shape, size_t *bytes) {

@@ -97,6 +97,9 @@ struct ScoreArgs {
     int32_t chunks_per_unit;        // ceil(unit_vecs / 256)
     int32_t esize;
     int32_t pooled;                 // 1: one score per segment over all listed heads, scores[n_seg]
+    int32_t t_begin, t_end;         // frames the partials pass streams (inclusive; frame H = K_cur's first)
+    int32_t cached;                 // finalize: 1 = frames < H from `stats`, the last pair from partials
+    double *stats;                  // per-frame sums [list n][H][units][2]: SQ(t), DOT(t, t+1)
     HeadList heads;
     SlotTable slots;
 };
@@ -151,6 +154,9 @@ hipError_t launch_append(const AppendArgs &a, int n_heads, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, hipStream_t s);
 hipError_t launch_select_copy(const SelectCopyArgs &a, int max_pieces, hipStream_t s);
 hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s);
+// incremental rescoring: per-frame statistics of the history, then per-step scores
+hipError_t launch_score_history(const ScoreArgs &a, bool f32, hipStream_t s);
+hipError_t launch_score_cached(const ScoreArgs &a, bool f32, hipStream_t s);
 hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s);
 size_t attention_part_bytes(int head_dim);  // bytes of one partial-result slot (bf16 kernel)
 

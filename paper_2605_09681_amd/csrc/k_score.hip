@@ -26,6 +26,13 @@
 // The first-block proxy of Sec. 4.3 (scores pooled over heads) runs the same
 // two passes over every head and sums the partials of all heads of a segment
 // before the cosine.
+//
+// Incremental rescoring.  During the AR steps of one chunk the history does not
+// change; only K_cur does, and with it only SQ[H] and DOT[H-1].  The history
+// pass streams frames 0..H-1 once and reduces each frame's partials into a
+// per-frame statistics buffer (SQ(t), and DOT(t) for t < H-1); each step then
+// streams frames H-1..H only (2 frames per head instead of H+1) and the
+// finalize takes every other term from the statistics.
 #include "fkv_internal.h"
 
 namespace fkv {
@@ -92,6 +99,12 @@ __device__ __forceinline__ int64_t ws_index(const ScoreArgs &a, int li, int t, i
     return ((((int64_t)li * (a.H + 1) + t) * a.units_per_frame + u) * a.chunks_per_unit + c) * kWaves + w;
 }
 
+// Statistics layout: stats[((li*H + t)*units + u)][2], [0] = SQ(t), [1] = DOT(t, t+1)
+// (DOT(H-1) is not part of the history and never stored).
+__device__ __forceinline__ int64_t stats_index(const ScoreArgs &a, int li, int t, int u) {
+    return ((int64_t)li * a.H + t) * a.units_per_frame + u;
+}
+
 template <bool F32>
 __global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
     using V = Vec<F32>;
@@ -105,10 +118,11 @@ __global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
     const u32x4 *hist = (const u32x4 *)a.K_hist + (int64_t)h * a.cap * frame_vecs;
     const u32x4 *cur = (const u32x4 *)a.K_cur + (int64_t)h * a.cur_vecs;
     const int H = a.H;
+    const int tb = a.t_begin, te = a.t_end;  // streamed frames (0..H for a full pass)
 
     auto load = [&](int t) -> u32x4 {
         u32x4 r = u32x4{0, 0, 0, 0};
-        if (active && t <= H) {
+        if (active && t <= te) {
             const u32x4 *base = t < H ? hist + (int64_t)a.slots.slot[t] * frame_vecs : cur;
             r = __builtin_nontemporal_load(base + off);
         }
@@ -117,17 +131,17 @@ __global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
 
     u32x4 ring[kDepth];
 #pragma unroll
-    for (int i = 0; i < kDepth; ++i) ring[i] = load(i);
+    for (int i = 0; i < kDepth; ++i) ring[i] = load(tb + i);
 
     double prev[V::N];
 #pragma unroll
     for (int i = 0; i < V::N; ++i) prev[i] = 0.0;
 
-    for (int t0 = 0; t0 <= H; t0 += kDepth) {
+    for (int t0 = tb; t0 <= te; t0 += kDepth) {
 #pragma unroll
         for (int i = 0; i < kDepth; ++i) {
             const int t = t0 + i;
-            if (t > H) break;
+            if (t > te) break;
             double x[V::N];
             V::widen(ring[i], x);
             ring[i] = load(t + kDepth);
@@ -142,7 +156,7 @@ __global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
             dot = wave_sum(dot);
             if (lane == 63) {
                 a.ws[ws_index(a, li, t, u, c, w) * 2 + 0] = sq;
-                if (t > 0) a.ws[ws_index(a, li, t - 1, u, c, w) * 2 + 1] = dot;
+                if (t > tb) a.ws[ws_index(a, li, t - 1, u, c, w) * 2 + 1] = dot;
             }
         }
     }
@@ -170,17 +184,39 @@ __global__ __launch_bounds__(kThreads) void score_finalize_kernel(ScoreArgs a) {
     }
     const int li0 = a.pooled ? 0 : blockIdx.y;
     const int nli = a.pooled ? a.heads.n : 1;
-    const int per_head = (t1 - t0) * nparts;
-    const int n = nli * per_head;
     double dot = 0.0, na = 0.0, nb = 0.0;
-    for (int i = tid; i < n; i += kThreads) {
-        const int li = li0 + i / per_head, j = i % per_head;
-        const int t = t0 + j / nparts, k = j % nparts;
-        const double *pa = a.ws + ws_index(a, li, t, u, 0, 0) * 2;
-        const double *pb = a.ws + ws_index(a, li, t + 1, u, 0, 0) * 2;
-        na += pa[2 * k];
-        dot += pa[2 * k + 1];
-        nb += pb[2 * k];
+    if (!a.cached) {
+        const int per_head = (t1 - t0) * nparts;
+        const int n = nli * per_head;
+        for (int i = tid; i < n; i += kThreads) {
+            const int li = li0 + i / per_head, j = i % per_head;
+            const int t = t0 + j / nparts, k = j % nparts;
+            const double *pa = a.ws + ws_index(a, li, t, u, 0, 0) * 2;
+            const double *pb = a.ws + ws_index(a, li, t + 1, u, 0, 0) * 2;
+            na += pa[2 * k];
+            dot += pa[2 * k + 1];
+            nb += pb[2 * k];
+        }
+    } else {
+        // every term from the statistics, except the pair (H-1, H): DOT(H-1)
+        // and SQ(H) come from this step's partials
+        const int per_head = t1 - t0;
+        for (int i = tid; i < nli * per_head; i += kThreads) {
+            const int li = li0 + i / per_head, t = t0 + i % per_head;
+            const double *st = a.stats + stats_index(a, li, t, u) * 2;
+            na += st[0];
+            if (t + 1 < a.H) {
+                dot += st[1];
+                nb += st[2 * a.units_per_frame];  // SQ(t + 1)
+            }
+        }
+        if (t1 == a.H) {
+            for (int i = tid; i < nli * nparts; i += kThreads) {
+                const int li = li0 + i / nparts, k = i % nparts;
+                dot += a.ws[ws_index(a, li, a.H - 1, u, 0, 0) * 2 + 2 * k + 1];
+                nb += a.ws[ws_index(a, li, a.H, u, 0, 0) * 2 + 2 * k];
+            }
+        }
     }
     red[0][tid] = dot;
     red[1][tid] = na;
@@ -202,22 +238,80 @@ __global__ __launch_bounds__(kThreads) void score_finalize_kernel(ScoreArgs a) {
     }
 }
 
+// History statistics: one wave per (unit u, frame t < H, listed head li) sums
+// the frame's partials in a fixed order (lanes stride over the parts, then the
+// DPP tree) into SQ(t) and, for t < H-1, DOT(t).
+__global__ __launch_bounds__(64) void score_stats_kernel(ScoreArgs a) {
+    const int u = blockIdx.x, t = blockIdx.y, li = blockIdx.z;
+    const int lane = threadIdx.x;
+    const int nparts = a.chunks_per_unit * kWaves;
+    const double *p = a.ws + ws_index(a, li, t, u, 0, 0) * 2;
+    const bool has_dot = t + 1 < a.H;
+    double sq = 0.0, dot = 0.0;
+    for (int k = lane; k < nparts; k += 64) {
+        sq += p[2 * k];
+        if (has_dot) dot += p[2 * k + 1];
+    }
+    sq = wave_sum(sq);
+    dot = wave_sum(dot);
+    if (lane == 63) {
+        double *st = a.stats + stats_index(a, li, t, u) * 2;
+        st[0] = sq;
+        if (has_dot) st[1] = dot;
+    }
+}
+
 }  // namespace
 
 size_t score_workspace_doubles(int n_dyn, int H, int units_per_frame, int chunks_per_unit) {
     return (size_t)n_dyn * (H + 1) * units_per_frame * chunks_per_unit * kWaves * 2;
 }
 
-hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s) {
-    if (a.heads.n == 0 || a.H == 0) return hipSuccess;
+namespace {
+
+hipError_t launch_partials(const ScoreArgs &a, bool f32, hipStream_t s) {
     dim3 grid((unsigned)a.chunks_per_unit, (unsigned)a.units_per_frame, (unsigned)a.heads.n);
     if (f32)
         hipLaunchKernelGGL(score_partials_kernel<true>, grid, dim3(kThreads), 0, s, a);
     else
         hipLaunchKernelGGL(score_partials_kernel<false>, grid, dim3(kThreads), 0, s, a);
-    hipError_t e = hipGetLastError();
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_score_history(const ScoreArgs &a, bool f32, hipStream_t s) {
+    if (a.heads.n == 0 || a.H == 0) return hipSuccess;
+    ScoreArgs h = a;
+    h.t_begin = 0;
+    h.t_end = a.H - 1;
+    hipError_t e = launch_partials(h, f32, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(score_finalize_kernel, dim3(a.n_seg, a.pooled ? 1 : a.heads.n), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(score_stats_kernel, dim3(a.units_per_frame, a.H, a.heads.n), dim3(64), 0, s, h);
+    return hipGetLastError();
+}
+
+hipError_t launch_score_cached(const ScoreArgs &a, bool f32, hipStream_t s) {
+    if (a.heads.n == 0 || a.H == 0) return hipSuccess;
+    ScoreArgs c = a;
+    c.t_begin = a.H - 1;
+    c.t_end = a.H;
+    c.cached = 1;
+    hipError_t e = launch_partials(c, f32, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(score_finalize_kernel, dim3(a.n_seg, a.pooled ? 1 : a.heads.n), dim3(kThreads), 0, s, c);
+    return hipGetLastError();
+}
+
+hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s) {
+    if (a.heads.n == 0 || a.H == 0) return hipSuccess;
+    ScoreArgs f = a;  // the full pass: frames 0..H, finalize from the partials
+    f.t_begin = 0;
+    f.t_end = a.H;
+    f.cached = 0;
+    hipError_t e = launch_partials(f, f32, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(score_finalize_kernel, dim3(a.n_seg, a.pooled ? 1 : a.heads.n), dim3(kThreads), 0, s, f);
     return hipGetLastError();
 }
 

@@ -32,7 +32,8 @@ from . import (FKV_DYNAMIC, FKV_STATIC, fkv_append_frames, fkv_attention_mass,
                fkv_classify_heads,
                fkv_chunk_attention_fp8, fkv_compress_static, fkv_fp8_pack, fkv_fp8_sizes,
                fkv_num_segments, fkv_score_pooled, fkv_score_pooled_workspace_size,
-               fkv_score_segments, fkv_score_workspace_size, fkv_select_compact,
+               fkv_score_history, fkv_score_segments, fkv_score_segments_cached,
+               fkv_score_stats_size, fkv_score_workspace_size, fkv_select_compact,
                fkv_select_compact_pooled, make_heads, make_shape, slab_tokens)
 
 
@@ -207,7 +208,13 @@ class RolloutStack:
     :meth:`score_pooled` -- the first-block proxy of Sec. 4.3: one similarity
     row computed from one layer's keys pooled over all heads and reused by the
     dynamic heads of every layer.  ``budgets`` are per-head objects with
-    type/sink_frames/recent_frames/keep_k/scope for the given H."""
+    type/sink_frames/recent_frames/keep_k/scope for the given H.
+
+    Incremental rescoring: :meth:`history` stores a layer's per-frame
+    similarity statistics once per chunk (the history is fixed during the
+    chunk's AR steps); ``incremental=True`` in :meth:`run_layer` /
+    :meth:`score_pooled` then reads only the last history frame and the chunk's
+    first frame per head."""
 
     def __init__(self, n_layers: int, n_heads: int, head_dim: int, frame_tokens: int, window: int,
                  chunk_frames: int, seg_tokens: int, dtype: str = "bf16", device="cuda",
@@ -241,6 +248,10 @@ class RolloutStack:
         self.scale = 1.0 / math.sqrt(head_dim)
         self.side = torch.cuda.Stream(device=dev) if overlap else None
         self._shapes, self._heads = {}, {}
+        # per-layer statistics of incremental rescoring (listed heads x window x units x 2)
+        units = frame_tokens // min(seg_tokens, frame_tokens)
+        self._stats_len = n_heads * window * units * 2
+        self._stats, self._pooled_stats = {}, {}
 
     def _shape(self, H: int):
         return make_shape(self.n_heads, self.d, self.F, H, self.window, self.C, self.L, self.dtype_name)
@@ -263,17 +274,40 @@ class RolloutStack:
         k = self.n_heads * n_seg
         return self._scores[:k].view(self.n_heads, n_seg), self._kept[:k].view(self.n_heads, n_seg)
 
-    def score_pooled(self, layer: int, frame_slot, K_cur):
-        """The first-block proxy: one score row pooled over all heads of ``layer``."""
+    def _stats_buf(self, table, layer):
+        if layer not in table:
+            table[layer] = torch.empty(self._stats_len, dtype=torch.float64, device=self.device)
+        return table[layer]
+
+    def history(self, layer: int, budgets, frame_slot, pooled: bool = False):
+        """Per-frame statistics of the layer's history (its dynamic heads, or
+        every head for the pooled proxy); valid until the history changes."""
+        H = len(frame_slot)
+        if H == 0:
+            return
+        shape = self.shape(H)
+        heads = None if pooled else self._budget_array(budgets)[0]
+        stats = self._stats_buf(self._pooled_stats if pooled else self._stats, layer)
+        fkv_score_history(shape, heads, self.K_hist[layer], frame_slot, stats,
+                          self.pooled_ws if pooled else self.score_ws, pooled=pooled)
+
+    def score_pooled(self, layer: int, frame_slot, K_cur, incremental: bool = False):
+        """The first-block proxy: one score row pooled over all heads of ``layer``
+        (from the statistics of :meth:`history` when ``incremental``)."""
         H = len(frame_slot)
         if H == 0:
             return self.pooled_row[:0]
         shape = self.shape(H)
         row = self.pooled_row[:fkv_num_segments(shape)]
-        fkv_score_pooled(shape, self.K_hist[layer], frame_slot, K_cur, row, self.pooled_ws)
+        if incremental:
+            fkv_score_segments_cached(shape, None, self.K_hist[layer], frame_slot, K_cur,
+                                      self._pooled_stats[layer], row, self.pooled_ws, pooled=True)
+        else:
+            fkv_score_pooled(shape, self.K_hist[layer], frame_slot, K_cur, row, self.pooled_ws)
         return row
 
-    def run_layer(self, layer: int, budgets, frame_slot, Q, K_cur, V_cur, O, lse=None, pooled=None):
+    def run_layer(self, layer: int, budgets, frame_slot, Q, K_cur, V_cur, O, lse=None, pooled=None,
+                  incremental: bool = False):
         """One AR step of one layer: compress its cache, then chunk attention
         into O -- the static heads (gather, then their attention) on the side
         stream while the dynamic heads are scored, compacted and attended on
@@ -304,7 +338,11 @@ class RolloutStack:
                 fkv_select_compact_pooled(shape, heads, pooled, Kh, Vh, frame_slot, kept, self.Kc, self.Vc,
                                           self.kv_len)
             else:
-                fkv_score_segments(shape, heads, Kh, frame_slot, K_cur, scores, self.score_ws)
+                if incremental and H > 0:
+                    fkv_score_segments_cached(shape, heads, Kh, frame_slot, K_cur, self._stats[layer], scores,
+                                              self.score_ws)
+                else:
+                    fkv_score_segments(shape, heads, Kh, frame_slot, K_cur, scores, self.score_ws)
                 fkv_select_compact(shape, heads, scores, Kh, Vh, frame_slot, kept, self.Kc, self.Vc,
                                    self.kv_len)
         if side is not None:

@@ -237,6 +237,40 @@ def test_attention_heads_arg_errors(fkv):
     assert call([]) == 0
 
 
+def test_incremental_rescoring_args(fkv):
+    """Stats size = listed heads x H x units x 2 doubles; errors before any
+    device work; nothing to do (OK) when there is no history."""
+    L = fkv.lib()
+    heads = _heads(fkv)                                   # one static, one dynamic head
+    out = ctypes.c_size_t(0)
+    for kw, per_head, units in ((dict(), 1, 1), (dict(seg_tokens=16), 1, 4), (dict(seg_tokens=128, hist_frames=4), 1, 1)):
+        shape = _shape(fkv, **kw)
+        assert L.fkv_score_stats_size(ctypes.byref(shape), heads, 0, ctypes.byref(out)) == 0
+        assert out.value == per_head * shape.hist_frames * units * 16
+        assert L.fkv_score_stats_size(ctypes.byref(shape), None, 1, ctypes.byref(out)) == 0
+        assert out.value == 2 * shape.hist_frames * units * 16
+    shape = _shape(fkv)
+    assert L.fkv_score_stats_size(ctypes.byref(shape), heads, 2, ctypes.byref(out)) == 1
+    assert L.fkv_score_stats_size(ctypes.byref(shape), None, 0, ctypes.byref(out)) == 1
+    sl = (ctypes.c_int32 * 4)(0, 1, 2, 3)
+    need = ctypes.c_size_t(0)
+    assert L.fkv_score_workspace_size(ctypes.byref(shape), heads, ctypes.byref(need)) == 0
+    st = 4 * 16
+    assert L.fkv_score_history(ctypes.byref(shape), heads, 0, FAKE, sl, None, st, FAKE, need.value, None) == 1
+    assert L.fkv_score_history(ctypes.byref(shape), heads, 0, FAKE, sl, FAKE, st - 8, FAKE, need.value, None) == 3
+    assert L.fkv_score_history(ctypes.byref(shape), heads, 0, FAKE, sl, FAKE, st, FAKE, need.value - 8, None) == 3
+    assert L.fkv_score_history(ctypes.byref(shape), heads, 0, FAKE, sl, FAKE, st, None, need.value, None) == 1
+    assert L.fkv_score_segments_cached(ctypes.byref(shape), heads, 0, FAKE, sl, None, FAKE, st, FAKE, FAKE,
+                                       need.value, None) == 1
+    bad = (ctypes.c_int32 * 4)(0, 1, 9, 3)          # slot outside [0, cap_frames)
+    assert L.fkv_score_segments_cached(ctypes.byref(shape), heads, 0, FAKE, bad, FAKE, FAKE, st, FAKE, FAKE,
+                                       need.value, None) == 1
+    empty = _shape(fkv, hist_frames=0)
+    assert L.fkv_score_history(ctypes.byref(empty), heads, 0, None, None, None, 0, None, 0, None) == 0
+    assert L.fkv_score_segments_cached(ctypes.byref(empty), heads, 1, None, None, None, None, 0, None, None, 0,
+                                       None) == 0
+
+
 def test_segment_count(fkv):
     for H, F, L in [(21, 1560, 1560), (21, 1560, 390), (21, 1560, 4680), (20, 1560, 4680), (0, 64, 64)]:
         assert fkv.fkv_num_segments(_shape(fkv, frame_tokens=F, hist_frames=H, cap_frames=max(H, 1),

@@ -216,6 +216,51 @@ def test_attention_heads_subset(balanced):
             assert (W.bf16_bits_to_f32(Of[h]) == 7.0).all() and (lf[h] == -3.0).all(), h
 
 
+@pytest.mark.parametrize("dtype,F,L,pooled", [("bf16", 100, 25, False), ("bf16", 100, 100, False),
+                                               ("bf16", 100, 300, False), ("f32", 100, 50, False),
+                                               ("bf16", 100, 25, True), ("bf16", 100, 200, True),
+                                               ("f32", 100, 100, True)])
+def test_incremental_rescoring(dtype, F, L, pooled):
+    """fkv_score_history once, then fkv_score_segments_cached for three
+    different chunks K_cur: every score bit-exact with the oracle's full
+    scoring of that step (per dynamic head, or pooled over all heads), for
+    segments shorter than, equal to and longer than a frame."""
+    import paper_2605_09681_amd as fkv
+    cfg = _small(F=F, L=L, d=64, dtype=dtype)
+    if L >= F:
+        cfg = cfg.replace(heads=tuple(W.HeadBudget(b.type, b.sink_frames, b.recent_frames, b.keep_k, W.SCOPE_GLOBAL)
+                                      for b in cfg.heads))
+    slot = np.array([3, 0, 8, 1, 5, 2, 7], np.int32)
+    x = W.make_layer_inputs(cfg, seed=40 + L, frame_slot=slot)
+    _print_case("incremental", dtype=dtype, F=F, L=L, pooled=pooled)
+    shape = fkv.make_shape(cfg.n_heads, cfg.head_dim, F, cfg.hist_frames, cfg.cap_frames, cfg.chunk_frames, L, dtype)
+    heads = fkv.make_heads(cfg.heads)
+    ws_bytes = fkv.fkv_score_pooled_workspace_size(shape) if pooled else fkv.fkv_score_workspace_size(shape, heads)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    stats = torch.empty(fkv.fkv_score_stats_size(shape, heads, pooled) // 8, dtype=torch.float64, device="cuda")
+    Kh = to_dev(x.K_hist, dtype)
+    fkv.fkv_score_history(shape, heads, Kh, slot, stats, ws, pooled=pooled)
+    n_seg = fkv.fkv_num_segments(shape)
+    dyn = [h for h, b in enumerate(cfg.heads) if b.type == W.DYNAMIC]
+    for step in range(3):
+        Kq = W.normal_tensor(41, step, (cfg.n_heads, cfg.lq, cfg.head_dim), dtype) if step else x.K_cur
+        scores = torch.full((n_seg,) if pooled else (cfg.n_heads, n_seg), 9.0, dtype=torch.float32, device="cuda")
+        fkv.fkv_score_segments_cached(shape, heads, Kh, slot, to_dev(Kq, dtype), stats, scores, ws, pooled=pooled)
+        torch.cuda.synchronize()
+        got = from_dev(scores)
+        if pooled:
+            want, _ = oracle.score_pooled(x.K_hist, slot, Kq, cfg.hist_frames, L)
+            np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32), err_msg=f"step {step}")
+        else:
+            for h in range(cfg.n_heads):
+                if h in dyn:
+                    want, _ = oracle.score_head(x.K_hist[h], slot, Kq[h], cfg.hist_frames, L)
+                    np.testing.assert_array_equal(got[h].view(np.uint32), want.view(np.uint32),
+                                                  err_msg=f"step {step} head {h}")
+                else:
+                    assert (got[h] == 9.0).all(), h
+
+
 def test_480p_no_pruning_equals_full_attention():
     """Keep everything (dynamic f = 1, static recent = H): both head types
     reduce to full attention over the uncompressed cache."""
@@ -567,14 +612,17 @@ def _stack_budgets(mask_row, H, F, L):
                  W.HeadBudget(W.STATIC, 1, 2) for m in mask_row)
 
 
-@pytest.mark.parametrize("pooled", [False, True])
-def test_rollout_stack(pooled):
+@pytest.mark.parametrize("pooled,incremental", [(False, False), (True, False), (False, True), (True, True)])
+def test_rollout_stack(pooled, incremental):
     """RolloutStack: 3 layers with their own head masks and rolling caches
     (window 7, sink pinned, 2-frame chunks) over 6 chunks of 2 AR steps, across
     the ring wrap, sharing one set of compressed buffers.  Every layer's step is
     checked against the oracle (compression bit-exact, attention on every row);
     with pooled=True the dynamic heads of every layer select with the score row
-    pooled over all heads of layer 0 (the first-block proxy)."""
+    pooled over all heads of layer 0 (the first-block proxy); with
+    incremental=True the scores come from per-chunk history statistics plus
+    the pair touching the chunk (fkv_score_history once per chunk,
+    fkv_score_segments_cached every step)."""
     import paper_2605_09681_amd as fkv
     from paper_2605_09681_amd.layer import RolloutStack
     from types import SimpleNamespace
@@ -587,6 +635,12 @@ def test_rollout_stack(pooled):
     for i in range(n_chunks):
         slots = W.ring_frame_slots(i, C, window)
         H = len(slots)
+        if incremental:
+            if pooled:
+                stack.history(0, None, slots, pooled=True)
+            else:
+                for layer in range(n_layers):
+                    stack.history(layer, _stack_budgets(masks[layer], H, F, L), slots)
         for step in range(n_steps):
             ex = (i, step)
             Kq = W.normal_tensor(22, 1, (nh, C * F, d), "bf16", extra=ex)
@@ -595,17 +649,17 @@ def test_rollout_stack(pooled):
             Kq_d, Vq_d, Q_d = to_dev(Kq, "bf16"), to_dev(Vq, "bf16"), to_dev(Q, "bf16")
             row = None
             if pooled and H > 0:
-                row_d = stack.score_pooled(0, slots, Kq_d)
+                row_d = stack.score_pooled(0, slots, Kq_d, incremental=incremental)
                 row_want, _ = oracle.score_pooled(K_o[0], slots, Kq, H, L)
                 torch.cuda.synchronize()
                 np.testing.assert_array_equal(from_dev(row_d).view(np.uint32), row_want.view(np.uint32))
                 row = row_d
             for layer in range(n_layers):
-                _print_case("rollout-stack", pooled=pooled, chunk=i, step=step, layer=layer)
+                _print_case("rollout-stack", pooled=pooled, incremental=incremental, chunk=i, step=step, layer=layer)
                 heads = _stack_budgets(masks[layer], H, F, L)
                 O = torch.empty_like(Q_d)
                 lse = torch.empty((nh, C * F), dtype=torch.float32, device="cuda")
-                stack.run_layer(layer, heads, slots, Q_d, Kq_d, Vq_d, O, lse, pooled=row)
+                stack.run_layer(layer, heads, slots, Q_d, Kq_d, Vq_d, O, lse, pooled=row, incremental=incremental)
                 torch.cuda.synchronize()
                 cfg = W.LayerConfig("stack", nh, d, F, H, window, C, L, "bf16", heads)
                 x = W.LayerInputs(cfg, K_o[layer], V_o[layer], Kq, Vq, Q, slots)
