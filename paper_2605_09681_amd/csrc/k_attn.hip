@@ -373,9 +373,8 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
             if (it + 3 < n) load_k(tile0(it + 3), stage);
         }
         __syncthreads();
-        __builtin_amdgcn_s_setprio(1);
+        // (no wave-priority raise around the block: measured 1% slower with it)
         mfma_block<D, true, true>(Vs[it & 1], Ks[(it + 1) & 1], vbase, kbase, pb, qf, o, s);
-        __builtin_amdgcn_s_setprio(0);
         __syncthreads();
     }
     if (grp == 0) __syncthreads();
