@@ -98,6 +98,8 @@ struct ScoreArgs {
     int32_t esize;
     int32_t pooled;                 // 1: one score per segment over all listed heads, scores[n_seg]
     int32_t t_begin, t_end;         // frames the partials pass streams (inclusive; frame H = K_cur's first)
+    int32_t n_parts;                // the streamed range split into parts of part_frames frames (the
+    int32_t part_frames;            // last part to t_end), one workgroup column per part
     int32_t cached;                 // finalize: 1 = frames < H from `stats`, the last pair from partials
     double *stats;                  // per-frame sums [list n][H][units][2]: SQ(t), DOT(t, t+1)
     HeadList heads;

@@ -41,6 +41,15 @@ namespace {
 constexpr int kThreads = kScoreThreads;
 constexpr int kWaves = kScoreWaves;
 constexpr int kDepth = 8;  // frames in flight per thread
+// Frames per part when a long range is split over several workgroup columns:
+// more waves in flight per CU hide the fp64 products and reductions behind the
+// loads.  At 480P (22 frames) 6-frame parts (4 columns, 3 frames read twice)
+// took the partials pass from 19.0 to 16.7 us; 11- and 8-frame parts gave 17.6
+// and 17.8 us.
+#ifndef FKV_SCORE_PART_FRAMES
+#define FKV_SCORE_PART_FRAMES 6
+#endif
+constexpr int kScorePartFrames = FKV_SCORE_PART_FRAMES;
 
 // One DPP step on a double (both 32-bit halves moved with the same control);
 // lanes without a source, or outside row_mask, contribute 0.
@@ -108,7 +117,7 @@ __device__ __forceinline__ int64_t stats_index(const ScoreArgs &a, int li, int t
 template <bool F32>
 __global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
     using V = Vec<F32>;
-    const int c = blockIdx.x, u = blockIdx.y, li = blockIdx.z;
+    const int c = blockIdx.x, u = blockIdx.y, li = blockIdx.z / a.n_parts, part = blockIdx.z % a.n_parts;
     const int h = a.heads.head[li];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t v = (int64_t)c * kThreads + tid;       // vector within the unit
@@ -118,7 +127,13 @@ __global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
     const u32x4 *hist = (const u32x4 *)a.K_hist + (int64_t)h * a.cap * frame_vecs;
     const u32x4 *cur = (const u32x4 *)a.K_cur + (int64_t)h * a.cur_vecs;
     const int H = a.H;
-    const int tb = a.t_begin, te = a.t_end;  // streamed frames (0..H for a full pass)
+    // This workgroup streams frames [tb, te] of the range [t_begin, t_end]:
+    // parts overlap by one frame, whose SQ the later part writes and whose DOT
+    // with the previous frame the earlier part writes, so every per-frame
+    // partial is computed exactly as by a single pass.
+    const bool last_part = part == a.n_parts - 1;
+    const int tb = a.t_begin + part * a.part_frames;
+    const int te = last_part ? a.t_end : tb + a.part_frames;
 
     auto load = [&](int t) -> u32x4 {
         u32x4 r = u32x4{0, 0, 0, 0};
@@ -155,7 +170,7 @@ __global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
             sq = wave_sum(sq);
             dot = wave_sum(dot);
             if (lane == 63) {
-                a.ws[ws_index(a, li, t, u, c, w) * 2 + 0] = sq;
+                if (t < te || last_part) a.ws[ws_index(a, li, t, u, c, w) * 2 + 0] = sq;
                 if (t > tb) a.ws[ws_index(a, li, t - 1, u, c, w) * 2 + 1] = dot;
             }
         }
@@ -269,8 +284,21 @@ size_t score_workspace_doubles(int n_dyn, int H, int units_per_frame, int chunks
 
 namespace {
 
-hipError_t launch_partials(const ScoreArgs &a, bool f32, hipStream_t s) {
-    dim3 grid((unsigned)a.chunks_per_unit, (unsigned)a.units_per_frame, (unsigned)a.heads.n);
+// Frames per part of a streamed range of `frames` frames (kScorePartFrames,
+// or the whole range when it is short).
+int split_parts(int frames, int *part_frames) {
+    if (frames <= kScorePartFrames + 1) {
+        *part_frames = frames;
+        return 1;
+    }
+    *part_frames = kScorePartFrames;
+    return (frames - 1 + kScorePartFrames - 1) / kScorePartFrames;  // parts share a boundary frame
+}
+
+hipError_t launch_partials(const ScoreArgs &a0, bool f32, hipStream_t s) {
+    ScoreArgs a = a0;
+    a.n_parts = split_parts(a.t_end - a.t_begin + 1, &a.part_frames);
+    dim3 grid((unsigned)a.chunks_per_unit, (unsigned)a.units_per_frame, (unsigned)(a.heads.n * a.n_parts));
     if (f32)
         hipLaunchKernelGGL(score_partials_kernel<true>, grid, dim3(kThreads), 0, s, a);
     else
