@@ -162,14 +162,14 @@ def test_480p_many_segments():
     check_layer(cfg, x, rows=sample_rows(cfg.lq, 8, seed=15))
 
 
-@pytest.mark.parametrize("case", ["small", "480p"])
+@pytest.mark.parametrize("case", ["small", "small-d64", "small-f32", "480p"])
 def test_pipelined_step(case):
     """CompressedLayer.step: the static heads' gather and attention on a side
     stream while the dynamic heads are scored, compacted and attended on the
     main stream (fkv_chunk_attention_heads twice, each with its own workspace).
     Same parity bar as the serial path; the small case interleaves head types."""
-    if case == "small":
-        cfg = _small(F=100, L=25, d=128)
+    if case.startswith("small"):
+        cfg = _small(F=100, L=25, d=64 if case == "small-d64" else 128, dtype="f32" if case == "small-f32" else "bf16")
         x = W.make_layer_inputs(cfg, seed=30, frame_slot=np.array([3, 0, 8, 1, 5, 2, 7], np.int32))
         rows = None
     else:
@@ -178,7 +178,7 @@ def test_pipelined_step(case):
         rows = sample_rows(cfg.lq, 8, seed=31)
     _print_case("pipelined-step", case=case)
     layer = make_layer(cfg)
-    assert layer.side is not None and layer.attn_workspace2 is not None
+    assert layer.side is not None and (cfg.dtype == "f32" or layer.attn_workspace2 is not None)
     d = dev_inputs(x)
     O = torch.empty_like(d["Q"])
     lse = torch.empty((cfg.n_heads, cfg.lq), dtype=torch.float32, device="cuda")
