@@ -37,11 +37,12 @@
 // invariant; rows past the end of a source fall outside the buffer's range and
 // read as zero (the straddling tile merges both sources that way).
 //
-// Schedules: one workgroup per (head, query tile), or the balanced schedule
-// (Schedule below) that splits the key tiles of all items evenly over one
-// workgroup per CU and merges split items in a second kernel.  Heads with
-// longer caches make the per-item schedule uneven (at 480P a dynamic head has
-// 342 key tiles per query tile, a static head 245, on 228 items for 256 CUs).
+// Schedules: a work item is (entry of the launch's head list, query tile);
+// one workgroup per item, or the balanced schedule (attn_common.h) that splits
+// the key tiles of all items evenly over one workgroup per CU and merges split
+// items in a second kernel.  Heads with longer caches make the per-item
+// schedule uneven (at 480P a dynamic head has 342 key tiles per query tile, a
+// static head 245, on 228 items for 256 CUs).
 #include "attn_common.h"
 
 namespace fkv {
