@@ -14,9 +14,9 @@ layers of a real rollout would), so a step never finds its cache in the
 
 Prints ONE JSON line (see the keys below).  `value` is the wall-clock ms per
 step over the timed steps (lower is better); in the timed step the static
-heads' gather and attention run on a side stream while the dynamic heads are
-scored, compacted and attended on the main stream (they touch disjoint
-heads).  The per-stage breakdown comes from a
+heads' attention -- read in place from the cache, no gather -- runs on a side
+stream while the dynamic heads are scored, compacted and attended on the main
+stream (they touch disjoint heads).  The per-stage breakdown comes from a
 second pass that runs the four calls one after another with HIP events
 between them.  `roofline` covers the dominant
 kernel (chunk attention, MFMA-bound) timed with HIP events on the stream the
@@ -54,6 +54,9 @@ def parse():
     p.add_argument("--step", default="pipelined", choices=["pipelined", "serial"],
                    help="timed step: pipelined (static heads on a side stream) or the four calls "
                         "one after another on one stream")
+    p.add_argument("--static", default="in_place", choices=["in_place", "gather"],
+                   help="pipelined step: static heads attended in place from the cache, or gathered "
+                        "into the compressed buffers first")
     p.add_argument("--no-rollout", action="store_true",
                    help="skip the measured 30-layer x 4-step x 10-chunk rollout")
     p.add_argument("--no-extras", action="store_true",
@@ -149,14 +152,15 @@ def main():
         bufs.append(b)
         layers.append(CompressedLayer(cfg.n_heads, cfg.head_dim, cfg.frame_tokens, cfg.hist_frames,
                                       cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype,
-                                      cfg.heads, balanced=args.schedule == "balanced"))
+                                      cfg.heads, balanced=args.schedule == "balanced",
+                                      in_place=args.static == "in_place"))
     slots = x.frame_slot
     stream = torch.cuda.current_stream()
 
     def step(i):
-        """The timed step (CompressedLayer.step): the static heads' gather and
-        attention on a side stream while the dynamic heads are scored,
-        compacted and attended on the main stream."""
+        """The timed step (CompressedLayer.step): the static heads' attention
+        (in place, or gather + attention) on a side stream while the dynamic
+        heads are scored, compacted and attended on the main stream."""
         L, b = layers[i % len(layers)], bufs[i % len(layers)]
         L.step(b["K_hist"], b["V_hist"], slots, b["Q"], b["K_cur"], b["V_cur"], b["O"])
 
@@ -246,8 +250,10 @@ def main():
             "kv_len": kv_len.tolist(),
             "rotating_copies": args.copies,
             "attention_schedule": args.schedule,
-            "step": ("static heads (gather + attention) on a side stream, dynamic heads (score + select/compact "
-                     "+ attention) on the main stream" if args.step == "pipelined" else
+            "step": (("static heads (attention read in place from the cache" if args.static == "in_place" else
+                      "static heads (gather + attention") +
+                     ") on a side stream, dynamic heads (score + select/compact + attention) on the main stream"
+                     if args.step == "pipelined" else
                      "the four calls one after another on one stream"),
         },
         "roofline": {

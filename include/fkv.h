@@ -284,6 +284,26 @@ fkv_status fkv_chunk_attention_heads(const fkv_shape *shape, const int32_t *head
                                      void *O, float *lse, void *workspace,
                                      size_t workspace_bytes, void *stream);
 
+/* Chunk attention of the static heads (Eq. 2) read in place from the cache:
+ * for every head with heads[h].type == FKV_STATIC, the keys are the tokens of
+ * its kept history frames -- the first min(sink, H) frames and the last
+ * min(recent, H - sink) frames in logical order, logical frame t in slot
+ * frame_slot[t] of K_hist [n_heads][cap_frames][F][d] -- followed by
+ * K_cur[h], and likewise for the values.  This is exactly what
+ * fkv_compress_static followed by fkv_chunk_attention_heads over the static
+ * heads computes (same kernel, same rounding, the same result bit for bit),
+ * without the compressed copy: no Kc, Vc or kv_len.  Only the static heads'
+ * rows of O and lse are written.  Workspace and schedule as in
+ * fkv_chunk_attention.  bf16 only and frame_tokens >= 64 (a key tile then
+ * spans at most two cached frames): FKV_ERR_SHAPE otherwise.  frame_slot is
+ * a HOST int32 array of hist_frames entries in [0, cap_frames). */
+fkv_status fkv_chunk_attention_static(const fkv_shape *shape, const fkv_head *heads,
+                                      const void *K_hist, const void *V_hist,
+                                      const int32_t *frame_slot, const void *Q,
+                                      const void *K_cur, const void *V_cur, float scale,
+                                      void *O, float *lse, void *workspace,
+                                      size_t workspace_bytes, void *stream);
+
 /* ---------------------------------------------------------------------------
  * Offline head profiling (Sec. 4.1, Eq. 1).  A profiling pass runs the layer
  * on the uncompressed cache (every head static with recent_frames = H, so Kc

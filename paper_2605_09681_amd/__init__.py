@@ -14,6 +14,8 @@ Entry points (see ``include/fkv.h`` for the full contract):
 * :func:`fkv_select_compact`   -- BottomK + compaction (Sec. 4.3, Eq. 3)
 * :func:`fkv_chunk_attention`  -- chunk attention (Eq. 2 / Eq. 4)
 * :func:`fkv_chunk_attention_heads` -- the same for a subset of heads
+* :func:`fkv_chunk_attention_static` -- the static heads' attention read in
+  place from the cache (no compressed copy)
 * :func:`fkv_append_frames`    -- rolling-cache write of a finished chunk
 * :func:`fkv_fp8_pack`, :func:`fkv_chunk_attention_fp8` -- the FP8 variant of
   the chunk attention (App. F)
@@ -46,6 +48,7 @@ EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_select_compact_pooled", "fkv_score_stats_size", "fkv_score_history",
             "fkv_score_segments_cached",
             "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_chunk_attention_heads",
+            "fkv_chunk_attention_static",
             "fkv_fp8_sizes", "fkv_fp8_pack",
             "fkv_chunk_attention_fp8", "fkv_attention_mass_workspace_size", "fkv_attention_mass",
             "fkv_classify_heads", "fkv_last_error")
@@ -120,6 +123,8 @@ def lib():
         L.fkv_score_segments_cached.restype = ctypes.c_int
         L.fkv_chunk_attention_heads.argtypes = [S, P, I32, P, P, P, I32, P, P, P, F, P, P, P, SZ, P]
         L.fkv_chunk_attention_heads.restype = ctypes.c_int
+        L.fkv_chunk_attention_static.argtypes = [S, Hd, P, P, P, P, P, P, F, P, P, P, SZ, P]
+        L.fkv_chunk_attention_static.restype = ctypes.c_int
         L.fkv_fp8_sizes.argtypes = [S, I32] + [ctypes.POINTER(SZ)] * 4
         L.fkv_fp8_sizes.restype = ctypes.c_int
         L.fkv_fp8_pack.argtypes = [S, P, P, P, I32, P, P, P, P, P, P, P, P, SZ, P]
@@ -416,6 +421,28 @@ def fkv_chunk_attention_heads(shape: fkv_shape, heads: Sequence[int], Q, Kc, Vc,
     arr = (ctypes.c_int32 * max(len(ids), 1))(*ids)
     _raise(lib().fkv_chunk_attention_heads(ctypes.byref(shape), arr, len(ids), q, kc, vc, slab, kl, kq, vq,
                                            ctypes.c_float(scale), o, ls, ws, nws, _stream(stream)))
+
+
+def fkv_chunk_attention_static(shape: fkv_shape, heads, K_hist, V_hist, frame_slot, Q, K_cur, V_cur,
+                               scale: float, O, lse: Optional[torch.Tensor] = None,
+                               workspace: Optional[torch.Tensor] = None, stream=None):
+    """Attention of the static heads over their kept frames read in place
+    from K_hist / V_hist; only the static heads' rows of O and lse are
+    written."""
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    chunk = (shape.n_heads, _lq(shape), shape.head_dim)
+    kh, vh = _check(K_hist, "K_hist", dt, hist), _check(V_hist, "V_hist", dt, hist)
+    sl = _slots(frame_slot, shape.hist_frames)
+    q = _check(Q, "Q", dt, chunk)
+    kq, vq = _check(K_cur, "K_cur", dt, chunk), _check(V_cur, "V_cur", dt, chunk)
+    o = _check(O, "O", dt, chunk)
+    ls = None if lse is None else _check(lse, "lse", torch.float32, (shape.n_heads, _lq(shape)))
+    ws, nws = None, 0
+    if workspace is not None:
+        ws, nws = _check(workspace, "workspace", torch.uint8), workspace.numel()
+    _raise(lib().fkv_chunk_attention_static(ctypes.byref(shape), heads, kh, vh, sl, q, kq, vq,
+                                            ctypes.c_float(scale), o, ls, ws, nws, _stream(stream)))
 
 
 def fkv_fp8_sizes(shape: fkv_shape, slab: int):

@@ -9,7 +9,7 @@ namespace fkv {
 namespace attn {
 
 constexpr int BM = kAttnRowsBf16;  // query rows per workgroup (8 waves x 32)
-constexpr int BN = 64;             // keys per tile
+constexpr int BN = kAttnKeysPerTile;  // keys per tile
 
 // Number of key tiles of head h: [Kc[h][0:kv_len]; K_cur[h]] in tiles of BN.
 __device__ __forceinline__ int head_kvl(const AttnArgs &a, int h) {
@@ -18,6 +18,18 @@ __device__ __forceinline__ int head_kvl(const AttnArgs &a, int h) {
 }
 __device__ __forceinline__ int head_tiles(const AttnArgs &a, int h) {
     return (head_kvl(a, h) + a.Lq + BN - 1) / BN;
+}
+// The same for entry li of the launch's head list.  PAGED (a compile-time
+// switch): static heads read in place, whose history length follows from
+// their budgets, stored per list entry.
+template <bool PAGED = false>
+__device__ __forceinline__ int entry_kvl(const AttnArgs &a, int li) {
+    if constexpr (PAGED) return a.st_kept[li] * a.F;
+    return head_kvl(a, a.heads.head[li]);
+}
+template <bool PAGED = false>
+__device__ __forceinline__ int entry_tiles(const AttnArgs &a, int li) {
+    return (entry_kvl<PAGED>(a, li) + a.Lq + BN - 1) / BN;
 }
 
 // Work items are (entry li of the launch's head list, query tile qt),
@@ -43,20 +55,22 @@ struct ItemPos {
     int li, qt, T;
     int64_t ibase;
 };
+template <bool PAGED = false>
 __device__ __forceinline__ ItemPos locate(const AttnArgs &a, int64_t x) {
-    int li = 0, T = head_tiles(a, a.heads.head[0]);
+    int li = 0, T = entry_tiles<PAGED>(a, 0);
     int64_t base = 0;
     while (x >= base + (int64_t)a.n_qtiles * T) {
         base += (int64_t)a.n_qtiles * T;
-        T = head_tiles(a, a.heads.head[++li]);
+        T = entry_tiles<PAGED>(a, ++li);
     }
     const int qt = (int)((x - base) / T);
     return ItemPos{li, qt, T, base + (int64_t)qt * T};
 }
 
+template <bool PAGED = false>
 __device__ __forceinline__ Schedule make_schedule(const AttnArgs &a) {
     int64_t total = 0;
-    for (int li = 0; li < a.heads.n; ++li) total += (int64_t)a.n_qtiles * head_tiles(a, a.heads.head[li]);
+    for (int li = 0; li < a.heads.n; ++li) total += (int64_t)a.n_qtiles * entry_tiles<PAGED>(a, li);
     Schedule sc;
     sc.total = total;
     sc.G = (int)(total < a.n_blocks ? total : a.n_blocks);

@@ -621,12 +621,21 @@ fkv::HeadList all_heads(int n_heads) {
     return l;
 }
 
+// Static heads attended in place: the kept history frames are read from the
+// cache through the frame-slot map instead of from a compressed copy.
+struct PagedHistory {
+    const void *K_hist, *V_hist;
+    const int32_t *frame_slot;
+    const fkv_head *heads;
+};
+
 fkv_status chunk_attention_impl(const fkv_shape *shape, const fkv::HeadList &list, const void *Q,
                                 const void *Kc, const void *Vc, int32_t slab, const int32_t *kv_len,
                                 const void *K_cur, const void *V_cur, float scale, void *O, float *lse,
-                                void *workspace, size_t workspace_bytes, void *stream) {
+                                void *workspace, size_t workspace_bytes, void *stream,
+                                const PagedHistory *paged = nullptr) {
     fkv_status st;
-    if (!Q || !K_cur || !V_cur || !O || !kv_len) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (!Q || !K_cur || !V_cur || !O || (!kv_len && !paged)) return fail(FKV_ERR_ARG, "NULL tensor pointer");
     if (slab < 0) return fail(FKV_ERR_ARG, "slab %d < 0", slab);
     if (slab > 0 && (!Kc || !Vc)) return fail(FKV_ERR_ARG, "NULL Kc/Vc with slab %d", slab);
     if (!(scale > 0.f) || !isfinite(scale)) return fail(FKV_ERR_ARG, "scale %g must be positive and finite", (double)scale);
@@ -662,6 +671,21 @@ fkv_status chunk_attention_impl(const fkv_shape *shape, const fkv::HeadList &lis
     a.items_per_xcd = (a.n_items + 7) / 8;
     a.n_blocks = blocks;
     a.part = (float *)workspace;
+    if (paged) {
+        a.paged = 1;
+        a.K_hist = paged->K_hist;
+        a.V_hist = paged->V_hist;
+        a.F = shape->frame_tokens;
+        a.cap = shape->cap_frames;
+        for (int li = 0; li < list.n; ++li) {
+            const int h = list.head[li];
+            const StaticPlan p = static_plan(shape->hist_frames, paged->heads[h]);
+            a.st_first[li] = p.n_first;
+            a.st_gap[li] = p.gap;
+            a.st_kept[li] = p.n_kept;
+        }
+        for (int t = 0; t < shape->hist_frames; ++t) a.slots.slot[t] = paged->frame_slot[t];
+    }
     (void)hipGetLastError();
     hipError_t e = bf16 ? fkv::launch_attention_bf16(a, shape->head_dim, (hipStream_t)stream)
                         : fkv::launch_attention_f32(a, shape->head_dim, (hipStream_t)stream);
@@ -703,6 +727,28 @@ fkv_status fkv_chunk_attention_heads(const fkv_shape *shape, const int32_t *head
     }
     return chunk_attention_impl(shape, list, Q, Kc, Vc, slab, kv_len, K_cur, V_cur, scale, O, lse,
                                 workspace, workspace_bytes, stream);
+}
+
+fkv_status fkv_chunk_attention_static(const fkv_shape *shape, const fkv_head *heads, const void *K_hist,
+                                      const void *V_hist, const int32_t *frame_slot, const void *Q,
+                                      const void *K_cur, const void *V_cur, float scale, void *O, float *lse,
+                                      void *workspace, size_t workspace_bytes, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if (shape->dtype != FKV_BF16) return fail(FKV_ERR_SHAPE, "in-place static attention needs bf16");
+    if (shape->frame_tokens < fkv::kAttnKeysPerTile)
+        return fail(FKV_ERR_SHAPE, "in-place static attention needs frame_tokens %d >= %d",
+                    shape->frame_tokens, fkv::kAttnKeysPerTile);
+    if (shape->hist_frames > 0 && (!K_hist || !V_hist)) return fail(FKV_ERR_ARG, "NULL K_hist/V_hist");
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+    fkv::HeadList list;
+    memset(&list, 0, sizeof list);
+    for (int h = 0; h < shape->n_heads; ++h)
+        if (heads[h].type == FKV_STATIC) list.head[list.n++] = h;
+    const PagedHistory paged{K_hist, V_hist, frame_slot, heads};
+    return chunk_attention_impl(shape, list, Q, nullptr, nullptr, 0, nullptr, K_cur, V_cur, scale, O, lse,
+                                workspace, workspace_bytes, stream, &paged);
 }
 
 fkv_status fkv_fp8_sizes(const fkv_shape *shape, int32_t slab, size_t *q_bytes, size_t *kv_bytes,

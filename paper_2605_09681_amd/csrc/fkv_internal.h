@@ -128,6 +128,16 @@ struct AttnArgs {
     int64_t fp8_rows;               // FP8 path: key rows per head of the packed K / V^T
     float scale;                    // softmax scale
     float scale_log2;               // scale * log2(e)
+    // Paged static heads (fkv_chunk_attention_static): the retained history is
+    // read straight from the cache -- for head h = heads.head[li], kept frame y
+    // is logical frame y (y < st_first[li]) or y + st_gap[li], in slot
+    // slots.slot[t] of K_hist / V_hist [n_heads][cap][F][d] -- and its history
+    // length is st_kept[li] * F (kv_len is not read).
+    int32_t paged;
+    const void *K_hist, *V_hist;
+    int32_t F, cap;
+    int32_t st_first[FKV_MAX_HEADS], st_gap[FKV_MAX_HEADS], st_kept[FKV_MAX_HEADS];
+    SlotTable slots;
 };
 
 // ------------------------------------------------------------ FP8 packing
@@ -145,6 +155,7 @@ struct Fp8PackArgs {
 
 constexpr int kScoreThreads = 256;
 constexpr int kAttnRowsBf16 = 256;  // query rows per attention workgroup (bf16 MFMA kernel)
+constexpr int kAttnKeysPerTile = 64; // keys per tile of the bf16 MFMA kernel
 constexpr int kAttnRowsF32 = 32;    // query rows per attention workgroup (fp32 kernel)
 constexpr int kScoreWaves = kScoreThreads / 64;
 

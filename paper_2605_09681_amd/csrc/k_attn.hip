@@ -115,6 +115,63 @@ __device__ __forceinline__ void load_tile(const uint16_t *hist, const uint16_t *
     }
 }
 
+// Cache slots of a static head's kept frames, one byte each (cap <= 256):
+// kept frame y is logical frame y (y < st_first) or y + st_gap, and its slot
+// sits in byte y >> 6 of lane y & 63 -- up to 256 frames in one VGPR, looked
+// up with v_readlane, so the tile loop never waits on a scalar load (whose
+// counter it shares with the LDS reads).
+__device__ __forceinline__ uint32_t kept_slot_table(const AttnArgs &a, int li, int lane) {
+    const int n = a.st_kept[li], first = a.st_first[li], gap = a.st_gap[li];
+    uint32_t tab = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int y = lane + 64 * k;
+        if (y < n) tab |= (uint32_t)a.slots.slot[y < first ? y : y + gap] << (8 * k);
+    }
+    return tab;
+}
+__device__ __forceinline__ int kept_slot(uint32_t tab, int y) {
+    return (int)((uint32_t)__builtin_amdgcn_readlane((int)tab, y & 63) >> (8 * (y >> 6))) & 255;
+}
+
+// The same for a static head read in place from the cache (paged): history
+// row p is row p mod F of kept frame y = p / F, in cache slot
+// kept_slot(tab, y).  With F >= 64 a tile touches at most two kept frames and
+// the chunk; each part has its own range-checked buffer and the three loads
+// are OR-ed, every row outside a part reading as zero.
+template <int D, int N>
+__device__ __forceinline__ void load_tile_paged(const uint16_t *hist, uint32_t tab, int F,
+                                                const uint16_t *chunk, int j0, int kvl, int Lk, int Lq,
+                                                u32x4 *dst, uint32_t off0, uint32_t step) {
+    if (j0 >= kvl) {
+        const auto r = rsrc(chunk + (size_t)(j0 - kvl) * D, (uint32_t)(Lk - j0) * D * 2);
+#pragma unroll
+        for (int i = 0; i < N; ++i) dst[i] = bload(r, off0 + i * step);
+        return;
+    }
+    auto frame = [&](int y) { return hist + (size_t)kept_slot(tab, y) * F * D; };
+    const int y0 = j0 / F, r0 = j0 - y0 * F;
+    const int na = min(min(F - r0, kvl - j0), BN);            // rows of kept frame y0
+    const auto ra = rsrc(frame(y0) + (size_t)r0 * D, (uint32_t)na * D * 2);
+    if (na == BN) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) dst[i] = bload(ra, off0 + i * step);
+        return;
+    }
+    // the rest of the tile: the next kept frame while history lasts, then the chunk
+    const int nb = j0 + na < kvl ? min(BN - na, kvl - (j0 + na)) : 0;
+    const int nc = j0 + na + nb >= kvl ? min(BN - na - nb, Lq) : 0;
+    const auto rb = rsrc(nb > 0 ? frame(y0 + 1) : hist, (uint32_t)nb * D * 2);
+    const auto rc = rsrc(chunk, (uint32_t)nc * D * 2);
+    const uint32_t sb = (uint32_t)na * D * 2, sc = (uint32_t)(na + nb) * D * 2;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const uint32_t o = off0 + i * step;
+        // rows before a part's start wrap to huge offsets: out of range, read 0
+        dst[i] = bload(ra, o) | bload(rb, o - sb) | bload(rc, o - sc);
+    }
+}
+
 // One MFMA block of a wave: optionally O^T += V^T P^T for one key tile (4 x MB
 // products, accumulators o[mb] cycled so consecutive products are independent),
 // then optionally S^T = K Q^T for the next tile (KS x 2 products, the two
@@ -182,11 +239,12 @@ __device__ __forceinline__ void mfma_block(const uint16_t *vs, const uint16_t *k
 // whole item and the normalised output (and lse) is written; otherwise the
 // partial result goes to the slot.  Uses every thread of the workgroup and
 // leaves no LDS read pending.
-template <int D>
+template <int D, bool PAGED>
 __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2][Cfg<D>::TILE],
-                                             uint16_t (&Vs)[2][Cfg<D>::VTILE], int h, int qt, int t0,
+                                             uint16_t (&Vs)[2][Cfg<D>::VTILE], int li, int qt, int t0,
                                              int t1, int rot, float *slot) {
     using C = Cfg<D>;
+    const int h = a.heads.head[li];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int grp = wave >> 2;  // 0: leads by half a tile, 1: trails
     const int l32 = lane & 31, hl = lane >> 5;
@@ -205,12 +263,15 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
         qf[kk] = __builtin_bit_cast(bf16x8_t, v);
     }
 
-    const int kvl = head_kvl(a, h);
+    const int kvl = entry_kvl<PAGED>(a, li);
     const int Lk = kvl + Lq;
-    const uint16_t *Kc = (const uint16_t *)a.Kc + (size_t)h * a.slab * D;
-    const uint16_t *Vc = (const uint16_t *)a.Vc + (size_t)h * a.slab * D;
+    const uint16_t *Kc = PAGED ? (const uint16_t *)a.K_hist + (size_t)h * a.cap * a.F * D
+                               : (const uint16_t *)a.Kc + (size_t)h * a.slab * D;
+    const uint16_t *Vc = PAGED ? (const uint16_t *)a.V_hist + (size_t)h * a.cap * a.F * D
+                               : (const uint16_t *)a.Vc + (size_t)h * a.slab * D;
     const uint16_t *Kq = (const uint16_t *)a.K_cur + (size_t)h * Lq * D;
     const uint16_t *Vq = (const uint16_t *)a.V_cur + (size_t)h * Lq * D;
+    const uint32_t ktab = PAGED ? kept_slot_table(a, li, lane) : 0u;
 
     // Loop-invariant per-thread load geometry within the thread's group of 256:
     // rows r0 + RPP*i, chunk c (group 0 stages K tiles, group 1 V tiles).
@@ -230,10 +291,18 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
         return (k >= T ? k - T : k) * BN;
     };
     auto load_k = [&](int j0, u32x4 (&dst)[4]) {
-        load_tile<D, C::NV>(Kc, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
+        if (PAGED)
+            load_tile_paged<D, C::NV>(Kc, ktab, a.F, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
+        else
+            load_tile<D, C::NV>(Kc, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
     };
     auto load_v = [&](int j0, u32x4 (&dst)[4]) {
-        if (gtid < C::VUNITS) load_tile<D, 4>(Vc, Vq, j0, kvl, Lk, Lq, dst, voffv, D * 2);
+        if (gtid < C::VUNITS) {
+            if (PAGED)
+                load_tile_paged<D, 4>(Vc, ktab, a.F, Vq, j0, kvl, Lk, Lq, dst, voffv, D * 2);
+            else
+                load_tile<D, 4>(Vc, Vq, j0, kvl, Lk, Lq, dst, voffv, D * 2);
+        }
     };
     auto store_k = [&](uint16_t *tile, const u32x4 (&src)[4]) {
 #pragma unroll
@@ -416,7 +485,7 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
 // of items: the query tiles of a head then share that XCD's L2.
 // BAL = true: the balanced schedule above, with the same XCD-contiguous
 // assignment of ranges (n_blocks is a multiple of 8).
-template <int D, bool BAL>
+template <int D, bool BAL, bool PAGED>
 __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     using C = Cfg<D>;
     __shared__ __attribute__((aligned(16))) uint16_t Ks[2][C::TILE];
@@ -426,11 +495,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
         const int item = (blockIdx.x & 7) * a.items_per_xcd + (blockIdx.x >> 3);
         if (item >= a.n_items) return;
         const int li = item / a.n_qtiles;
-        const int h = a.heads.head[li];
-        attn_segment<D>(a, Ks, Vs, h, item - li * a.n_qtiles, 0, head_tiles(a, h), 0, nullptr);
+        attn_segment<D, PAGED>(a, Ks, Vs, li, item - li * a.n_qtiles, 0, entry_tiles<PAGED>(a, li), 0, nullptr);
         return;
     }
-    const Schedule sc = make_schedule(a);
+    const Schedule sc = make_schedule<PAGED>(a);
     const int r = (blockIdx.x & 7) * (a.n_blocks >> 3) + (blockIdx.x >> 3);
     if (r >= sc.G) return;
     const int64_t end = sc.start(r + 1);
@@ -438,8 +506,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     bool first = true;
     while (cur < end) {
         // locate the item holding tile `cur`
-        const ItemPos ip = locate(a, cur);
-        const int h = a.heads.head[ip.li], qt = ip.qt, T = ip.T;
+        const ItemPos ip = locate<PAGED>(a, cur);
+        const int qt = ip.qt, T = ip.T;
         const int64_t ibase = ip.ibase;
         const int t0 = (int)(cur - ibase);
         const int t1 = (int)((end < ibase + T ? end : ibase + T) - ibase);
@@ -452,7 +520,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
         // sweep its K/V in step (later parts in step among themselves, shifted
         // by a range length), so the XCD's L2 serves the re-reads.
         const int rot = (int)((ibase - sc.start(sc.owner(ibase))) % T);
-        attn_segment<D>(a, Ks, Vs, h, qt, t0, t1, rot, slot);
+        attn_segment<D, PAGED>(a, Ks, Vs, ip.li, qt, t0, t1, rot, slot);
         cur = ibase + t1;
         first = false;
     }
@@ -463,17 +531,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
 //   M = max_j m_j,  w_j = 2^(m_j - M) l_j,  L = sum_j w_j,  O = sum_j w_j o_j / L,
 // and lse = ln 2 * M + ln L.  Workgroup (item, w) handles the 32 rows of wave
 // w of the item's query tile; items computed whole are skipped.
-template <int D>
+template <int D, bool PAGED>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     using C = Cfg<D>;
     constexpr int kML = BM * D / 2;  // float offset of m within a slot
     const int item = blockIdx.x, w = blockIdx.y;
     const int li = item / a.n_qtiles, qt = item - li * a.n_qtiles;
     const int h = a.heads.head[li];
-    const Schedule sc = make_schedule(a);
+    const Schedule sc = make_schedule<PAGED>(a);
     int64_t P = 0;
-    for (int l = 0; l < li; ++l) P += (int64_t)a.n_qtiles * head_tiles(a, a.heads.head[l]);
-    const int T = head_tiles(a, h);
+    for (int l = 0; l < li; ++l) P += (int64_t)a.n_qtiles * entry_tiles<PAGED>(a, l);
+    const int T = entry_tiles<PAGED>(a, li);
     P += (int64_t)qt * T;
     const int b0 = sc.owner(P), b1 = sc.owner(P + T - 1);
     if (b0 == b1) return;
@@ -621,28 +689,41 @@ __global__ __launch_bounds__(256) void attn_mass_finalize_kernel(AttnArgs a) {
 }  // namespace
 
 hipError_t launch_attention_merge(const AttnArgs &a, int head_dim, hipStream_t s) {
-    if (head_dim == 128)
-        hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(a.n_items, BM / 32), dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(a.n_items, BM / 32), dim3(256), 0, s, a);
+    const dim3 grid(a.n_items, BM / 32);
+    if (a.paged) {
+        if (head_dim == 128)
+            hipLaunchKernelGGL((attn_merge_kernel<128, true>), grid, dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL((attn_merge_kernel<64, true>), grid, dim3(256), 0, s, a);
+    } else {
+        if (head_dim == 128)
+            hipLaunchKernelGGL((attn_merge_kernel<128, false>), grid, dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL((attn_merge_kernel<64, false>), grid, dim3(256), 0, s, a);
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s) {
+template <bool PAGED>
+hipError_t launch_bf16(const AttnArgs &a, int head_dim, hipStream_t s) {
     if (a.n_blocks > 0) {
         if (head_dim == 128)
-            hipLaunchKernelGGL((attn_bf16_kernel<128, true>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
+            hipLaunchKernelGGL((attn_bf16_kernel<128, true, PAGED>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
         else
-            hipLaunchKernelGGL((attn_bf16_kernel<64, true>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
+            hipLaunchKernelGGL((attn_bf16_kernel<64, true, PAGED>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
         const hipError_t e = hipGetLastError();
         return e != hipSuccess ? e : launch_attention_merge(a, head_dim, s);
     }
     const unsigned blocks = (unsigned)a.items_per_xcd * 8u;
     if (head_dim == 128)
-        hipLaunchKernelGGL((attn_bf16_kernel<128, false>), dim3(blocks), dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL((attn_bf16_kernel<128, false, PAGED>), dim3(blocks), dim3(kThreads), 0, s, a);
     else
-        hipLaunchKernelGGL((attn_bf16_kernel<64, false>), dim3(blocks), dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL((attn_bf16_kernel<64, false, PAGED>), dim3(blocks), dim3(kThreads), 0, s, a);
     return hipGetLastError();
+}
+
+hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s) {
+    return a.paged ? launch_bf16<true>(a, head_dim, s) : launch_bf16<false>(a, head_dim, s);
 }
 
 hipError_t launch_attention_mass(const AttnArgs &a, int head_dim, hipStream_t s) {

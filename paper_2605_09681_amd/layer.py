@@ -11,12 +11,16 @@ of one layer:
 4. ``fkv_chunk_attention`` (all heads, Eq. 2 / Eq. 4)
 
 Steps 1-2 and step 3 touch disjoint heads.  :meth:`CompressedLayer.step`
-therefore runs, on a second stream (default priority), the static gather and
-then attention over the static heads (``fkv_chunk_attention_heads``), while
-the current stream scores and compacts the dynamic heads and then attends
-them: the HBM-bound compression of the dynamic heads runs under the
-MFMA-bound attention of the static heads.  :meth:`CompressedLayer.compress`
-alone overlaps the static gather with the dynamic compression the same way.
+therefore runs, on a second stream (default priority), the static heads'
+attention, while the current stream scores and compacts the dynamic heads and
+then attends them (``fkv_chunk_attention_heads``): the HBM-bound compression
+of the dynamic heads runs under the MFMA-bound attention of the static heads.
+For bf16 with frames of at least 64 tokens the static heads are attended in
+place (``fkv_chunk_attention_static``: their kept frames are read straight
+from the cache, so step 3 is skipped and their rows of Kc/Vc/kv_len are left
+unwritten); otherwise the side stream gathers them first.
+:meth:`CompressedLayer.compress` alone overlaps the static gather with the
+dynamic compression the same way.
 The individual stages enqueue on the current torch stream; nothing
 synchronises with the host.
 """
@@ -29,7 +33,7 @@ import torch
 
 from . import (FKV_DYNAMIC, FKV_STATIC, fkv_append_frames, fkv_attention_mass,
                fkv_attention_workspace_size, fkv_chunk_attention, fkv_chunk_attention_heads,
-               fkv_classify_heads,
+               fkv_chunk_attention_static, fkv_classify_heads,
                fkv_chunk_attention_fp8, fkv_compress_static, fkv_fp8_pack, fkv_fp8_sizes,
                fkv_num_segments, fkv_score_pooled, fkv_score_pooled_workspace_size,
                fkv_score_history, fkv_score_segments, fkv_score_segments_cached,
@@ -37,11 +41,16 @@ from . import (FKV_DYNAMIC, FKV_STATIC, fkv_append_frames, fkv_attention_mass,
                fkv_select_compact_pooled, make_heads, make_shape, slab_tokens)
 
 
+def static_in_place_supported(dtype, frame_tokens: int) -> bool:
+    """Whether fkv_chunk_attention_static takes this dtype and frame size."""
+    return dtype in ("bf16", 0) and frame_tokens >= 64
+
+
 class CompressedLayer:
     def __init__(self, n_heads: int, head_dim: int, frame_tokens: int, hist_frames: int,
                  cap_frames: int, chunk_frames: int, seg_tokens: int, dtype: str,
                  budgets: Sequence, device="cuda", slab: Optional[int] = None,
-                 balanced: bool = True, overlap: bool = True):
+                 balanced: bool = True, overlap: bool = True, in_place: Optional[bool] = None):
         self.shape = make_shape(n_heads, head_dim, frame_tokens, hist_frames, cap_frames,
                                 chunk_frames, seg_tokens, dtype)
         self.heads = make_heads(budgets)
@@ -75,6 +84,11 @@ class CompressedLayer:
         self.dynamic_heads = [h for h, t in enumerate(self.types) if t == FKV_DYNAMIC]
         if self.side is not None and self.attn_workspace is not None:
             self.attn_workspace2 = torch.empty_like(self.attn_workspace)
+        # static heads attended in place by step() (bf16, frames >= 64 tokens)
+        can = static_in_place_supported(dtype, frame_tokens)
+        if in_place and not can:
+            raise ValueError("in-place static attention needs bf16 and frame_tokens >= 64")
+        self.static_in_place = can if in_place is None else bool(in_place)
 
     # individual stages -------------------------------------------------------
     def score(self, K_hist, frame_slot, K_cur):
@@ -137,8 +151,16 @@ class CompressedLayer:
         if self.has_static:
             self.compress_static(K_hist, V_hist, frame_slot)
 
+    def attention_static(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse=None, workspace=None):
+        """The static heads' attention read in place from the cache."""
+        fkv_chunk_attention_static(self.shape, self.heads, K_hist, V_hist, frame_slot, Q, K_cur, V_cur,
+                                   self.scale, O, lse, workspace)
+
     def step(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse=None):
         if self.side is None:
+            if self.static_in_place and not self.has_dynamic:
+                self.attention_static(K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse, self.attn_workspace)
+                return
             self.compress(K_hist, V_hist, frame_slot, K_cur)
             self.attention(Q, K_cur, V_cur, O, lse)
             return
@@ -146,9 +168,12 @@ class CompressedLayer:
         args = (self.Kc, self.Vc, self.kv_len, K_cur, V_cur, self.scale, O, lse)
         self.side.wait_stream(main)
         with torch.cuda.stream(self.side):
-            self.compress_static(K_hist, V_hist, frame_slot)
-            fkv_chunk_attention_heads(self.shape, self.static_heads, Q, *args[:7], lse=lse,
-                                      workspace=self.attn_workspace2)
+            if self.static_in_place:
+                self.attention_static(K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse, self.attn_workspace2)
+            else:
+                self.compress_static(K_hist, V_hist, frame_slot)
+                fkv_chunk_attention_heads(self.shape, self.static_heads, Q, *args[:7], lse=lse,
+                                          workspace=self.attn_workspace2)
         for t in (K_hist, V_hist, Q, K_cur, V_cur, O) + ((lse,) if lse is not None else ()):
             t.record_stream(self.side)
         self.score(K_hist, frame_slot, K_cur)
@@ -204,7 +229,9 @@ class RolloutStack:
     the history length H = len(frame_slot) may grow from chunk to chunk (0 on
     the first one).  Per layer and AR step :meth:`run_layer` makes the four
     C-ABI calls (the static gather on a side stream next to the dynamic heads'
-    scoring and compaction), or -- with a shared score row from
+    scoring and compaction; for bf16 and frames of at least 64 tokens the
+    static heads are attended in place, with no gather), or -- with a shared
+    score row from
     :meth:`score_pooled` -- the first-block proxy of Sec. 4.3: one similarity
     row computed from one layer's keys pooled over all heads and reused by the
     dynamic heads of every layer.  ``budgets`` are per-head objects with
@@ -247,6 +274,7 @@ class RolloutStack:
         self.attn_ws2 = torch.empty_like(self.attn_ws) if (n > 0 and overlap) else None
         self.scale = 1.0 / math.sqrt(head_dim)
         self.side = torch.cuda.Stream(device=dev) if overlap else None
+        self.static_in_place = static_in_place_supported(dtype, frame_tokens)
         self._shapes, self._heads = {}, {}
         # per-layer statistics of incremental rescoring (listed heads x window x units x 2)
         units = frame_tokens // min(seg_tokens, frame_tokens)
@@ -309,9 +337,9 @@ class RolloutStack:
     def run_layer(self, layer: int, budgets, frame_slot, Q, K_cur, V_cur, O, lse=None, pooled=None,
                   incremental: bool = False):
         """One AR step of one layer: compress its cache, then chunk attention
-        into O -- the static heads (gather, then their attention) on the side
-        stream while the dynamic heads are scored, compacted and attended on
-        the current stream.  ``pooled`` (a row from :meth:`score_pooled`)
+        into O -- the static heads (attended in place, or gathered and then
+        attended) on the side stream while the dynamic heads are scored,
+        compacted and attended on the current stream.  ``pooled`` (a row from :meth:`score_pooled`)
         replaces the layer's own per-head scoring."""
         H = len(frame_slot)
         shape = self.shape(H)
@@ -327,8 +355,12 @@ class RolloutStack:
             static_ids = [h for h, t in enumerate(types) if t == FKV_STATIC]
             side.wait_stream(main)
             with torch.cuda.stream(side):
-                fkv_compress_static(shape, heads, Kh, Vh, frame_slot, self.Kc, self.Vc, self.kv_len)
-                fkv_chunk_attention_heads(shape, static_ids, Q, *att, lse=lse, workspace=self.attn_ws2)
+                if self.static_in_place:
+                    fkv_chunk_attention_static(shape, heads, Kh, Vh, frame_slot, Q, K_cur, V_cur, self.scale, O,
+                                               lse, self.attn_ws2)
+                else:
+                    fkv_compress_static(shape, heads, Kh, Vh, frame_slot, self.Kc, self.Vc, self.kv_len)
+                    fkv_chunk_attention_heads(shape, static_ids, Q, *att, lse=lse, workspace=self.attn_ws2)
             for t in (Kh, Vh, Q, K_cur, V_cur, O) + ((lse,) if lse is not None else ()):
                 t.record_stream(side)
         elif has_static:

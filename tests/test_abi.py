@@ -237,6 +237,26 @@ def test_attention_heads_arg_errors(fkv):
     assert call([]) == 0
 
 
+def test_attention_static_arg_errors(fkv):
+    """fkv_chunk_attention_static: bf16 with frame_tokens >= 64 only (shape
+    error otherwise); slots, pointers and scale are checked before any device
+    work; a layer without static heads enqueues nothing."""
+    L = fkv.lib()
+
+    def call(shape, heads=None, slots=None, K=FAKE, scale=0.1):
+        H = shape.hist_frames
+        sl = (ctypes.c_int32 * max(H, 1))(*(range(H) if slots is None else slots))
+        return L.fkv_chunk_attention_static(ctypes.byref(shape), heads or _heads(fkv), K, FAKE, sl, FAKE, FAKE,
+                                            FAKE, ctypes.c_float(scale), FAKE, None, None, 0, None)
+    assert call(_shape(fkv, frame_tokens=32, seg_tokens=32)) == 2
+    assert call(_shape(fkv, dtype="f32")) == 2
+    assert call(_shape(fkv), slots=[0, 1, 2, 4]) == 1      # slot outside [0, cap_frames)
+    assert call(_shape(fkv), K=None) == 1
+    assert call(_shape(fkv), scale=-1.0) == 1
+    dyn = _heads(fkv, W.HeadBudget(W.DYNAMIC, 0, 0, 2), W.HeadBudget(W.DYNAMIC, 1, 0, 1))
+    assert call(_shape(fkv), heads=dyn) == 0
+
+
 def test_incremental_rescoring_args(fkv):
     """Stats size = listed heads x H x units x 2 doubles; errors before any
     device work; nothing to do (OK) when there is no history."""

@@ -162,12 +162,13 @@ def test_480p_many_segments():
     check_layer(cfg, x, rows=sample_rows(cfg.lq, 8, seed=15))
 
 
-@pytest.mark.parametrize("case", ["small", "small-d64", "small-f32", "480p"])
+@pytest.mark.parametrize("case", ["small", "small-d64", "small-f32", "480p", "480p-gather"])
 def test_pipelined_step(case):
-    """CompressedLayer.step: the static heads' gather and attention on a side
-    stream while the dynamic heads are scored, compacted and attended on the
-    main stream (fkv_chunk_attention_heads twice, each with its own workspace).
-    Same parity bar as the serial path; the small case interleaves head types."""
+    """CompressedLayer.step: the static heads' attention on a side stream --
+    read in place from the cache (bf16), or gathered first (fp32, and the
+    480p-gather case) -- while the dynamic heads are scored, compacted and
+    attended on the main stream, each stream with its own workspace.  Same
+    parity bar as the serial path; the small case interleaves head types."""
     if case.startswith("small"):
         cfg = _small(F=100, L=25, d=64 if case == "small-d64" else 128, dtype="f32" if case == "small-f32" else "bf16")
         x = W.make_layer_inputs(cfg, seed=30, frame_slot=np.array([3, 0, 8, 1, 5, 2, 7], np.int32))
@@ -177,15 +178,16 @@ def test_pipelined_step(case):
         x = W.make_layer_inputs(cfg, seed=31)
         rows = sample_rows(cfg.lq, 8, seed=31)
     _print_case("pipelined-step", case=case)
-    layer = make_layer(cfg)
+    layer = make_layer(cfg, in_place=False if case == "480p-gather" else None)
     assert layer.side is not None and (cfg.dtype == "f32" or layer.attn_workspace2 is not None)
+    assert layer.static_in_place == (cfg.dtype == "bf16" and case != "480p-gather")
     d = dev_inputs(x)
     O = torch.empty_like(d["Q"])
     lse = torch.empty((cfg.n_heads, cfg.lq), dtype=torch.float32, device="cuda")
     layer.step(d["K_hist"], d["V_hist"], x.frame_slot, d["Q"], d["K_cur"], d["V_cur"], O, lse)
     torch.cuda.synchronize()
     ref = oracle.run_layer(cfg, x, rows=rows, scale=1 / math.sqrt(cfg.head_dim))
-    assert_compression_exact(cfg, layer, ref)
+    assert_compression_exact(cfg, layer, ref, skip_static=layer.static_in_place)
     assert_attention_close(O, ref, cfg.dtype, lse)
 
 
@@ -210,6 +212,66 @@ def test_attention_heads_subset(balanced):
     Of, lf = from_dev(O), from_dev(lse)
     for h in range(cfg.n_heads):
         if h in listed:
+            one = oracle.LayerResult(None, None, None, None, None, None, ref.rows, ref.O[h:h + 1], ref.lse[h:h + 1])
+            assert_attention_close(O[h:h + 1], one, "bf16", lse[h:h + 1])
+        else:
+            assert (W.bf16_bits_to_f32(Of[h]) == 7.0).all() and (lf[h] == -3.0).all(), h
+
+
+_PERM = np.array([3, 0, 8, 1, 5, 2, 7], np.int32)
+
+
+@pytest.mark.parametrize("case", ["F100-d128", "F64-d64-per-item", "F80-budgets", "H0", "H2", "480p"])
+def test_attention_static_in_place(case):
+    """fkv_chunk_attention_static reads the static heads' kept frames straight
+    from the slot-permuted cache: bit for bit what fkv_compress_static followed
+    by fkv_chunk_attention_heads over the static heads gives, the other heads'
+    rows of O and lse untouched, and within the attention bar of the oracle.
+    Frames of 100 and 80 tokens put frame boundaries inside key tiles; the
+    budgets cover a full-history window, a sink longer than the history, an
+    empty history window (chunk only) and a one-frame gap."""
+    import paper_2605_09681_amd as fkv
+    balanced, slot, rows = True, _PERM, None
+    if case == "F100-d128":
+        cfg = _small(F=100, L=25, d=128)
+    elif case == "F64-d64-per-item":
+        cfg, balanced = _small(F=64, L=16, d=64), False
+    elif case == "F80-budgets":
+        S, D = W.STATIC, W.DYNAMIC
+        cfg = _small(F=80, L=20, d=128, heads=(
+            W.HeadBudget(S, 0, 7), W.HeadBudget(D, 1, 0, 2, W.SCOPE_FRAME), W.HeadBudget(S, 9, 0),
+            W.HeadBudget(S, 0, 0), W.HeadBudget(S, 3, 3), W.HeadBudget(S, 0, 1)))
+    elif case == "H0":
+        cfg, slot = _small(F=100, L=25, H=0, cap=4, d=64), np.zeros(0, np.int32)
+    elif case == "H2":
+        cfg, slot = _small(F=72, L=24, H=2, cap=3, d=64, heads=(
+            W.HeadBudget(W.STATIC, 3, 4), W.HeadBudget(W.DYNAMIC, 1, 0, 1, W.SCOPE_FRAME),
+            W.HeadBudget(W.STATIC, 0, 1))), np.array([2, 0], np.int32)
+    else:
+        cfg, slot = W.wan_layer_config("480p"), None
+        rows = sample_rows(cfg.lq, 8, seed=33)
+    x = W.make_layer_inputs(cfg, seed=33, frame_slot=slot)
+    _print_case("attention-static-in-place", case=case, balanced=balanced)
+    static = [h for h, b in enumerate(cfg.heads) if b.type == W.STATIC]
+    layer = make_layer(cfg, balanced=balanced)
+    d = dev_inputs(x)
+    fkv.fkv_compress_static(layer.shape, layer.heads, d["K_hist"], d["V_hist"], x.frame_slot, layer.Kc, layer.Vc,
+                            layer.kv_len)
+    O_ref = torch.full_like(d["Q"], 7.0)
+    l_ref = torch.full((cfg.n_heads, cfg.lq), -3.0, dtype=torch.float32, device="cuda")
+    fkv.fkv_chunk_attention_heads(layer.shape, static, d["Q"], layer.Kc, layer.Vc, layer.kv_len, d["K_cur"],
+                                  d["V_cur"], layer.scale, O_ref, l_ref, layer.attn_workspace)
+    O = torch.full_like(d["Q"], 7.0)
+    lse = torch.full((cfg.n_heads, cfg.lq), -3.0, dtype=torch.float32, device="cuda")
+    fkv.fkv_chunk_attention_static(layer.shape, layer.heads, d["K_hist"], d["V_hist"], x.frame_slot, d["Q"],
+                                   d["K_cur"], d["V_cur"], layer.scale, O, lse, layer.attn_workspace)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(from_dev(O), from_dev(O_ref))
+    np.testing.assert_array_equal(from_dev(lse).view(np.uint32), from_dev(l_ref).view(np.uint32))
+    ref = oracle.run_layer(cfg, x, rows=rows, scale=layer.scale)
+    Of, lf = from_dev(O), from_dev(lse)
+    for h in range(cfg.n_heads):
+        if h in static:
             one = oracle.LayerResult(None, None, None, None, None, None, ref.rows, ref.O[h:h + 1], ref.lse[h:h + 1])
             assert_attention_close(O[h:h + 1], one, "bf16", lse[h:h + 1])
         else:
@@ -545,7 +607,7 @@ def test_gpu_rollout_with_rolling_cache():
         layer.step(K_g, V_g, slots, Q_d, Kq_d, Vq_d, O, lse)
         torch.cuda.synchronize()
         ref = oracle.run_layer(cfg, x, scale=1 / math.sqrt(d))
-        assert_compression_exact(cfg, layer, ref)
+        assert_compression_exact(cfg, layer, ref, skip_static=layer.static_in_place)
         assert_attention_close(O, ref, "bf16", lse)
         dst = W.chunk_write_slots(i, C, window)
         fkv.fkv_append_frames(layer.shape, Kq_d, Vq_d, dst.tolist(), K_g, V_g)
@@ -665,9 +727,10 @@ def test_rollout_stack(pooled, incremental):
                 x = W.LayerInputs(cfg, K_o[layer], V_o[layer], Kq, Vq, Q, slots)
                 scores, kept = stack.views(H)
                 got = SimpleNamespace(kv_len=stack.kv_len, scores=scores, kept_seg=kept, Kc=stack.Kc, Vc=stack.Vc)
+                assert stack.static_in_place   # static heads attended in place: Kc/Vc rows not written
                 if row is None:
                     ref = oracle.run_layer(cfg, x, scale=1 / math.sqrt(d))
-                    assert_compression_exact(cfg, got, ref)
+                    assert_compression_exact(cfg, got, ref, skip_static=True)
                 else:
                     ref = oracle.run_layer(cfg, x, scale=1 / math.sqrt(d), attention=False)
                     kept_d, kv_d = from_dev(kept), from_dev(stack.kv_len)
@@ -679,14 +742,12 @@ def test_rollout_stack(pooled, incremental):
                             np.testing.assert_array_equal(kept_d[h], want)
                             kc = oracle.compact_head(K_o[layer][h], slots, want[:cnt], H, L)
                             vc = oracle.compact_head(V_o[layer][h], slots, want[:cnt], H, L)
-                        else:
-                            kc, vc = ref.Kc[h], ref.Vc[h]
-                        assert int(kv_d[h]) == kc.shape[0]
-                        np.testing.assert_array_equal(Kc_d[h, :kc.shape[0]], kc)
-                        np.testing.assert_array_equal(Vc_d[h, :vc.shape[0]], vc)
+                            assert int(kv_d[h]) == kc.shape[0]
+                            np.testing.assert_array_equal(Kc_d[h, :kc.shape[0]], kc)
+                            np.testing.assert_array_equal(Vc_d[h, :vc.shape[0]], vc)
                     rows = np.arange(C * F, dtype=np.int32)
-                    Kc_l = [Kc_d[h, :int(kv_d[h])] for h in range(nh)]
-                    Vc_l = [Vc_d[h, :int(kv_d[h])] for h in range(nh)]
+                    Kc_l = [Kc_d[h, :int(kv_d[h])] if b.type == W.DYNAMIC else ref.Kc[h] for h, b in enumerate(heads)]
+                    Vc_l = [Vc_d[h, :int(kv_d[h])] if b.type == W.DYNAMIC else ref.Vc[h] for h, b in enumerate(heads)]
                     att = [oracle.attention_rows(Q[h], Kc_l[h], Vc_l[h], Kq[h], Vq[h], 1 / math.sqrt(d), rows)
                            for h in range(nh)]
                     ref = oracle.LayerResult(None, None, None, None, None, None, rows,
