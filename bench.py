@@ -97,6 +97,7 @@ def cpu_baseline(cfg, x, rows_per_head):
     unit (the attention time is multiplied by Lq / rows_per_head)."""
     import numpy as np
     import oracle
+    import workloads as W
     oracle.lib()
     rng = np.random.default_rng(0)
     rows = np.sort(rng.choice(cfg.lq, size=min(rows_per_head, cfg.lq), replace=False)).astype(np.int32)
@@ -108,6 +109,21 @@ def cpu_baseline(cfg, x, rows_per_head):
         oracle.attention_rows(x.Q[h], res.Kc[h], res.Vc[h], x.K_cur[h], x.V_cur[h], scale, rows)
     t2 = time.perf_counter()
     per_unit_s = (t1 - t0) + (t2 - t1) * cfg.lq / len(rows)
+    # the tiny fp32 configuration in full on one thread, for reference
+    threads = oracle.max_threads()
+    tiny = W.tiny_config()
+    xt = W.make_layer_inputs(tiny, seed=0)
+    oracle.set_threads(1)
+    t3 = time.perf_counter()
+    oracle.run_layer(tiny, xt)
+    t4 = time.perf_counter()
+    oracle.set_threads(threads)
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
     return {
         "value": round(per_unit_s * 1e3, 1),
         "unit": "ms",
@@ -117,6 +133,10 @@ def cpu_baseline(cfg, x, rows_per_head):
                    f"({t1 - t0:.2f} s) + attention of {len(rows)} of {cfg.lq} query rows per head "
                    f"({t2 - t1:.2f} s), attention scaled x{cfg.lq / len(rows):.1f} to one unit"),
         "measured_s": round(t2 - t0, 2),
+        "cpu_model": cpu_model,
+        "nproc": os.cpu_count(),
+        "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+        "tiny_f32_unit_1thread_ms": round((t4 - t3) * 1e3, 2),
     }
 
 

@@ -79,6 +79,8 @@ def lib():
         L.fkvo_attention_mass.restype = None
         L.fkvo_max_threads.argtypes = []
         L.fkvo_max_threads.restype = I
+        L.fkvo_set_threads.argtypes = [I]
+        L.fkvo_set_threads.restype = None
         _lib = L
     return _lib
 
@@ -103,6 +105,11 @@ def _c(a, dtype=None):
 
 def max_threads() -> int:
     return lib().fkvo_max_threads()
+
+
+def set_threads(n: int) -> None:
+    """Threads of the oracle's OpenMP regions (timing only)."""
+    lib().fkvo_set_threads(int(n))
 
 
 # ---------------------------------------------------------------------------

@@ -30,6 +30,14 @@ static double load_elem(const void *base, int dtype, size_t i) {
     return (double)((const float *)base)[i];
 }
 
+void fkvo_set_threads(int n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 int fkvo_max_threads(void) {
 #ifdef _OPENMP
     return omp_get_max_threads();

@@ -99,6 +99,9 @@ void fkvo_attention_mass(int dtype, int d, long kv_len, long Lq, int F, const vo
 
 /* Number of OpenMP threads a parallel region would use. */
 int fkvo_max_threads(void);
+/* Threads of the following parallel regions (timing only; results do not
+ * depend on it). */
+void fkvo_set_threads(int n);
 
 #ifdef __cplusplus
 }

@@ -5,7 +5,9 @@
 // history, then the current chunk) and likewise for values; every query row of
 // the chunk attends to all of it with no mask.  The per-head key count is
 // ragged (it comes from the device-side kv_len), and one key tile may straddle
-// the history/chunk boundary.
+// the history/chunk boundary.  The PAGED instantiation attends static heads in
+// place: their retained history is the kept frames of Eq. 2 read straight from
+// the slot-permuted cache (load_tile_paged), with no compressed copy.
 //
 // Workgroup = 8 waves = 256 query rows of one head (32 per wave), in two
 // groups of four waves; one workgroup fills a CU.  Keys are processed in tiles
