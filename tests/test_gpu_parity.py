@@ -221,7 +221,7 @@ def test_attention_heads_subset(balanced):
 _PERM = np.array([3, 0, 8, 1, 5, 2, 7], np.int32)
 
 
-@pytest.mark.parametrize("case", ["F100-d128", "F64-d64-per-item", "F80-budgets", "H0", "H2", "480p"])
+@pytest.mark.parametrize("case", ["F100-d128", "F64-d64-per-item", "F80-budgets", "H0", "H2", "480p", "1080p"])
 def test_attention_static_in_place(case):
     """fkv_chunk_attention_static reads the static heads' kept frames straight
     from the slot-permuted cache: bit for bit what fkv_compress_static followed
@@ -248,8 +248,9 @@ def test_attention_static_in_place(case):
             W.HeadBudget(W.STATIC, 3, 4), W.HeadBudget(W.DYNAMIC, 1, 0, 1, W.SCOPE_FRAME),
             W.HeadBudget(W.STATIC, 0, 1))), np.array([2, 0], np.int32)
     else:
-        cfg, slot = W.wan_layer_config("480p"), None
-        rows = sample_rows(cfg.lq, 8, seed=33)
+        cfg = W.wan_layer_config(case)
+        slot = np.roll(np.arange(cfg.hist_frames, dtype=np.int32), 5)    # a rotated ring
+        rows = sample_rows(cfg.lq, 8 if case == "480p" else 4, seed=33)
     x = W.make_layer_inputs(cfg, seed=33, frame_slot=slot)
     _print_case("attention-static-in-place", case=case, balanced=balanced)
     static = [h for h, b in enumerate(cfg.heads) if b.type == W.STATIC]
