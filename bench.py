@@ -316,6 +316,7 @@ def main():
         del layers, base
         torch.cuda.empty_cache()
         out["rollout_480p"] = {"per_layer_scoring": measure_rollout(pooled=False),
+                               "per_layer_incremental_rescoring": measure_rollout(pooled=False, incremental=True),
                                "pooled_first_block_proxy": measure_rollout(pooled=True)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, x, args.cpu_rows)
