@@ -435,6 +435,28 @@ def test_determinism():
     np.testing.assert_array_equal(from_dev(a[2]), from_dev(b[2]))
 
 
+def test_determinism_pipelined_step():
+    """The two-stream step (static heads in place on a side stream) gives the
+    same bits on repeated runs: the streams touch disjoint heads, each has its
+    own workspace, and nothing depends on how they interleave."""
+    cfg = W.wan_layer_config("480p")
+    _print_case("determinism-pipelined")
+    x = W.make_layer_inputs(cfg, seed=13)
+    d = dev_inputs(x)
+    layer = make_layer(cfg)
+    assert layer.static_in_place and layer.side is not None
+    outs = []
+    for _ in range(3):
+        O = torch.empty_like(d["Q"])
+        lse = torch.empty((cfg.n_heads, cfg.lq), dtype=torch.float32, device="cuda")
+        layer.step(d["K_hist"], d["V_hist"], x.frame_slot, d["Q"], d["K_cur"], d["V_cur"], O, lse)
+        torch.cuda.synchronize()
+        outs.append((from_dev(O), from_dev(lse), from_dev(layer.scores), from_dev(layer.kept_seg)))
+    for run in outs[1:]:
+        for a, b in zip(run, outs[0]):
+            np.testing.assert_array_equal(a.view(np.uint8), b.view(np.uint8))
+
+
 def test_api_errors_on_gpu():
     """Host-side validation rejects a short slab before anything runs."""
     import paper_2605_09681_amd as fkv
