@@ -286,8 +286,8 @@ fkv_status fkv_chunk_attention_heads(const fkv_shape *shape, const int32_t *head
 
 /* Chunk attention of the static heads (Eq. 2) read in place from the cache:
  * for every head with heads[h].type == FKV_STATIC, the keys are the tokens of
- * its kept history frames -- the first min(sink, H) frames and the last
- * min(recent, H - sink) frames in logical order, logical frame t in slot
+ * its kept history frames -- logical frames [0, min(sink, H)) U
+ * [max(H - recent, 0), H) in ascending order, logical frame t in slot
  * frame_slot[t] of K_hist [n_heads][cap_frames][F][d] -- followed by
  * K_cur[h], and likewise for the values.  This is exactly what
  * fkv_compress_static followed by fkv_chunk_attention_heads over the static
