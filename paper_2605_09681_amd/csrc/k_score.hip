@@ -40,12 +40,18 @@ namespace {
 
 constexpr int kThreads = kScoreThreads;
 constexpr int kWaves = kScoreWaves;
-constexpr int kDepth = 8;  // frames in flight per thread
+// Frames in flight per thread.  Four keep the pass within 64 VGPRs (the
+// launch bound below), so its waves fit on a CU next to the two 224-VGPR
+// waves per SIMD of a running attention workgroup: in the two-stream layer
+// step the scoring of the dynamic heads then runs beside the static heads'
+// attention instead of waiting for CUs (8 frames took 88 VGPRs).
+constexpr int kDepth = 4;
 // Frames per part when a long range is split over several workgroup columns:
 // more waves in flight per CU hide the fp64 products and reductions behind the
 // loads.  At 480P (22 frames) 6-frame parts (4 columns, 3 frames read twice)
-// took the partials pass from 19.0 to 16.7 us; 11- and 8-frame parts gave 17.6
-// and 17.8 us.
+// took the partials pass from 19.0 to 16.7 us with 8 frames in flight (11- and
+// 8-frame parts: 17.6 and 17.8 us); with 4 in flight 4-, 6-, 8- and 11-frame
+// parts are within 3% of each other.
 #ifndef FKV_SCORE_PART_FRAMES
 #define FKV_SCORE_PART_FRAMES 6
 #endif
@@ -115,7 +121,7 @@ __device__ __forceinline__ int64_t stats_index(const ScoreArgs &a, int li, int t
 }
 
 template <bool F32>
-__global__ __launch_bounds__(kThreads) void score_partials_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(kThreads, 8) void score_partials_kernel(ScoreArgs a) {
     using V = Vec<F32>;
     const int c = blockIdx.x, u = blockIdx.y, li = blockIdx.z / a.n_parts, part = blockIdx.z % a.n_parts;
     const int h = a.heads.head[li];
