@@ -49,28 +49,67 @@ struct Schedule {
     __device__ __forceinline__ int owner(int64_t x) const { return (int)(((x + 1) * G - 1) / total); }
 };
 
-// The item holding tile x of the concatenated sequence: list entry li, its
-// query tile qt, the item's first tile ibase and its tile count T.
+// The launch's work list as one wave sees it: lane l < heads.n holds the key
+// tile count T of list entry l and the inclusive prefix sum of n_qtiles * T
+// over entries 0..l; lanes past the list repeat the total.  One vector load of
+// the entries' lengths and a wave scan, instead of a chain of dependent scalar
+// loads (one per entry, each a full memory latency) at the start of every
+// workgroup.
+struct WorkList {
+    int T;
+    int64_t incl;
+};
+
+__device__ __forceinline__ int64_t readlane64(int64_t v, int l) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), l);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+template <bool PAGED = false>
+__device__ __forceinline__ WorkList work_list(const AttnArgs &a) {
+    const int lane = threadIdx.x & 63;
+    // entry l's head (or kept-frame count) into lane l, with uniform indices
+    // into the launch arguments (a per-lane index would copy them to private
+    // memory)
+    int e = 0;
+    for (int l = 0; l < a.heads.n; ++l)
+        if (lane == l) e = PAGED ? a.st_kept[l] : a.heads.head[l];
+    int T = 0;
+    if (lane < a.heads.n) {
+        const int kvl = PAGED ? e * a.F : head_kvl(a, e);
+        T = (kvl + a.Lq + BN - 1) / BN;
+    }
+    long long v = (long long)a.n_qtiles * T;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const long long u = __shfl_up(v, d, 64);
+        if (lane >= d) v += u;
+    }
+    return WorkList{T, (int64_t)v};
+}
+
+// Tiles of all items before entry li.
+__device__ __forceinline__ int64_t entry_base(const WorkList &wl, int li) {
+    return li > 0 ? readlane64(wl.incl, li - 1) : 0;
+}
+
+// The item holding tile x (0 <= x < total) of the concatenated sequence: list
+// entry li, its query tile qt, the item's first tile ibase and its tile count T.
 struct ItemPos {
     int li, qt, T;
     int64_t ibase;
 };
-template <bool PAGED = false>
-__device__ __forceinline__ ItemPos locate(const AttnArgs &a, int64_t x) {
-    int li = 0, T = entry_tiles<PAGED>(a, 0);
-    int64_t base = 0;
-    while (x >= base + (int64_t)a.n_qtiles * T) {
-        base += (int64_t)a.n_qtiles * T;
-        T = entry_tiles<PAGED>(a, ++li);
-    }
+__device__ __forceinline__ ItemPos locate(const WorkList &wl, int64_t x) {
+    const int li = (int)__builtin_ctzll(__ballot(wl.incl > x));   // first entry ending past x
+    const int64_t base = entry_base(wl, li);
+    const int T = __builtin_amdgcn_readlane(wl.T, li);
     const int qt = (int)((x - base) / T);
     return ItemPos{li, qt, T, base + (int64_t)qt * T};
 }
 
-template <bool PAGED = false>
-__device__ __forceinline__ Schedule make_schedule(const AttnArgs &a) {
-    int64_t total = 0;
-    for (int li = 0; li < a.heads.n; ++li) total += (int64_t)a.n_qtiles * entry_tiles<PAGED>(a, li);
+__device__ __forceinline__ Schedule make_schedule(const AttnArgs &a, const WorkList &wl) {
+    const int64_t total = readlane64(wl.incl, 63);
     Schedule sc;
     sc.total = total;
     sc.G = (int)(total < a.n_blocks ? total : a.n_blocks);

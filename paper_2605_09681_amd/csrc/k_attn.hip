@@ -500,7 +500,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
         attn_segment<D, PAGED>(a, Ks, Vs, li, item - li * a.n_qtiles, 0, entry_tiles<PAGED>(a, li), 0, nullptr);
         return;
     }
-    const Schedule sc = make_schedule<PAGED>(a);
+    const WorkList wl = work_list<PAGED>(a);
+    const Schedule sc = make_schedule(a, wl);
     const int r = (blockIdx.x & 7) * (a.n_blocks >> 3) + (blockIdx.x >> 3);
     if (r >= sc.G) return;
     const int64_t end = sc.start(r + 1);
@@ -508,7 +509,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     bool first = true;
     while (cur < end) {
         // locate the item holding tile `cur`
-        const ItemPos ip = locate<PAGED>(a, cur);
+        const ItemPos ip = locate(wl, cur);
         const int qt = ip.qt, T = ip.T;
         const int64_t ibase = ip.ibase;
         const int t0 = (int)(cur - ibase);
@@ -540,11 +541,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     const int item = blockIdx.x, w = blockIdx.y;
     const int li = item / a.n_qtiles, qt = item - li * a.n_qtiles;
     const int h = a.heads.head[li];
-    const Schedule sc = make_schedule<PAGED>(a);
-    int64_t P = 0;
-    for (int l = 0; l < li; ++l) P += (int64_t)a.n_qtiles * entry_tiles<PAGED>(a, l);
-    const int T = entry_tiles<PAGED>(a, li);
-    P += (int64_t)qt * T;
+    const WorkList wl = work_list<PAGED>(a);
+    const Schedule sc = make_schedule(a, wl);
+    const int T = __builtin_amdgcn_readlane(wl.T, li);
+    const int64_t P = entry_base(wl, li) + (int64_t)qt * T;
     const int b0 = sc.owner(P), b1 = sc.owner(P + T - 1);
     if (b0 == b1) return;
     // the item is b0's last segment unless b0's range starts with it, and the

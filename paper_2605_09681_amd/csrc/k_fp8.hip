@@ -636,14 +636,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fp8_kernel(AttnArgs a) {
         fp8_segment<D>(a, Ks, Vs, h, item - li * a.n_qtiles, 0, head_tiles(a, h), 0, nullptr);
         return;
     }
-    const Schedule sc = make_schedule(a);
+    // (the work list is rebuilt per segment rather than kept live: this kernel
+    // has no VGPRs to spare across the segment)
+    const Schedule sc = make_schedule(a, work_list(a));
     const int r = (blockIdx.x & 7) * (a.n_blocks >> 3) + (blockIdx.x >> 3);
     if (r >= sc.G) return;
     const int64_t end = sc.start(r + 1);
     int64_t cur = sc.start(r);
     bool first = true;
     while (cur < end) {
-        const ItemPos ip = locate(a, cur);
+        const ItemPos ip = locate(work_list(a), cur);
         const int h = a.heads.head[ip.li], qt = ip.qt, T = ip.T;
         const int64_t ibase = ip.ibase;
         const int t0 = (int)(cur - ibase);
