@@ -221,7 +221,8 @@ def test_attention_heads_subset(balanced):
 _PERM = np.array([3, 0, 8, 1, 5, 2, 7], np.int32)
 
 
-@pytest.mark.parametrize("case", ["F100-d128", "F64-d64-per-item", "F80-budgets", "H0", "H2", "480p", "1080p"])
+@pytest.mark.parametrize("case", ["F100-d128", "F64-d64-per-item", "F80-budgets", "H0", "H2", "H200-cap256", "480p",
+                                  "1080p"])
 def test_attention_static_in_place(case):
     """fkv_chunk_attention_static reads the static heads' kept frames straight
     from the slot-permuted cache: bit for bit what fkv_compress_static followed
@@ -243,6 +244,13 @@ def test_attention_static_in_place(case):
             W.HeadBudget(S, 0, 0), W.HeadBudget(S, 3, 3), W.HeadBudget(S, 0, 1)))
     elif case == "H0":
         cfg, slot = _small(F=100, L=25, H=0, cap=4, d=64), np.zeros(0, np.int32)
+    elif case == "H200-cap256":
+        # more than 64 kept frames: slot bytes 1..3 of the lane table
+        S, D = W.STATIC, W.DYNAMIC
+        cfg = _small(F=64, L=32, H=200, cap=256, C=2, d=64, heads=(
+            W.HeadBudget(S, 2, 190), W.HeadBudget(D, 1, 0, 1, W.SCOPE_FRAME), W.HeadBudget(S, 0, 200),
+            W.HeadBudget(S, 70, 60)))
+        slot = np.random.default_rng(7).permutation(256)[:200].astype(np.int32)
     elif case == "H2":
         cfg, slot = _small(F=72, L=24, H=2, cap=3, d=64, heads=(
             W.HeadBudget(W.STATIC, 3, 4), W.HeadBudget(W.DYNAMIC, 1, 0, 1, W.SCOPE_FRAME),
