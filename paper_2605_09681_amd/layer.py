@@ -227,14 +227,14 @@ class RolloutStack:
     chunk's frames back with :meth:`append`.  Layers run one after another, so
     they share one set of compressed-cache buffers, sized for a full window;
     the history length H = len(frame_slot) may grow from chunk to chunk (0 on
-    the first one).  Per layer and AR step :meth:`run_layer` makes the four
-    C-ABI calls (the static gather on a side stream next to the dynamic heads'
-    scoring and compaction; for bf16 and frames of at least 64 tokens the
-    static heads are attended in place, with no gather), or -- with a shared
-    score row from
-    :meth:`score_pooled` -- the first-block proxy of Sec. 4.3: one similarity
-    row computed from one layer's keys pooled over all heads and reused by the
-    dynamic heads of every layer.  ``budgets`` are per-head objects with
+    the first one).  Per layer and AR step :meth:`run_layer` runs the static
+    heads' attention on a side stream (read in place from the cache for bf16
+    and frames of at least 64 tokens, else gathered first) next to the
+    dynamic heads' scoring, compaction and attention, or -- with a shared
+    score row from :meth:`score_pooled` -- the first-block proxy of Sec. 4.3:
+    the dynamic heads of every layer select with one similarity row computed
+    from one layer's keys pooled over all heads.  ``budgets`` are per-head
+    objects with
     type/sink_frames/recent_frames/keep_k/scope for the given H.
 
     Incremental rescoring: :meth:`history` stores a layer's per-frame
