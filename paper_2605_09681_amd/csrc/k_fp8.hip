@@ -619,7 +619,7 @@ __device__ __forceinline__ void fp8_segment(const AttnArgs &a, uint8_t (&Ks)[2][
                                 o[mb][4 * g + 2] * w.z * inv, o[mb][4 * g + 3] * w.w * inv);
             }
         if (a.lse && hl == 0)
-            a.lse[(size_t)h * Lq + qrow] = (m_run - kPBias) * 0.69314718055994530942f + logf(l_tot);
+            a.lse[(size_t)h * Lq + qrow] = fmaf(m_run - kPBias, 0.69314718055994530942f, logf(l_tot));
     }
 }
 
