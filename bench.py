@@ -299,6 +299,11 @@ def main():
             "compress_static": round(static_copy_bytes / (static_ms * 1e-3) / 1e9, 1),
             "peak": PEAK_HBM_GBS,
         },
+        "breakdown_frac_of_hbm_peak": {
+            "score_segments": round(score_bytes / (score_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 3),
+            "select_compact": round(dyn_copy_bytes / (select_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 3),
+            "compress_static": round(static_copy_bytes / (static_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 3),
+        },
         "breakdown_ms_p10_p50_p90": {
             k: [round(float(p10[j]), 4), round(float(p50[j]), 4), round(float(p90[j]), 4)]
             for j, k in enumerate(("score_segments", "select_compact", "compress_static", "chunk_attention"))},
