@@ -636,16 +636,35 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fp8_kernel(AttnArgs a) {
         fp8_segment<D>(a, Ks, Vs, h, item - li * a.n_qtiles, 0, head_tiles(a, h), 0, nullptr);
         return;
     }
-    // (the work list is rebuilt per segment rather than kept live: this kernel
-    // has no VGPRs to spare across the segment)
-    const Schedule sc = make_schedule(a, work_list(a));
+    // The schedule walks the head list entry by entry (dependent scalar loads)
+    // rather than building the wave-parallel work list of attn_common.h: at
+    // 252 VGPRs this kernel has none to spare, and the work list cost it a
+    // private segment for no measured gain.
+    auto tiles = [&](int l) { return head_tiles(a, a.heads.head[l]); };
+    Schedule sc;
+    {
+        int64_t total = 0;
+        for (int l = 0; l < a.heads.n; ++l) total += (int64_t)a.n_qtiles * tiles(l);
+        sc.total = total;
+        sc.G = (int)(total < a.n_blocks ? total : a.n_blocks);
+    }
     const int r = (blockIdx.x & 7) * (a.n_blocks >> 3) + (blockIdx.x >> 3);
     if (r >= sc.G) return;
     const int64_t end = sc.start(r + 1);
     int64_t cur = sc.start(r);
     bool first = true;
     while (cur < end) {
-        const ItemPos ip = locate(work_list(a), cur);
+        ItemPos ip;  // the item holding tile `cur`
+        {
+            int li = 0, T = tiles(0);
+            int64_t base = 0;
+            while (cur >= base + (int64_t)a.n_qtiles * T) {
+                base += (int64_t)a.n_qtiles * T;
+                T = tiles(++li);
+            }
+            const int qt = (int)((cur - base) / T);
+            ip = ItemPos{li, qt, T, base + (int64_t)qt * T};
+        }
         const int h = a.heads.head[ip.li], qt = ip.qt, T = ip.T;
         const int64_t ibase = ip.ibase;
         const int t0 = (int)(cur - ibase);
