@@ -162,7 +162,7 @@ def test_480p_many_segments():
     check_layer(cfg, x, rows=sample_rows(cfg.lq, 8, seed=15))
 
 
-@pytest.mark.parametrize("case", ["small", "small-d64", "small-f32", "480p", "480p-gather"])
+@pytest.mark.parametrize("case", ["small", "small-d64", "small-f32", "480p", "480p-gather", "1080p"])
 def test_pipelined_step(case):
     """CompressedLayer.step: the static heads' attention on a side stream --
     read in place from the cache (bf16), or gathered first (fp32, and the
@@ -174,9 +174,10 @@ def test_pipelined_step(case):
         x = W.make_layer_inputs(cfg, seed=30, frame_slot=np.array([3, 0, 8, 1, 5, 2, 7], np.int32))
         rows = None
     else:
-        cfg = W.wan_layer_config("480p")
-        x = W.make_layer_inputs(cfg, seed=31)
-        rows = sample_rows(cfg.lq, 8, seed=31)
+        cfg = W.wan_layer_config("1080p" if case == "1080p" else "480p")
+        slot = np.roll(np.arange(cfg.hist_frames, dtype=np.int32), 3) if case == "1080p" else None
+        x = W.make_layer_inputs(cfg, seed=31, frame_slot=slot)
+        rows = sample_rows(cfg.lq, 8 if case != "1080p" else 4, seed=31)
     _print_case("pipelined-step", case=case)
     layer = make_layer(cfg, in_place=False if case == "480p-gather" else None)
     assert layer.side is not None and (cfg.dtype == "f32" or layer.attn_workspace2 is not None)
