@@ -480,6 +480,34 @@ def test_api_errors_on_gpu():
     assert e.value.status == fkv.FKV_ERR_CAPACITY
 
 
+def test_attention_workspace_capacity_on_gpu():
+    """A balanced-schedule workspace one byte short is rejected before any
+    launch by every bf16 attention entry point, the in-place static one
+    included; the output is left untouched."""
+    import paper_2605_09681_amd as fkv
+    cfg = _small(F=100, L=25, d=64)
+    x = W.make_layer_inputs(cfg, seed=3, frame_slot=_PERM)
+    layer = make_layer(cfg)
+    d = dev_inputs(x)
+    need = fkv.fkv_attention_workspace_size(layer.shape)
+    short = torch.zeros(need - 1, dtype=torch.uint8, device="cuda")
+    O = torch.full_like(d["Q"], 5.0)
+    calls = (
+        lambda: fkv.fkv_chunk_attention(layer.shape, d["Q"], layer.Kc, layer.Vc, layer.kv_len, d["K_cur"],
+                                        d["V_cur"], layer.scale, O, workspace=short),
+        lambda: fkv.fkv_chunk_attention_heads(layer.shape, [0, 3], d["Q"], layer.Kc, layer.Vc, layer.kv_len,
+                                              d["K_cur"], d["V_cur"], layer.scale, O, workspace=short),
+        lambda: fkv.fkv_chunk_attention_static(layer.shape, layer.heads, d["K_hist"], d["V_hist"], x.frame_slot,
+                                               d["Q"], d["K_cur"], d["V_cur"], layer.scale, O, workspace=short),
+    )
+    for call in calls:
+        with pytest.raises(fkv.FkvError) as e:
+            call()
+        assert e.value.status == fkv.FKV_ERR_CAPACITY
+    torch.cuda.synchronize()
+    assert (W.bf16_bits_to_f32(from_dev(O)) == 5.0).all()
+
+
 # ---------------------------------------------------------------------------
 # streaming rollout with a ring-buffer cache (sampled units)
 # ---------------------------------------------------------------------------
