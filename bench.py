@@ -328,6 +328,16 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+_pair_counter = [0]
+
+
+def _next_pair(layers, bufs):
+    """The next (layer, buffers) copy in rotation."""
+    i = _pair_counter[0] % len(layers)
+    _pair_counter[0] += 1
+    return layers[i], bufs[i]
+
+
 def _time_ms(fn, reps, stream):
     """Mean ms of fn() over reps launches, HIP events on the launch stream."""
     import torch
@@ -369,6 +379,35 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
                          stream)
     n_dyn = sum(1 for t in L0.types if t == W.DYNAMIC)
 
+    # where the two-stream step's time goes: each attention launch alone, the
+    # one 12-head launch, and the step without the dynamic compression (its
+    # attention then reads the compacted cache of the previous step)
+    def rot(fn):
+        return lambda: fn(*_next_pair(layers, bufs))
+
+    def static_only(L, bb):
+        L.attention_static(bb["K_hist"], bb["V_hist"], x.frame_slot, bb["Q"], bb["K_cur"], bb["V_cur"], bb["O"],
+                           None, L.attn_workspace)
+
+    def dynamic_only(L, bb):
+        fkv.fkv_chunk_attention_heads(L.shape, L.dynamic_heads, bb["Q"], L.Kc, L.Vc, L.kv_len, bb["K_cur"],
+                                      bb["V_cur"], L.scale, bb["O"], None, L.attn_workspace)
+
+    def all_heads(L, bb):
+        L.attention(bb["Q"], bb["K_cur"], bb["V_cur"], bb["O"])
+
+    def step_nocomp(L, bb):
+        main = torch.cuda.current_stream()
+        L.side.wait_stream(main)
+        with torch.cuda.stream(L.side):
+            static_only(L, bb)
+        dynamic_only(L, bb)
+        main.wait_stream(L.side)
+
+    parts = {name: round(_time_ms(rot(fn), 50, stream), 4)
+             for name, fn in (("static_heads_in_place_ms", static_only), ("dynamic_heads_ms", dynamic_only),
+                              ("all_heads_one_launch_ms", all_heads), ("step_without_compression_ms", step_nocomp))}
+
     O8 = torch.empty_like(b["Q"])
     pack_ms = _time_ms(lambda: L0.pack_fp8(b["Q"], b["K_cur"], b["V_cur"]), 20, stream)
     fp8_ms = _time_ms(lambda: L0.attention_fp8_packed(O8), 20, stream)
@@ -404,6 +443,8 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
     del L10, Kh, Vh, Kq, Vq, Q10, O10
 
     return {
+        "step_parts_480p": dict(parts, note="each timed alone over the rotated buffer copies; the step runs the "
+                                          "first two on two streams after the dynamic compression"),
         "unit_1080p": {
             "ms": round(unit10_ms, 3), "attention_ms": round(att10_ms, 3),
             "attention_TFLOP_s": round(flop10 / (att10_ms * 1e-3) / 1e12, 1),
