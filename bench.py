@@ -1,9 +1,9 @@
 """Benchmark of the Forcing-KV hot path on one MI355X.
 
 One step = one AR step of one attention layer (a "unit"): segment scoring and
-BottomK selection + compaction for the dynamic heads, structural gather for
-the static heads, then chunk attention of all heads over their compressed
-caches -- the four C-ABI calls, on the 480P Wan-1.3B-style layer (12 heads,
+BottomK selection + compaction for the dynamic heads, the static heads'
+structural pruning, then chunk attention of all heads over their compressed
+caches -- the C-ABI calls, on the 480P Wan-1.3B-style layer (12 heads,
 d = 128, 1560 tokens/frame, 21-frame history, 3-frame chunk, heads 0-5 static
 with sink + 6 recent frames, heads 6-11 dynamic with sink + 10 of 20 frames).
 
@@ -12,15 +12,16 @@ rotates through several independent copies of the layer's buffers (as the
 layers of a real rollout would), so a step never finds its cache in the
 256 MB last-level cache from the previous step.
 
-Prints ONE JSON line (see the keys below).  `value` is the wall-clock ms per
-step over the timed steps (lower is better); in the timed step the static
-heads' attention -- read in place from the cache, no gather -- runs on a side
-stream while the dynamic heads are scored, compacted and attended on the main
-stream (they touch disjoint heads).  The per-stage breakdown comes from a
-second pass that runs the four calls one after another with HIP events
-between them.  `roofline` covers the dominant
-kernel (chunk attention, MFMA-bound) timed with HIP events on the stream the
-kernels run on.  `cpu_baseline` times the CPU oracle on the host cores on a
+Prints ONE JSON line.  `value` is the wall-clock ms per step (one layer, one
+AR step) over the timed steps, lower is better.  The timed step is the layer
+driver's step (CompressedLayer.step): the static heads' attention -- read in
+place from the cache, no gather -- on a side stream while the dynamic heads
+are scored, compacted and attended on the main stream.  Before the timed
+steps a serial pass of the four calls with HIP events between them gives the
+per-stage breakdown (and brings the clock up).  During the timed steps HIP
+events on each launch's own stream time every attention launch the step
+makes; `roofline` reports the longest of them (MFMA-bound), `roofline_launches`
+all of them.  `cpu_baseline` times the CPU oracle on the host cores on a
 bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -38,6 +39,7 @@ if ROOT not in sys.path:
 
 METRIC = "ms per AR chunk (score+compact+attn) and attn TFLOP/s, 480P/1080P shapes"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0      # MI355X dense FP8 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
@@ -49,7 +51,9 @@ def parse():
     p.add_argument("--resolution", default="480p", choices=["480p", "1080p"])
     p.add_argument("--copies", type=int, default=4, help="independent layer buffers rotated per step")
     p.add_argument("--cpu-rows", type=int, default=4680,
-                   help="query rows per head in the CPU oracle sample (4680 = every row at 480P)")
+                   help="query rows per head in the 480P CPU oracle sample (4680 = every row)")
+    p.add_argument("--cpu-rows-1080p", type=int, default=512,
+                   help="query rows per head in the 1080P CPU oracle sample (extrapolated to 24480)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--step", default="pipelined", choices=["pipelined", "serial"],
                    help="timed step: pipelined (static heads on a side stream) or the four calls "
@@ -58,9 +62,9 @@ def parse():
                    help="pipelined step: static heads attended in place from the cache, or gathered "
                         "into the compressed buffers first")
     p.add_argument("--no-rollout", action="store_true",
-                   help="skip the measured 30-layer x 4-step x 10-chunk rollout")
+                   help="skip the measured 30-layer x 4-step rollouts (10 and 60 chunks)")
     p.add_argument("--no-extras", action="store_true",
-                   help="skip the extra measurements (pooled proxy scoring, uncompressed attention)")
+                   help="skip the extra measurements (1080P, sweep, FP8, proxy, uncompressed attention)")
     p.add_argument("--schedule", default="balanced", choices=["balanced", "per-item"],
                    help="attention work schedule (balanced needs the attention workspace)")
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "attention_traffic.json"),
@@ -91,53 +95,234 @@ def to_dev(a, dtype):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def cpu_baseline(cfg, x, rows_per_head):
-    """Time the CPU oracle on the host cores: full compression of every head
-    and attention for a seeded sample of query rows per head, scaled to one
-    unit (the attention time is multiplied by Lq / rows_per_head)."""
+def host_bits(t):
+    """A bf16 device tensor as its uint16 bit pattern on the host."""
     import numpy as np
-    import oracle
+    import torch
+    return t.cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+def device_layer_inputs(cfg, seed):
+    """The layer's tensors generated on the device from a seed (the 1080P
+    cache is too large to draw quickly on the host): keys an AR(1) chain over
+    the H history frames and the chunk's frames (rho = 0.9, elementwise, fp32,
+    each frame rounded to bf16), values and queries N(0,1); logical frame t in
+    slot t."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    h, d, F, H, C = cfg.n_heads, cfg.head_dim, cfg.frame_tokens, cfg.hist_frames, cfg.chunk_frames
+    rho = 0.9
+    a = math.sqrt(1 - rho * rho)
+    K_hist = torch.empty(h, cfg.cap_frames, F, d, dtype=torch.bfloat16, device="cuda")
+    K_cur = torch.empty(h, C * F, d, dtype=torch.bfloat16, device="cuda")
+    k = torch.randn(h, F, d, device="cuda", generator=g)
+    for t in range(H + C):
+        if t > 0:
+            k = rho * k + a * torch.randn(h, F, d, device="cuda", generator=g)
+        if t < H:
+            K_hist[:, t] = k.to(torch.bfloat16)
+        else:
+            K_cur[:, (t - H) * F:(t - H + 1) * F] = k.to(torch.bfloat16)
+    V_hist = torch.randn(h, cfg.cap_frames, F, d, device="cuda", generator=g).to(torch.bfloat16)
+    V_cur = torch.randn(h, C * F, d, device="cuda", generator=g).to(torch.bfloat16)
+    Q = torch.randn(h, C * F, d, device="cuda", generator=g).to(torch.bfloat16)
+    return dict(K_hist=K_hist, V_hist=V_hist, K_cur=K_cur, V_cur=V_cur, Q=Q)
+
+
+def attention_flop(cfg, kv_len, heads=None):
+    """4 * Lq * d * (kv_len + Lq) summed over the given heads (QK^T and PV only)."""
+    idx = range(cfg.n_heads) if heads is None else heads
+    return float(sum(4.0 * cfg.lq * cfg.head_dim * (int(kv_len[h]) + cfg.lq) for h in idx))
+
+
+def static_kv_len(cfg, heads):
+    """Retained history tokens of every head whose kept set follows from its
+    budget alone (static heads: |kept frames| * F); None for dynamic heads."""
     import workloads as W
-    oracle.lib()
-    rng = np.random.default_rng(0)
-    rows = np.sort(rng.choice(cfg.lq, size=min(rows_per_head, cfg.lq), replace=False)).astype(np.int32)
-    t0 = time.perf_counter()
-    res = oracle.run_layer(cfg, x, attention=False)
-    t1 = time.perf_counter()
-    scale = 1.0 / math.sqrt(cfg.head_dim)
-    for h in range(cfg.n_heads):
-        oracle.attention_rows(x.Q[h], res.Kc[h], res.Vc[h], x.K_cur[h], x.V_cur[h], scale, rows)
-    t2 = time.perf_counter()
-    per_unit_s = (t1 - t0) + (t2 - t1) * cfg.lq / len(rows)
-    # the tiny fp32 configuration in full on one thread, for reference
-    threads = oracle.max_threads()
-    tiny = W.tiny_config()
-    xt = W.make_layer_inputs(tiny, seed=0)
-    oracle.set_threads(1)
-    t3 = time.perf_counter()
-    oracle.run_layer(tiny, xt)
-    t4 = time.perf_counter()
-    oracle.set_threads(threads)
-    cpu_model = ""
-    try:
-        with open("/proc/cpuinfo") as f:
-            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
-    except OSError:
-        pass
-    return {
-        "value": round(per_unit_s * 1e3, 1),
-        "unit": "ms",
-        "cores": oracle.max_threads(),
-        "kind": "oracle",
-        "sample": (f"fp64 C oracle: scoring+selection+compaction of all {cfg.n_heads} heads in full "
-                   f"({t1 - t0:.2f} s) + attention of {len(rows)} of {cfg.lq} query rows per head "
-                   f"({t2 - t1:.2f} s), attention scaled x{cfg.lq / len(rows):.1f} to one unit"),
-        "measured_s": round(t2 - t0, 2),
-        "cpu_model": cpu_model,
-        "nproc": os.cpu_count(),
-        "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
-        "tiny_f32_unit_1thread_ms": round((t4 - t3) * 1e3, 2),
+    H = cfg.hist_frames
+    out = []
+    for b in heads:
+        if b.type != W.STATIC:
+            out.append(None)
+            continue
+        a = min(b.sink_frames, H)
+        lo = max(H - b.recent_frames, 0)
+        out.append((H if lo <= a else a + (H - lo)) * cfg.frame_tokens)
+    return out
+
+
+def _time_ms(fn, reps, stream, warm=3):
+    """Mean ms of fn() over reps launches, HIP events on the launch stream."""
+    import torch
+    for _ in range(warm):
+        fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def staged_breakdown(layers, bufs, slots, reps, stream, warm=10):
+    """The four calls one after another on one stream with HIP events between
+    them, rotating over the buffer copies.  Returns [reps][4] ms (score,
+    select_compact, compress_static, attention)."""
+    import numpy as np
+    import torch
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(reps)]
+
+    def staged(i, e):
+        L, b = layers[i % len(layers)], bufs[i % len(layers)]
+        e[0].record(stream)
+        L.score(b["K_hist"], slots, b["K_cur"])
+        e[1].record(stream)
+        L.select_compact(b["K_hist"], b["V_hist"], slots)
+        e[2].record(stream)
+        L.compress_static(b["K_hist"], b["V_hist"], slots)
+        e[3].record(stream)
+        L.attention(b["Q"], b["K_cur"], b["V_cur"], b["O"])
+        e[4].record(stream)
+
+    for i in range(warm):
+        staged(i, ev[0])
+    torch.cuda.synchronize()
+    for i in range(reps):
+        staged(i, ev[i])
+    torch.cuda.synchronize()
+    return np.array([[e[j].elapsed_time(e[j + 1]) for j in range(4)] for e in ev])
+
+
+def stage_report(cfg, layer, stage_ms):
+    """Per-kernel ms, achieved GB/s (algorithmic bytes) and fraction of peak."""
+    import numpy as np
+    import workloads as W
+    kv = layer.kv_len.cpu().numpy().astype(np.int64)
+    d, e, F, H = cfg.head_dim, cfg.esize, cfg.frame_tokens, cfg.hist_frames
+    dyn = np.array([b.type == W.DYNAMIC for b in layer_budgets(layer)])
+    score_bytes = int(dyn.sum()) * (H + 1) * F * d * e
+    dyn_bytes = 4 * d * e * int(kv[dyn].sum())
+    st_bytes = 4 * d * e * int(kv[~dyn].sum())
+    flop = attention_flop(cfg, kv)
+    mean = stage_ms.mean(axis=0)
+    p10, p50, p90 = np.percentile(stage_ms, [10, 50, 90], axis=0)
+    names = ("score_segments", "select_compact", "compress_static", "chunk_attention")
+    gbs = lambda b, ms: b / (ms * 1e-3) / 1e9
+    rep = {
+        "ms": {k: round(float(mean[j]), 4) for j, k in enumerate(names)},
+        "ms_p10_p50_p90": {k: [round(float(p10[j]), 4), round(float(p50[j]), 4), round(float(p90[j]), 4)]
+                           for j, k in enumerate(names)},
+        "algorithmic_bytes": {"score_segments": score_bytes, "select_compact": dyn_bytes,
+                              "compress_static": st_bytes},
+        "GB_s": {"score_segments": round(gbs(score_bytes, mean[0]), 1),
+                 "select_compact": round(gbs(dyn_bytes, mean[1]), 1),
+                 "compress_static": round(gbs(st_bytes, mean[2]), 1)},
+        "frac_of_hbm_peak": {"score_segments": round(gbs(score_bytes, mean[0]) / PEAK_HBM_GBS, 3),
+                             "select_compact": round(gbs(dyn_bytes, mean[1]) / PEAK_HBM_GBS, 3),
+                             "compress_static": round(gbs(st_bytes, mean[2]) / PEAK_HBM_GBS, 3)},
+        "attention_algorithmic_flop": flop,
+        "attention_TFLOP_s": round(flop / (mean[3] * 1e-3) / 1e12, 1),
+        "attention_frac_of_bf16_peak": round(flop / (mean[3] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "serial_unit_ms": round(float(mean.sum()), 4),
     }
+    return rep
+
+
+def layer_budgets(layer):
+    import workloads as W
+    return [W.HeadBudget(int(h.type), int(h.sink_frames), int(h.recent_frames), int(h.keep_k), int(h.scope))
+            for h in layer.heads]
+
+
+def make_layers(cfg, n, args, budgets=None):
+    from paper_2605_09681_amd.layer import CompressedLayer
+    return [CompressedLayer(cfg.n_heads, cfg.head_dim, cfg.frame_tokens, cfg.hist_frames, cfg.cap_frames,
+                            cfg.chunk_frames, cfg.seg_tokens, cfg.dtype, cfg.heads if budgets is None else budgets,
+                            balanced=args.schedule == "balanced", in_place=args.static == "in_place")
+            for _ in range(n)]
+
+
+def timed_steps(cfg, layers, bufs, slots, args, mode):
+    """W warm-up steps, then exactly K timed steps bracketed by device
+    synchronisation; HIP events around every attention launch of the timed
+    steps, on the stream that launch runs on."""
+    import numpy as np
+    import torch
+    stream = torch.cuda.current_stream()
+    names = (("static_attention", "dynamic_attention") if mode == "pipelined" else ("attention",))
+    events = [{n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
+              for _ in range(args.steps)]
+
+    def step(i, ev=None):
+        L, b = layers[i % len(layers)], bufs[i % len(layers)]
+        if mode == "pipelined":
+            L.step(b["K_hist"], b["V_hist"], slots, b["Q"], b["K_cur"], b["V_cur"], b["O"], events=ev)
+            return
+        L.score(b["K_hist"], slots, b["K_cur"])
+        L.select_compact(b["K_hist"], b["V_hist"], slots)
+        L.compress_static(b["K_hist"], b["V_hist"], slots)
+        if ev is not None:
+            ev["attention"][0].record(stream)
+        L.attention(b["Q"], b["K_cur"], b["V_cur"], b["O"])
+        if ev is not None:
+            ev["attention"][1].record(stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, events[i])
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    launch_ms = {n: np.array([e[n][0].elapsed_time(e[n][1]) for e in events]) for n in names}
+    return wall_ms, launch_ms
+
+
+def launch_rooflines(cfg, layer, launch_ms, traffic):
+    """Per attention launch of the timed step: algorithmic FLOP, mean ms,
+    achieved TFLOP/s and fraction of the bf16 peak."""
+    import numpy as np
+    import workloads as W
+    budgets = layer_budgets(layer)
+    kv = layer.kv_len.cpu().numpy().astype(np.int64)
+    st = static_kv_len(cfg, budgets)
+    kv_all = [st[h] if st[h] is not None else int(kv[h]) for h in range(cfg.n_heads)]
+    groups = {"static_attention": [h for h, b in enumerate(budgets) if b.type == W.STATIC],
+              "dynamic_attention": [h for h, b in enumerate(budgets) if b.type == W.DYNAMIC],
+              "attention": list(range(cfg.n_heads))}
+    kernels = {"static_attention": "fkv_chunk_attention_static: attn_bf16_kernel<128, balanced, paged> + "
+                                   "attn_merge_kernel<128, paged> (static heads, history read in place)",
+               "dynamic_attention": "fkv_chunk_attention_heads: attn_bf16_kernel<128, balanced> + "
+                                    "attn_merge_kernel<128> (dynamic heads, compacted history)",
+               "attention": "fkv_chunk_attention: attn_bf16_kernel<128, balanced> + attn_merge_kernel<128> "
+                            "(all heads, compacted history)"}
+    out = []
+    for name, ms in launch_ms.items():
+        flop = attention_flop(cfg, kv_all, groups[name])
+        avg = float(ms.mean())
+        tf = flop / (avg * 1e-3) / 1e12
+        out.append({"launch": name, "kernel": kernels[name], "bound": "mfma", "achieved": round(tf, 1),
+                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4),
+                    "traffic": (traffic or {}).get(name), "algorithmic_flop_per_launch": flop,
+                    "avg_launch_ms": round(avg, 4),
+                    "launch_ms_p10_p50_p90": [round(float(v), 4) for v in np.percentile(ms, [10, 50, 90])]})
+    return out
+
+
+def load_traffic(path, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, only
+    while the attention sources are the ones the counters were taken on."""
+    try:
+        with open(path) as f:
+            tj = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if tj.get("workload") != workload or tj.get("kernel_source_sha") != _kernel_sha():
+        return None
+    return tj.get("bytes_per_launch_by_launch")
 
 
 def main():
@@ -145,8 +330,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
-              "the Forcing-KV hot path shards by head with no exchange, so N GPUs run N "
-              "independent copies of this step.", file=sys.stderr)
+              "this build runs on a single GPU.  The Forcing-KV hot path shards by head with no "
+              "exchange, so N GPUs would run N independent head subsets of this step.", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
@@ -157,98 +342,35 @@ def main():
 
     import workloads as W
     import paper_2605_09681_amd as fkv
-    from paper_2605_09681_amd.layer import CompressedLayer
 
     fkv.lib()  # fail loudly if the HIP library is missing
     torch.cuda.set_device(0)
     cfg = W.wan_layer_config(args.resolution)
-    x = W.make_layer_inputs(cfg, seed=0)
-
-    layers, bufs = [], []
-    base = {k: to_dev(getattr(x, k), cfg.dtype) for k in ("K_hist", "V_hist", "K_cur", "V_cur", "Q")}
+    x = None
+    if args.resolution == "480p":
+        x = W.make_layer_inputs(cfg, seed=0)
+        base = {k: to_dev(getattr(x, k), cfg.dtype) for k in ("K_hist", "V_hist", "K_cur", "V_cur", "Q")}
+    else:
+        base = device_layer_inputs(cfg, seed=0)
+    slots = np.arange(cfg.hist_frames, dtype=np.int32) if x is None else x.frame_slot
+    bufs = []
     for c in range(args.copies):
         b = base if c == 0 else {k: v.clone() for k, v in base.items()}
         b["O"] = torch.empty_like(b["Q"])
         bufs.append(b)
-        layers.append(CompressedLayer(cfg.n_heads, cfg.head_dim, cfg.frame_tokens, cfg.hist_frames,
-                                      cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype,
-                                      cfg.heads, balanced=args.schedule == "balanced",
-                                      in_place=args.static == "in_place"))
-    slots = x.frame_slot
+    layers = make_layers(cfg, args.copies, args)
     stream = torch.cuda.current_stream()
 
-    def step(i):
-        """The timed step (CompressedLayer.step): the static heads' attention
-        (in place, or gather + attention) on a side stream while the dynamic
-        heads are scored, compacted and attended on the main stream."""
-        L, b = layers[i % len(layers)], bufs[i % len(layers)]
-        L.step(b["K_hist"], b["V_hist"], slots, b["Q"], b["K_cur"], b["V_cur"], b["O"])
+    # per-stage breakdown first: it also brings the clock up before the timed steps
+    stage = staged_breakdown(layers, bufs, slots, max(args.steps, 50), stream)
+    breakdown = stage_report(cfg, layers[0], stage)
 
-    def staged(i, ev):
-        """The same four calls one after another on one stream, with HIP
-        events between them: the per-stage breakdown."""
-        L, b = layers[i % len(layers)], bufs[i % len(layers)]
-        ev[0].record(stream)
-        L.score(b["K_hist"], slots, b["K_cur"])
-        ev[1].record(stream)
-        L.select_compact(b["K_hist"], b["V_hist"], slots)
-        ev[2].record(stream)
-        L.compress_static(b["K_hist"], b["V_hist"], slots)
-        ev[3].record(stream)
-        L.attention(b["Q"], b["K_cur"], b["V_cur"], b["O"])
-        ev[4].record(stream)
+    traffic = load_traffic(args.traffic_json, cfg.name)
+    wall_ms, launch_ms = timed_steps(cfg, layers, bufs, slots, args, args.step)
+    launches = launch_rooflines(cfg, layers[0], launch_ms, traffic)
+    dominant = max(launches, key=lambda r: r["avg_launch_ms"])
 
-    def serial(i):
-        L, b = layers[i % len(layers)], bufs[i % len(layers)]
-        L.score(b["K_hist"], slots, b["K_cur"])
-        L.select_compact(b["K_hist"], b["V_hist"], slots)
-        L.compress_static(b["K_hist"], b["V_hist"], slots)
-        L.attention(b["Q"], b["K_cur"], b["V_cur"], b["O"])
-
-    timed = step if args.step == "pipelined" else serial
-    for i in range(args.warmup):
-        timed(i)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        timed(i)
-    torch.cuda.synchronize()
-    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
-
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    for i in range(min(args.warmup, 10)):
-        staged(i, events[0])
-    torch.cuda.synchronize()
-    for i in range(args.steps):
-        staged(i, events[i])
-    torch.cuda.synchronize()
-
-    stage = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(4)] for e in events])  # ms
-    score_ms, select_ms, static_ms, attn_ms = stage.mean(axis=0).tolist()
-    p10, p50, p90 = np.percentile(stage, [10, 50, 90], axis=0)
-    extras = None if args.no_extras else measure_extras(args, cfg, x, bufs, layers, stream)
-
-    # algorithmic work per unit
-    kv_len = layers[0].kv_len.cpu().numpy().astype(np.int64)
-    d, e, F, H, Lq = cfg.head_dim, 2, cfg.frame_tokens, cfg.hist_frames, cfg.lq
-    n_dyn = sum(1 for b in cfg.heads if b.type == W.DYNAMIC)
-    dyn = np.array([b.type == W.DYNAMIC for b in cfg.heads])
-    attn_flop = float(4.0 * Lq * d * np.sum(kv_len + Lq))
-    score_bytes = n_dyn * (H + 1) * F * d * e
-    dyn_copy_bytes = 4 * d * e * int(kv_len[dyn].sum())
-    static_copy_bytes = 4 * d * e * int(kv_len[~dyn].sum())
-    attn_tflops = attn_flop / (attn_ms * 1e-3) / 1e12
-
-    traffic = None
-    if os.path.exists(args.traffic_json):
-        try:
-            with open(args.traffic_json) as f:
-                tj = json.load(f)
-            if tj.get("workload") == cfg.name and tj.get("kernel_source_sha") == _kernel_sha():
-                traffic = tj.get("bytes_per_launch")
-        except (OSError, ValueError):
-            traffic = None
-
+    d, F, H, Lq = cfg.head_dim, cfg.frame_tokens, cfg.hist_frames, cfg.lq
     out = {
         "metric": METRIC,
         "value": round(wall_ms, 4),
@@ -267,7 +389,8 @@ def main():
                          f"{F} tokens/frame, {H}-frame history, {cfg.chunk_frames}-frame chunk "
                          f"(Lq {Lq}); heads 0-5 static (sink 1 + recent 6), heads 6-11 dynamic "
                          f"(sink 1 + 10 of 20 frame segments)"),
-            "kv_len": kv_len.tolist(),
+            "value_is": "ms per layer per AR step (one unit); the measured 30-layer x 4-step ms per chunk "
+                        "is rollout_480p",
             "rotating_copies": args.copies,
             "attention_schedule": args.schedule,
             "step": (("static heads (attention read in place from the cache" if args.static == "in_place" else
@@ -276,55 +399,37 @@ def main():
                      if args.step == "pipelined" else
                      "the four calls one after another on one stream"),
         },
-        "roofline": {
-            "kernel": "fkv_chunk_attention: attn_bf16_kernel<128, balanced> + attn_merge_kernel<128>",
-            "bound": "mfma",
-            "achieved": round(attn_tflops, 1),
-            "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": traffic,
-            "algorithmic_flop_per_launch": attn_flop,
-            "avg_launch_ms": round(attn_ms, 4),
-        },
-        "breakdown_ms": {
-            "score_segments": round(score_ms, 4),
-            "select_compact": round(select_ms, 4),
-            "compress_static": round(static_ms, 4),
-            "chunk_attention": round(attn_ms, 4),
-        },
-        "breakdown_gbs": {
-            "score_segments": round(score_bytes / (score_ms * 1e-3) / 1e9, 1),
-            "select_compact": round(dyn_copy_bytes / (select_ms * 1e-3) / 1e9, 1),
-            "compress_static": round(static_copy_bytes / (static_ms * 1e-3) / 1e9, 1),
-            "peak": PEAK_HBM_GBS,
-        },
-        "breakdown_frac_of_hbm_peak": {
-            "score_segments": round(score_bytes / (score_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 3),
-            "select_compact": round(dyn_copy_bytes / (select_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 3),
-            "compress_static": round(static_copy_bytes / (static_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 3),
-        },
-        "breakdown_ms_p10_p50_p90": {
-            k: [round(float(p10[j]), 4), round(float(p50[j]), 4), round(float(p90[j]), 4)]
-            for j, k in enumerate(("score_segments", "select_compact", "compress_static", "chunk_attention"))},
-        "attn_tflops": round(attn_tflops, 1),
-        "serial_step_ms": round(score_ms + select_ms + static_ms + attn_ms, 4),
-        "ms_per_chunk_extrapolated_30layers_4steps": round(wall_ms * 120, 2),
+        "roofline": {k: v for k, v in dominant.items() if k != "launch_ms_p10_p50_p90"},
+        "roofline_launches": launches,
+        "breakdown_serial": breakdown,
+        "attn_tflops": dominant["achieved"],
     }
-    if extras is not None:
-        ua = extras["uncompressed_attention"]
-        ua["speedup_of_compressed"] = round(ua["ms"] / attn_ms, 3)
+    extras = None
+    if not args.no_extras:
+        extras = measure_extras(args, cfg, slots, bufs, layers, stream)
+        ua = extras.get("uncompressed_attention")
+        if ua is not None:
+            ua["speedup_of_compressed"] = round(ua["ms"] / breakdown["ms"]["chunk_attention"], 3)
         out["extras"] = extras
+    if not args.no_extras and args.resolution == "480p":
+        for b in bufs[1:]:
+            b.clear()
+        del layers
+        torch.cuda.empty_cache()
+        out["extras"]["sweep_480p"] = measure_sweep(args, bufs[0], stream)
+        out["extras"]["unit_1080p"] = measure_1080p(args, stream)
     if not args.no_rollout and not args.no_extras:
         for b in bufs:   # free the single-layer buffers before the 30-layer caches
             b.clear()
-        del layers, base
         torch.cuda.empty_cache()
         out["rollout_480p"] = measure_rollouts({"per_layer_scoring": (False, False),
                                                 "per_layer_incremental_rescoring": (False, True),
                                                 "pooled_first_block_proxy": (True, False)})
-    if not args.no_cpu_baseline:
+        out["rollout_480p_60_chunks"] = measure_rollouts({"per_layer_scoring": (False, False)}, n_chunks=60,
+                                                         reps=1)
+    if not args.no_cpu_baseline and args.resolution == "480p":
         out["cpu_baseline"] = cpu_baseline(cfg, x, args.cpu_rows)
+        out["cpu_baseline"]["leg_1080p"] = cpu_baseline_1080p(args.cpu_rows_1080p)
     print(json.dumps(out), flush=True)
 
 
@@ -338,24 +443,10 @@ def _next_pair(layers, bufs):
     return layers[i], bufs[i]
 
 
-def _time_ms(fn, reps, stream):
-    """Mean ms of fn() over reps launches, HIP events on the launch stream."""
-    import torch
-    for _ in range(3):
-        fn()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for _ in range(reps):
-        fn()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / reps
-
-
-def measure_extras(args, cfg, x, bufs, layers, stream):
-    """Measurements outside the step: the first-block proxy (scores pooled over
-    all heads, computed once per chunk and shared by every layer) and the same
+def measure_extras(args, cfg, slots, bufs, layers, stream):
+    """Measurements outside the step: where the two-stream step's time goes,
+    the FP8 variant, incremental rescoring, the first-block proxy (scores
+    pooled over all heads, once per chunk, shared by every layer) and the same
     attention kernel on the uncompressed cache (every head keeps all H frames),
     for the kernel-level speedup of the compression."""
     import numpy as np
@@ -368,13 +459,13 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
     L0, b = layers[0], bufs[0]
     pooled = torch.empty((L0.n_seg,), dtype=torch.float32, device="cuda")
     ws = torch.empty(max(fkv.fkv_score_pooled_workspace_size(L0.shape), 1), dtype=torch.uint8, device="cuda")
-    pooled_ms = _time_ms(lambda: fkv.fkv_score_pooled(L0.shape, b["K_hist"], x.frame_slot, b["K_cur"], pooled, ws),
+    pooled_ms = _time_ms(lambda: fkv.fkv_score_pooled(L0.shape, b["K_hist"], slots, b["K_cur"], pooled, ws),
                          20, stream)
     pooled_bytes = cfg.n_heads * (H + 1) * F * d * 2
     stats = torch.empty(fkv.fkv_score_stats_size(L0.shape, L0.heads) // 8, dtype=torch.float64, device="cuda")
-    hist_ms = _time_ms(lambda: fkv.fkv_score_history(L0.shape, L0.heads, b["K_hist"], x.frame_slot, stats,
+    hist_ms = _time_ms(lambda: fkv.fkv_score_history(L0.shape, L0.heads, b["K_hist"], slots, stats,
                                                      L0.workspace), 20, stream)
-    cached_ms = _time_ms(lambda: fkv.fkv_score_segments_cached(L0.shape, L0.heads, b["K_hist"], x.frame_slot,
+    cached_ms = _time_ms(lambda: fkv.fkv_score_segments_cached(L0.shape, L0.heads, b["K_hist"], slots,
                                                                b["K_cur"], stats, L0.scores, L0.workspace), 20,
                          stream)
     n_dyn = sum(1 for t in L0.types if t == W.DYNAMIC)
@@ -386,7 +477,7 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
         return lambda: fn(*_next_pair(layers, bufs))
 
     def static_only(L, bb):
-        L.attention_static(bb["K_hist"], bb["V_hist"], x.frame_slot, bb["Q"], bb["K_cur"], bb["V_cur"], bb["O"],
+        L.attention_static(bb["K_hist"], bb["V_hist"], slots, bb["Q"], bb["K_cur"], bb["V_cur"], bb["O"],
                            None, L.attn_workspace)
 
     def dynamic_only(L, bb):
@@ -412,47 +503,25 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
     pack_ms = _time_ms(lambda: L0.pack_fp8(b["Q"], b["K_cur"], b["V_cur"]), 20, stream)
     fp8_ms = _time_ms(lambda: L0.attention_fp8_packed(O8), 20, stream)
     kv_len = L0.kv_len.cpu().numpy().astype(np.int64)
-    attn_flop = 4.0 * Lq * d * float(np.sum(kv_len + Lq))
+    attn_flop = attention_flop(cfg, kv_len)
 
     full_heads = tuple(W.HeadBudget(W.STATIC, 0, H) for _ in range(cfg.n_heads))
     full = CompressedLayer(cfg.n_heads, d, F, H, cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype,
                            full_heads, balanced=args.schedule == "balanced")
-    full.compress_static(b["K_hist"], b["V_hist"], x.frame_slot)
+    full.compress_static(b["K_hist"], b["V_hist"], slots)
     O = torch.empty_like(b["Q"])
     full_ms = _time_ms(lambda: full.attention(b["Q"], b["K_cur"], b["V_cur"], O), 10, stream)
     full_flop = 4.0 * Lq * d * cfg.n_heads * (H * F + Lq)
     del full
-    # the 1080P layer (68x120 patches per frame) with device-generated N(0,1) inputs
-    c10 = W.wan_layer_config("1080p")
-    g = torch.Generator(device="cuda").manual_seed(1)
-    rn = lambda *sh: torch.randn(*sh, device="cuda", dtype=torch.bfloat16, generator=g)
-    L10 = CompressedLayer(c10.n_heads, c10.head_dim, c10.frame_tokens, c10.hist_frames, c10.cap_frames,
-                          c10.chunk_frames, c10.seg_tokens, c10.dtype, c10.heads,
-                          balanced=args.schedule == "balanced")
-    Kh, Vh = rn(12, c10.cap_frames, c10.frame_tokens, d), rn(12, c10.cap_frames, c10.frame_tokens, d)
-    Kq, Vq, Q10 = rn(12, c10.lq, d), rn(12, c10.lq, d), rn(12, c10.lq, d)
-    O10 = torch.empty_like(Q10)
-    slots10 = np.arange(c10.hist_frames, dtype=np.int32)
-    unit10_ms = _time_ms(lambda: L10.step(Kh, Vh, slots10, Q10, Kq, Vq, O10), 5, stream)
-    # the step attends the static heads in place; gather them once so the
-    # 12-head attention call below sees every head's kept history
-    L10.compress(Kh, Vh, slots10, Kq)
-    att10_ms = _time_ms(lambda: L10.attention(Q10, Kq, Vq, O10), 5, stream)
-    kv10 = L10.kv_len.cpu().numpy().astype(np.int64)
-    flop10 = 4.0 * c10.lq * d * float(np.sum(kv10 + c10.lq))
-    del L10, Kh, Vh, Kq, Vq, Q10, O10
 
     return {
-        "step_parts_480p": dict(parts, note="each timed alone over the rotated buffer copies; the step runs the "
-                                          "first two on two streams after the dynamic compression"),
-        "unit_1080p": {
-            "ms": round(unit10_ms, 3), "attention_ms": round(att10_ms, 3),
-            "attention_TFLOP_s": round(flop10 / (att10_ms * 1e-3) / 1e12, 1),
-            "workload": "wan1.3b-1080p-layer: 12 heads x d128, 8160 tokens/frame, 21-frame history, 3-frame chunk",
-            "note": "device-generated N(0,1) inputs, one buffer set (the cache far exceeds the 256 MB MALL)"},
+        "step_parts": dict(parts, note="each timed alone over the rotated buffer copies; the step runs the "
+                                       "first two on two streams after the dynamic compression"),
         "fp8_attention": {
             "attention_ms": round(fp8_ms, 4), "TFLOP_s": round(attn_flop / (fp8_ms * 1e-3) / 1e12, 1),
-            "peak_TFLOP_s": 5000.0, "pack_ms": round(pack_ms, 4),
+            "peak_TFLOP_s": PEAK_FP8_TFLOPS,
+            "frac_of_fp8_peak": round(attn_flop / (fp8_ms * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 4),
+            "pack_ms": round(pack_ms, 4), "pack_plus_attention_ms": round(pack_ms + fp8_ms, 4),
             "note": "E4M3 Q/K/V/P on gfx950 FP8 MFMA; pack = statistics + quantise + transpose"},
         "incremental_score": {"history_ms": round(hist_ms, 4), "step_ms": round(cached_ms, 4),
                               "step_GB_s": round(n_dyn * 2 * F * d * 2 / (cached_ms * 1e-3) / 1e9, 1),
@@ -460,6 +529,7 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
                                       "them plus frames H-1 and H (2 of the 22 frames per dynamic head)"},
         "pooled_proxy_score": {
             "ms": round(pooled_ms, 4), "GB_s": round(pooled_bytes / (pooled_ms * 1e-3) / 1e9, 1),
+            "frac_of_hbm_peak": round(pooled_bytes / (pooled_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 3),
             "note": "all 12 heads pooled, once per AR step for all layers (not part of the step)"},
         "uncompressed_attention": {
             "ms": round(full_ms, 4), "TFLOP_s": round(full_flop / (full_ms * 1e-3) / 1e12, 1),
@@ -467,22 +537,75 @@ def measure_extras(args, cfg, x, bufs, layers, stream):
     }
 
 
+def measure_sweep(args, b, stream, reps=30):
+    """The keep-fraction x segment-length sweep at 480P: per point the four
+    calls one after another (score, select + compact, static gather, 12-head
+    attention), mean ms per kernel over `reps` units with HIP events, achieved
+    GB/s of the HBM kernels and attention TFLOP/s.  Keep 100% also keeps every
+    frame of the static heads (full-attention equivalence)."""
+    import numpy as np
+    import workloads as W
+    out = []
+    slots = np.arange(21, dtype=np.int32)
+    for L in (390, 1560, 4680):
+        for frac in (0.25, 0.5, 0.75, 1.0):
+            cfg = W.wan_layer_config("480p", keep_fraction=frac, seg_tokens=L,
+                                     static_recent=21 if frac == 1.0 else 6)
+            layer = make_layers(cfg, 1, args)[0]
+            stage = staged_breakdown([layer], [b], slots, reps, stream, warm=3)
+            rep = stage_report(cfg, layer, stage)
+            out.append({"seg_tokens": L, "keep_fraction": frac, "unit_ms": rep["serial_unit_ms"],
+                        "ms": rep["ms"], "GB_s": rep["GB_s"], "frac_of_hbm_peak": rep["frac_of_hbm_peak"],
+                        "attention_TFLOP_s": rep["attention_TFLOP_s"],
+                        "attention_frac_of_bf16_peak": rep["attention_frac_of_bf16_peak"],
+                        "kv_len_dynamic": int(layer.kv_len[6].item())})
+            del layer
+    return {"points": out,
+            "note": "one buffer set (cache 202 MB: the rotating copies are freed first), serial calls"}
+
+
+def measure_1080p(args, stream):
+    """The 1080P layer (68x120 patches per frame): the default step, the four
+    calls with a per-kernel breakdown, and each launch of the step, with
+    device-generated inputs and one buffer set (the 1.05 GB cache far exceeds
+    the 256 MB MALL)."""
+    import numpy as np
+    import torch
+    import workloads as W
+    c10 = W.wan_layer_config("1080p")
+    b = device_layer_inputs(c10, seed=1)
+    b["O"] = torch.empty_like(b["Q"])
+    slots10 = np.arange(c10.hist_frames, dtype=np.int32)
+    layer = make_layers(c10, 1, args)[0]
+    stage = staged_breakdown([layer], [b], slots10, 6, stream, warm=2)
+    rep = stage_report(c10, layer, stage)
+    a10 = argparse.Namespace(**vars(args))
+    a10.steps, a10.warmup = 6, 2
+    wall, launch_ms = timed_steps(c10, [layer], [b], slots10, a10, "pipelined")
+    launches = launch_rooflines(c10, layer, launch_ms, None)
+    del layer, b
+    torch.cuda.empty_cache()
+    return {"step_ms": round(wall, 3), "breakdown_serial": rep, "step_launches": launches,
+            "workload": "wan1.3b-1080p-layer: 12 heads x d128, 8160 tokens/frame, 21-frame history, "
+                        "3-frame chunk; heads 0-5 static (sink 1 + recent 6), 6-11 dynamic (sink 1 + 10 of 20)",
+            "note": "device-generated inputs, one buffer set"}
+
+
 def measure_rollouts(modes, n_chunks: int = 10, n_steps: int = 4, n_layers: int = 30, reps: int = 3):
     """The metric measured rather than extrapolated: the 30-layer stack of the
-    480P layer, 4 denoising steps per chunk, 10 chunks, each layer with its own
-    rolling 21-frame cache (sink pinned, 3-frame chunks written back after
-    each chunk) and its own seeded head mask (6 of 12 heads dynamic).  modes
-    maps a name to (pooled, incremental): every step re-scores and compacts
-    every layer (pooled=False), or scores once per step from the first layer's
-    keys pooled over all heads and reuses that row in every layer (pooled=True,
-    the first-block proxy); incremental=True computes each layer's history
-    statistics once per chunk and then scores each step from them plus the
-    pair touching the chunk.  All modes run on one stack (one allocation: a
-    re-allocated 6 GB stack has measured up to 8% slower) in `reps` rounds,
-    each round one pass per mode from empty caches; the pass with the median
-    full-window time is reported.  Inputs are device-generated N(0,1) tensors
-    (values do not change the work)."""
-    import numpy as np
+    480P layer, 4 denoising steps per chunk, `n_chunks` chunks, each layer with
+    its own rolling 21-frame cache (sink pinned, 3-frame chunks written back
+    after each chunk) and its own seeded head mask (6 of 12 heads dynamic).
+    modes maps a name to (pooled, incremental): every step re-scores and
+    compacts every layer (pooled=False), or scores once per step from the first
+    layer's keys pooled over all heads and reuses that row in every layer
+    (pooled=True, the first-block proxy); incremental=True computes each
+    layer's history statistics once per chunk and then scores each step from
+    them plus the pair touching the chunk.  All modes run on one stack (one
+    allocation: a re-allocated 6 GB stack has measured up to 8% slower) in
+    `reps` rounds, each round one pass per mode from empty caches; the pass
+    with the median full-window time is reported.  Inputs are device-generated
+    N(0,1) tensors (values do not change the work)."""
     import torch
     import workloads as W
     from paper_2605_09681_amd.layer import RolloutStack
@@ -534,8 +657,9 @@ def measure_rollouts(modes, n_chunks: int = 10, n_steps: int = 4, n_layers: int 
         full = [t for i, t in enumerate(per_chunk) if len(W.ring_frame_slots(i, C, window)) == window]
         return (sum(full) / len(full) if full else wall / n_chunks, wall / n_chunks, per_chunk)
 
-    for pooled, incremental in modes.values():    # untimed: fills the caches, warms the clock
-        run(pooled, incremental)
+    if reps > 1:
+        for pooled, incremental in modes.values():    # untimed: fills the caches, warms the clock
+            run(pooled, incremental)
     runs = {name: [] for name in modes}
     for _ in range(reps):
         for name, (pooled, incremental) in modes.items():
@@ -546,15 +670,104 @@ def measure_rollouts(modes, n_chunks: int = 10, n_steps: int = 4, n_layers: int 
     for name, rs in runs.items():
         rs.sort(key=lambda r: r[0])
         full_ms, chunk_ms, per_chunk = rs[len(rs) // 2]
-        out[name] = {"ms_per_chunk": round(chunk_ms, 2),
-                     "ms_per_chunk_full_window": round(full_ms, 2),
-                     "full_window_ms_of_each_pass": [round(r[0], 2) for r in rs],
-                     "per_chunk_ms": [round(t, 2) for t in per_chunk]}
+        rec = {"ms_per_chunk": round(chunk_ms, 2), "ms_per_chunk_full_window": round(full_ms, 2),
+               "full_window_ms_of_each_pass": [round(r[0], 2) for r in rs]}
+        if n_chunks <= 12:
+            rec["per_chunk_ms"] = [round(t, 2) for t in per_chunk]
+        else:
+            full = [t for i, t in enumerate(per_chunk) if len(W.ring_frame_slots(i, C, window)) == window]
+            rec["full_window_chunks"] = len(full)
+            rec["full_window_ms_p10_p50_p90"] = [round(float(v), 2) for v in
+                                                 __import__("numpy").percentile(full, [10, 50, 90])]
+            rec["ring_wraps"] = round((n_chunks * C - window) / (window - 1), 2)
+        out[name] = rec
     out["workload"] = (f"{n_layers} layers x {n_steps} steps x {n_chunks} chunks, rolling {window}-frame cache "
                        "(sink pinned), 3-frame chunks appended, seeded masks with 6 of 12 heads dynamic; "
-                       f"wall-clock including the chunk writes; median of {reps} passes per mode, "
-                       "modes interleaved on one stack")
+                       f"wall-clock including the chunk writes; median of {reps} passes per mode"
+                       + (", modes interleaved on one stack" if len(modes) > 1 else ""))
     return out
+
+
+def cpu_baseline(cfg, x, rows_per_head):
+    """Time the CPU oracle on the host cores: full compression of every head
+    and attention for a seeded sample of query rows per head, scaled to one
+    unit (the attention time is multiplied by Lq / rows_per_head)."""
+    import numpy as np
+    import oracle
+    import workloads as W
+    oracle.lib()
+    rng = np.random.default_rng(0)
+    rows = np.sort(rng.choice(cfg.lq, size=min(rows_per_head, cfg.lq), replace=False)).astype(np.int32)
+    t0 = time.perf_counter()
+    res = oracle.run_layer(cfg, x, attention=False)
+    t1 = time.perf_counter()
+    scale = 1.0 / math.sqrt(cfg.head_dim)
+    for h in range(cfg.n_heads):
+        oracle.attention_rows(x.Q[h], res.Kc[h], res.Vc[h], x.K_cur[h], x.V_cur[h], scale, rows)
+    t2 = time.perf_counter()
+    per_unit_s = (t1 - t0) + (t2 - t1) * cfg.lq / len(rows)
+    # the tiny fp32 configuration in full on one thread, for reference
+    threads = oracle.max_threads()
+    tiny = W.tiny_config()
+    xt = W.make_layer_inputs(tiny, seed=0)
+    oracle.set_threads(1)
+    t3 = time.perf_counter()
+    oracle.run_layer(tiny, xt)
+    t4 = time.perf_counter()
+    oracle.set_threads(threads)
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
+    return {
+        "value": round(per_unit_s * 1e3, 1),
+        "unit": "ms",
+        "cores": oracle.max_threads(),
+        "kind": "oracle",
+        "sample": (f"480P layer unit: fp64 C oracle, scoring+selection+compaction of all {cfg.n_heads} heads "
+                   f"in full ({t1 - t0:.2f} s) + attention of {len(rows)} of {cfg.lq} query rows per head "
+                   f"({t2 - t1:.2f} s), attention scaled x{cfg.lq / len(rows):.1f} to one unit"),
+        "measured_s": round(t2 - t0, 2),
+        "cpu_model": cpu_model,
+        "nproc": os.cpu_count(),
+        "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+        "tiny_f32_unit_1thread_ms": round((t4 - t3) * 1e3, 2),
+    }
+
+
+def cpu_baseline_1080p(rows_per_head):
+    """The oracle on the 1080P layer: scoring, selection and compaction of all
+    heads in full, attention on a seeded sample of query rows per head,
+    extrapolated to all 24480 rows (labelled so).  Inputs are generated on the
+    device and copied to the host (the same bits on both sides)."""
+    import numpy as np
+    import torch
+    import oracle
+    import workloads as W
+    c10 = W.wan_layer_config("1080p")
+    b = device_layer_inputs(c10, seed=1)
+    x = W.LayerInputs(c10, host_bits(b["K_hist"]), host_bits(b["V_hist"]), host_bits(b["K_cur"]),
+                      host_bits(b["V_cur"]), host_bits(b["Q"]), np.arange(c10.hist_frames, dtype=np.int32))
+    del b
+    torch.cuda.empty_cache()
+    rng = np.random.default_rng(1)
+    rows = np.sort(rng.choice(c10.lq, size=min(rows_per_head, c10.lq), replace=False)).astype(np.int32)
+    t0 = time.perf_counter()
+    res = oracle.run_layer(c10, x, attention=False)
+    t1 = time.perf_counter()
+    scale = 1.0 / math.sqrt(c10.head_dim)
+    for h in range(c10.n_heads):
+        oracle.attention_rows(x.Q[h], res.Kc[h], res.Vc[h], x.K_cur[h], x.V_cur[h], scale, rows)
+    t2 = time.perf_counter()
+    per_unit_s = (t1 - t0) + (t2 - t1) * c10.lq / len(rows)
+    return {"value": round(per_unit_s * 1e3, 1), "unit": "ms", "cores": oracle.max_threads(), "kind": "oracle",
+            "extrapolated": True,
+            "sample": (f"1080P layer unit: scoring+selection+compaction of all 12 heads in full ({t1 - t0:.2f} s) "
+                       f"+ attention of {len(rows)} of {c10.lq} query rows per head ({t2 - t1:.2f} s), "
+                       f"attention extrapolated x{c10.lq / len(rows):.1f} to one unit"),
+            "measured_s": round(t2 - t0, 2)}
 
 
 def _kernel_sha():

@@ -42,7 +42,9 @@
  * Errors: a non-OK status is returned before anything is enqueued, so a
  * failed call writes nothing.  FKV_ERR_ARG: null pointer, bad enum, negative
  * budget, non-positive scale, slot out of range.  FKV_ERR_SHAPE: unsupported
- * shape (see fkv_shape).  FKV_ERR_CAPACITY: `slab` or the workspace is too
+ * shape (see fkv_shape; also a frame, the chunk or one head's cache of 2^31
+ * bytes or more, which the kernels' 32-bit buffer ranges cannot address).
+ * FKV_ERR_CAPACITY: `slab` or the workspace is too
  * small.  FKV_ERR_DEVICE: the HIP runtime reported a launch error.
  * fkv_last_error() returns a message for the last non-OK status of the calling
  * thread.  Calls on distinct streams are independent; calls that share an
@@ -245,9 +247,15 @@ fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes);
  *   O[h][r] = softmax(scale * Q[h][r] . keys^T) . values   (no mask)
  * bf16: bf16 inputs, MFMA products accumulated in fp32, fp32 online softmax,
  * probabilities rounded to bf16 for the value product, output normalised and
- * rounded to bf16.  fp32: all fp32.  lse (nullable, float [n_heads][C*F])
- * receives the natural-log normaliser log(sum exp(scale*q.k)).  scale must be
- * positive and finite (1/sqrt(d) is the usual choice).
+ * rounded to bf16.  fp32: all fp32.  scale must be positive and finite
+ * (1/sqrt(d) is the usual choice).
+ * lse (nullable, float [n_heads][C*F]) receives the natural-log normaliser of
+ * the weights that multiply V.  fp32: log(sum_j exp(z_j)), z_j = scale*q.k_j.
+ * bf16: m*ln2 + log(sum_j p_j) with p_j = bf16(2^(z_j*log2(e) - m)), the
+ * bf16-rounded probabilities the value product uses, and m a per-row reference
+ * (the running maximum in log2 units); since every p_j lies within a relative
+ * 2^-9 of its exact value, this differs from log(sum_j exp(z_j)) by at most
+ * -log(1 - 2^-9) = 1.96e-3 beyond the rounding of the bf16 score products.
  *
  * Work schedule (bf16): with workspace == NULL every (head, 256-row query
  * tile) is one workgroup; heads with longer caches then finish last.  With a

@@ -194,6 +194,20 @@ def _slots(frame_slot, H):
     return arr
 
 
+def _heads(shape: fkv_shape, heads, allow_none: bool = False):
+    """The host fkv_head array of a call: the C entry points read exactly
+    shape.n_heads entries, so a shorter or longer array is rejected here."""
+    if heads is None:
+        if allow_none:
+            return None
+        raise ValueError("heads is None")
+    if not isinstance(heads, ctypes.Array) or heads._type_ is not fkv_head:
+        raise TypeError("heads must be an fkv_head array (see make_heads)")
+    if len(heads) != shape.n_heads:
+        raise ValueError(f"heads has {len(heads)} entries, the shape has {shape.n_heads} heads")
+    return heads
+
+
 def _stream(stream) -> ctypes.c_void_p:
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
@@ -217,7 +231,7 @@ def fkv_num_segments(shape: fkv_shape) -> int:
 
 def fkv_kept_tokens_max(shape: fkv_shape, heads, head: int) -> int:
     out = ctypes.c_int64(0)
-    _raise(lib().fkv_kept_tokens_max(ctypes.byref(shape), heads, int(head), ctypes.byref(out)))
+    _raise(lib().fkv_kept_tokens_max(ctypes.byref(shape), _heads(shape, heads), int(head), ctypes.byref(out)))
     return int(out.value)
 
 
@@ -228,7 +242,7 @@ def slab_tokens(shape: fkv_shape, heads) -> int:
 
 def fkv_score_workspace_size(shape: fkv_shape, heads) -> int:
     out = ctypes.c_size_t(0)
-    _raise(lib().fkv_score_workspace_size(ctypes.byref(shape), heads, ctypes.byref(out)))
+    _raise(lib().fkv_score_workspace_size(ctypes.byref(shape), _heads(shape, heads), ctypes.byref(out)))
     return int(out.value)
 
 
@@ -242,7 +256,7 @@ def fkv_compress_static(shape: fkv_shape, heads, K_hist, V_hist, frame_slot, Kc,
     sl = _slots(frame_slot, shape.hist_frames)
     args += [_check(Kc, "Kc", dt, comp), _check(Vc, "Vc", dt, comp)]
     kl = _check(kv_len, "kv_len", torch.int32, (shape.n_heads,))
-    _raise(lib().fkv_compress_static(ctypes.byref(shape), heads, args[0], args[1], sl, args[2],
+    _raise(lib().fkv_compress_static(ctypes.byref(shape), _heads(shape, heads), args[0], args[1], sl, args[2],
                                      args[3], int(slab), kl, _stream(stream)))
 
 
@@ -261,7 +275,7 @@ def fkv_score_segments(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, score
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=K_hist.device)
     ws = _check(workspace, "workspace", torch.uint8)
-    _raise(lib().fkv_score_segments(ctypes.byref(shape), heads, kh, sl, kc, sc, ws,
+    _raise(lib().fkv_score_segments(ctypes.byref(shape), _heads(shape, heads), kh, sl, kc, sc, ws,
                                     workspace.numel(), _stream(stream)))
     return workspace
 
@@ -269,7 +283,7 @@ def fkv_score_segments(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, score
 def fkv_score_stats_size(shape: fkv_shape, heads, pooled: bool = False) -> int:
     """Bytes of the per-frame statistics buffer of incremental rescoring."""
     out = ctypes.c_size_t(0)
-    _raise(lib().fkv_score_stats_size(ctypes.byref(shape), heads, int(pooled), ctypes.byref(out)))
+    _raise(lib().fkv_score_stats_size(ctypes.byref(shape), _heads(shape, heads, allow_none=bool(pooled)), int(pooled), ctypes.byref(out)))
     return int(out.value)
 
 
@@ -282,7 +296,7 @@ def fkv_score_history(shape: fkv_shape, heads, K_hist, frame_slot, stats, worksp
     kh = _check(K_hist, "K_hist", dt, hist)
     st = _check(stats, "stats", torch.float64)
     ws = _check(workspace, "workspace", torch.uint8)
-    _raise(lib().fkv_score_history(ctypes.byref(shape), heads, int(pooled), kh, _slots(frame_slot, shape.hist_frames),
+    _raise(lib().fkv_score_history(ctypes.byref(shape), _heads(shape, heads, allow_none=bool(pooled)), int(pooled), kh, _slots(frame_slot, shape.hist_frames),
                                    st, stats.numel() * 8, ws, workspace.numel(), _stream(stream)))
 
 
@@ -299,7 +313,7 @@ def fkv_score_segments_cached(shape: fkv_shape, heads, K_hist, frame_slot, K_cur
     sc = _check(scores, "scores", torch.float32, (n_seg,) if pooled else (shape.n_heads, n_seg))
     st = _check(stats, "stats", torch.float64)
     ws = _check(workspace, "workspace", torch.uint8)
-    _raise(lib().fkv_score_segments_cached(ctypes.byref(shape), heads, int(pooled), kh,
+    _raise(lib().fkv_score_segments_cached(ctypes.byref(shape), _heads(shape, heads, allow_none=bool(pooled)), int(pooled), kh,
                                            _slots(frame_slot, shape.hist_frames), kc, st, stats.numel() * 8, sc,
                                            ws, workspace.numel(), _stream(stream)))
 
@@ -372,7 +386,7 @@ def _select_compact(shape, heads, scores, K_hist, V_hist, frame_slot, kept_seg, 
     kc, vc = _check(Kc, "Kc", dt, comp), _check(Vc, "Vc", dt, comp)
     kl = _check(kv_len, "kv_len", torch.int32, (shape.n_heads,))
     fn = lib().fkv_select_compact_pooled if pooled else lib().fkv_select_compact
-    _raise(fn(ctypes.byref(shape), heads, sc, kh, vh, sl, ks, kc, vc, int(slab), kl, _stream(stream)))
+    _raise(fn(ctypes.byref(shape), _heads(shape, heads), sc, kh, vh, sl, ks, kc, vc, int(slab), kl, _stream(stream)))
 
 
 def fkv_attention_workspace_size(shape: fkv_shape) -> int:
@@ -441,7 +455,7 @@ def fkv_chunk_attention_static(shape: fkv_shape, heads, K_hist, V_hist, frame_sl
     ws, nws = None, 0
     if workspace is not None:
         ws, nws = _check(workspace, "workspace", torch.uint8), workspace.numel()
-    _raise(lib().fkv_chunk_attention_static(ctypes.byref(shape), heads, kh, vh, sl, q, kq, vq,
+    _raise(lib().fkv_chunk_attention_static(ctypes.byref(shape), _heads(shape, heads), kh, vh, sl, q, kq, vq,
                                             ctypes.c_float(scale), o, ls, ws, nws, _stream(stream)))
 
 

@@ -57,6 +57,16 @@ fkv_status check_shape(const fkv_shape *s) {
     if (cap_tokens + lq > (int64_t)1 << 30)
         return fail(FKV_ERR_SHAPE, "cache + chunk of %lld tokens per head is too large",
                     (long long)(cap_tokens + lq));
+    // Kernels address a frame, a segment piece and the chunk of one head
+    // through 32-bit byte offsets and raw buffer ranges: keep each below 2^31.
+    const int64_t row_bytes = (int64_t)s->head_dim * (s->dtype == FKV_BF16 ? 2 : 4);
+    if ((int64_t)s->frame_tokens * row_bytes >= (int64_t)1 << 31)
+        return fail(FKV_ERR_SHAPE, "a frame of %d tokens spans 2^31 bytes or more", s->frame_tokens);
+    if (lq * row_bytes >= (int64_t)1 << 31)
+        return fail(FKV_ERR_SHAPE, "a chunk of %lld tokens spans 2^31 bytes or more", (long long)lq);
+    if (cap_tokens * row_bytes >= (int64_t)1 << 31)
+        return fail(FKV_ERR_SHAPE, "a head's cache of %lld tokens spans 2^31 bytes or more",
+                    (long long)cap_tokens);
     const int64_t n_seg = (hist_tokens + s->seg_tokens - 1) / s->seg_tokens;
     if (n_seg > FKV_MAX_SEGMENTS)
         return fail(FKV_ERR_SHAPE, "%lld segments exceed %d", (long long)n_seg, FKV_MAX_SEGMENTS);
@@ -757,6 +767,9 @@ fkv_status fkv_fp8_sizes(const fkv_shape *shape, int32_t slab, size_t *q_bytes, 
     if ((st = check_shape(shape)) != FKV_OK) return st;
     if (shape->dtype != FKV_BF16) return fail(FKV_ERR_SHAPE, "the FP8 path takes bf16 inputs");
     if (slab < 0) return fail(FKV_ERR_ARG, "slab %d < 0", slab);
+    if ((int64_t)slab > (int64_t)shape->cap_frames * shape->frame_tokens)
+        return fail(FKV_ERR_ARG, "slab %d exceeds the cache's %lld tokens", slab,
+                    (long long)shape->cap_frames * shape->frame_tokens);
     if (!q_bytes || !kv_bytes || !scale_bytes || !workspace_bytes) return fail(FKV_ERR_ARG, "NULL size pointer");
     const int64_t lq = (int64_t)shape->chunk_frames * shape->frame_tokens;
     const int64_t rows = (slab + lq + 63) / 64 * 64;
@@ -794,14 +807,14 @@ fkv_status fkv_fp8_pack(const fkv_shape *shape, const void *Q, const void *Kc, c
     a.n_heads = shape->n_heads;
     a.Lq = shape->chunk_frames * shape->frame_tokens;
     a.d = shape->head_dim;
-    a.rows = (slab + a.Lq + 63) / 64 * 64;
+    a.rows = ((int64_t)slab + a.Lq + 63) / 64 * 64;
     a.Q8 = (uint8_t *)Q8;
     a.K8 = (uint8_t *)K8;
     a.V8T = (uint8_t *)V8T;
     a.scales = scales;
     a.ws = (double *)workspace;
     a.chunk_rows = fkv::kFp8ChunkRows;
-    a.n_kchunks = (int)((slab + a.Lq + fkv::kFp8ChunkRows - 1) / fkv::kFp8ChunkRows);
+    a.n_kchunks = (int)(((int64_t)slab + a.Lq + fkv::kFp8ChunkRows - 1) / fkv::kFp8ChunkRows);
     a.n_qchunks = (a.Lq + fkv::kFp8ChunkRows - 1) / fkv::kFp8ChunkRows;
     (void)hipGetLastError();
     return device_status(fkv::launch_fp8_pack(a, (hipStream_t)stream), "fkv_fp8_pack launch");
@@ -843,7 +856,7 @@ fkv_status fkv_chunk_attention_fp8(const fkv_shape *shape, const void *Q8, const
     a.n_blocks = blocks;
     a.part = (float *)workspace;
     a.fp8_scales = scales;
-    a.fp8_rows = (slab + a.Lq + 63) / 64 * 64;
+    a.fp8_rows = ((int64_t)slab + a.Lq + 63) / 64 * 64;
     (void)hipGetLastError();
     return device_status(fkv::launch_attention_fp8(a, shape->head_dim, (hipStream_t)stream),
                          "fkv_chunk_attention_fp8 launch");

@@ -51,6 +51,8 @@ class CompressedLayer:
                  cap_frames: int, chunk_frames: int, seg_tokens: int, dtype: str,
                  budgets: Sequence, device="cuda", slab: Optional[int] = None,
                  balanced: bool = True, overlap: bool = True, in_place: Optional[bool] = None):
+        if len(budgets) != n_heads:
+            raise ValueError(f"{len(budgets)} head budgets for {n_heads} heads")
         self.shape = make_shape(n_heads, head_dim, frame_tokens, hist_frames, cap_frames,
                                 chunk_frames, seg_tokens, dtype)
         self.heads = make_heads(budgets)
@@ -156,30 +158,48 @@ class CompressedLayer:
         fkv_chunk_attention_static(self.shape, self.heads, K_hist, V_hist, frame_slot, Q, K_cur, V_cur,
                                    self.scale, O, lse, workspace)
 
-    def step(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse=None):
+    def step(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse=None, events=None):
+        """One AR step of the layer.  ``events`` (optional) maps a launch name to
+        a pair of torch.cuda.Events that are recorded around that attention
+        launch on the stream it runs on ("attention", or "static_attention" and
+        "dynamic_attention" in the two-stream step), for per-launch timing."""
+        def mark(name, i, stream):
+            if events is not None and name in events:
+                events[name][i].record(stream)
         if self.side is None:
+            cur = torch.cuda.current_stream(self.device)
             if self.static_in_place and not self.has_dynamic:
+                mark("attention", 0, cur)
                 self.attention_static(K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse, self.attn_workspace)
+                mark("attention", 1, cur)
                 return
             self.compress(K_hist, V_hist, frame_slot, K_cur)
+            mark("attention", 0, cur)
             self.attention(Q, K_cur, V_cur, O, lse)
+            mark("attention", 1, cur)
             return
         main = torch.cuda.current_stream(self.device)
         args = (self.Kc, self.Vc, self.kv_len, K_cur, V_cur, self.scale, O, lse)
         self.side.wait_stream(main)
         with torch.cuda.stream(self.side):
             if self.static_in_place:
+                mark("static_attention", 0, self.side)
                 self.attention_static(K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse, self.attn_workspace2)
+                mark("static_attention", 1, self.side)
             else:
                 self.compress_static(K_hist, V_hist, frame_slot)
+                mark("static_attention", 0, self.side)
                 fkv_chunk_attention_heads(self.shape, self.static_heads, Q, *args[:7], lse=lse,
                                           workspace=self.attn_workspace2)
+                mark("static_attention", 1, self.side)
         for t in (K_hist, V_hist, Q, K_cur, V_cur, O) + ((lse,) if lse is not None else ()):
             t.record_stream(self.side)
         self.score(K_hist, frame_slot, K_cur)
         self.select_compact(K_hist, V_hist, frame_slot)
+        mark("dynamic_attention", 0, main)
         fkv_chunk_attention_heads(self.shape, self.dynamic_heads, Q, *args[:7], lse=lse,
                                   workspace=self.attn_workspace)
+        mark("dynamic_attention", 1, main)
         main.wait_stream(self.side)
 
 
@@ -290,6 +310,8 @@ class RolloutStack:
         return self._shapes[H]
 
     def _budget_array(self, budgets):
+        if len(budgets) != self.n_heads:
+            raise ValueError(f"{len(budgets)} head budgets for {self.n_heads} heads")
         key = tuple((int(b.type), int(b.sink_frames), int(b.recent_frames), int(b.keep_k), int(b.scope))
                     for b in budgets)
         if key not in self._heads:

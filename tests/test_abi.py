@@ -319,3 +319,55 @@ def test_kept_tokens_max_matches_oracle_selection(fkv, oracle_lib):
                                            b.sink_frames, b.recent_frames, b.keep_k, b.scope)
             seen.add(sum(min(g * L + L, H * F) - g * L for g in kept[:cnt]))
         assert max(seen) == bound
+
+
+def test_byte_ranges_beyond_32_bits_rejected(fkv):
+    """Frames, chunks and a head's cache that span 2^31 bytes or more are shape
+    errors (the kernels address them through 32-bit buffer ranges), returned
+    before any device work."""
+    heads = _heads(fkv)
+    # a chunk of 8.4M bf16 tokens x 128 dims = 2^31 bytes
+    big_chunk = _shape(fkv, frame_tokens=1 << 16, chunk_frames=128, seg_tokens=1 << 16, hist_frames=1, cap_frames=1)
+    assert _call_static(fkv, big_chunk, heads) == 2
+    assert "chunk" in fkv.fkv_last_error()
+    # one frame of 2^23 fp32 tokens x 64 dims = 2^31 bytes
+    big_frame = _shape(fkv, head_dim=64, dtype="f32", frame_tokens=1 << 23, seg_tokens=1 << 23,
+                       hist_frames=1, cap_frames=1)
+    assert _call_static(fkv, big_frame, heads) == 2
+    # a 256-slot cache of 2^16-token bf16 frames at d = 128: 2^32 bytes per head
+    big_cache = _shape(fkv, frame_tokens=1 << 16, seg_tokens=1 << 16, hist_frames=4, cap_frames=256)
+    assert _call_static(fkv, big_cache, heads) == 2
+    # just below: 2^14 tokens x 256 B = 4 MiB frames, 64 slots = 256 MiB per head
+    ok = _shape(fkv, frame_tokens=1 << 14, seg_tokens=1 << 14, hist_frames=4, cap_frames=64)
+    assert fkv.fkv_num_segments(ok) == 4
+
+
+def test_fp8_sizes_bound_slab(fkv):
+    """fkv_fp8_sizes rejects a slab above the cache's token count (its row
+    arithmetic is 64-bit, so nothing overflows below that bound)."""
+    shape = _shape(fkv)                      # cap 4 frames x 64 tokens
+    L = fkv.lib()
+    out = [ctypes.c_size_t(0) for _ in range(4)]
+    args = [ctypes.byref(o) for o in out]
+    assert L.fkv_fp8_sizes(ctypes.byref(shape), 256, *args) == 0
+    assert out[1].value == 2 * (256 + 64) * 128
+    assert L.fkv_fp8_sizes(ctypes.byref(shape), 257, *args) == 1
+    assert L.fkv_fp8_sizes(ctypes.byref(shape), 2**31 - 1, *args) == 1
+
+
+def test_binding_rejects_wrong_head_count(fkv):
+    """The binding checks that the fkv_head array has exactly shape.n_heads
+    entries before any C call reads it."""
+    shape = _shape(fkv)                      # 2 heads
+    one = fkv.make_heads([W.HeadBudget(W.STATIC, 1, 1)])
+    three = fkv.make_heads([W.HeadBudget(W.STATIC, 1, 1)] * 3)
+    for heads in (one, three):
+        with pytest.raises(ValueError, match="entries"):
+            fkv.fkv_kept_tokens_max(shape, heads, 0)
+        with pytest.raises(ValueError, match="entries"):
+            fkv.fkv_score_workspace_size(shape, heads)
+        with pytest.raises(ValueError, match="entries"):
+            fkv.slab_tokens(shape, heads)
+    with pytest.raises(TypeError):
+        fkv.fkv_score_workspace_size(shape, [W.HeadBudget(W.STATIC, 1, 1)] * 2)
+    assert fkv.fkv_score_stats_size(shape, None, pooled=True) > 0
