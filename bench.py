@@ -55,11 +55,13 @@ def parse():
     p.add_argument("--cpu-rows-1080p", type=int, default=512,
                    help="query rows per head in the 1080P CPU oracle sample (extrapolated to 24480)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--step", default="pipelined", choices=["pipelined", "serial"],
-                   help="timed step: pipelined (static heads on a side stream) or the four calls "
-                        "one after another on one stream")
+    p.add_argument("--step", default="paged", choices=["paged", "paged2", "compact", "serial"],
+                   help="timed step: paged (score + select in one launch, then one attention launch over "
+                        "every head read in place), paged2 (the same with the static heads on a side "
+                        "stream), compact (static heads on a side stream, dynamic heads scored, compacted "
+                        "and attended), or serial (the four calls of the compacting path on one stream)")
     p.add_argument("--static", default="in_place", choices=["in_place", "gather"],
-                   help="pipelined step: static heads attended in place from the cache, or gathered "
+                   help="compact step: static heads attended in place from the cache, or gathered "
                         "into the compressed buffers first")
     p.add_argument("--no-rollout", action="store_true",
                    help="skip the measured 30-layer x 4-step rollouts (10 and 60 chunks)")
@@ -236,11 +238,23 @@ def layer_budgets(layer):
             for h in layer.heads]
 
 
+def step_mode_of(args, cfg):
+    """The layer's step mode for the timed step (the paged modes fall back to
+    the compacting step where the shape does not allow them)."""
+    from paper_2605_09681_amd.layer import paged_supported
+    if args.step in ("paged", "paged2") and paged_supported(cfg.dtype, cfg.frame_tokens, cfg.seg_tokens,
+                                                           cfg.cap_frames):
+        return args.step
+    return "compact"
+
+
 def make_layers(cfg, n, args, budgets=None):
     from paper_2605_09681_amd.layer import CompressedLayer
+    mode = step_mode_of(args, cfg)
     return [CompressedLayer(cfg.n_heads, cfg.head_dim, cfg.frame_tokens, cfg.hist_frames, cfg.cap_frames,
                             cfg.chunk_frames, cfg.seg_tokens, cfg.dtype, cfg.heads if budgets is None else budgets,
-                            balanced=args.schedule == "balanced", in_place=args.static == "in_place")
+                            balanced=args.schedule == "balanced",
+                            in_place=args.static == "in_place" if mode == "compact" else None, step_mode=mode)
             for _ in range(n)]
 
 
@@ -251,13 +265,13 @@ def timed_steps(cfg, layers, bufs, slots, args, mode):
     import numpy as np
     import torch
     stream = torch.cuda.current_stream()
-    names = (("static_attention", "dynamic_attention") if mode == "pipelined" else ("attention",))
+    names = ("attention",) if mode in ("paged", "serial") else ("static_attention", "dynamic_attention")
     events = [{n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
               for _ in range(args.steps)]
 
     def step(i, ev=None):
         L, b = layers[i % len(layers)], bufs[i % len(layers)]
-        if mode == "pipelined":
+        if mode != "serial":
             L.step(b["K_hist"], b["V_hist"], slots, b["Q"], b["K_cur"], b["V_cur"], b["O"], events=ev)
             return
         L.score(b["K_hist"], slots, b["K_cur"])
@@ -281,7 +295,7 @@ def timed_steps(cfg, layers, bufs, slots, args, mode):
     return wall_ms, launch_ms
 
 
-def launch_rooflines(cfg, layer, launch_ms, traffic):
+def launch_rooflines(cfg, layer, launch_ms, traffic, mode):
     """Per attention launch of the timed step: algorithmic FLOP, mean ms,
     achieved TFLOP/s and fraction of the bf16 peak."""
     import numpy as np
@@ -293,12 +307,19 @@ def launch_rooflines(cfg, layer, launch_ms, traffic):
     groups = {"static_attention": [h for h, b in enumerate(budgets) if b.type == W.STATIC],
               "dynamic_attention": [h for h, b in enumerate(budgets) if b.type == W.DYNAMIC],
               "attention": list(range(cfg.n_heads))}
-    kernels = {"static_attention": "fkv_chunk_attention_static: attn_bf16_kernel<128, balanced, paged> + "
-                                   "attn_merge_kernel<128, paged> (static heads, history read in place)",
-               "dynamic_attention": "fkv_chunk_attention_heads: attn_bf16_kernel<128, balanced> + "
-                                    "attn_merge_kernel<128> (dynamic heads, compacted history)",
-               "attention": "fkv_chunk_attention: attn_bf16_kernel<128, balanced> + attn_merge_kernel<128> "
-                            "(all heads, compacted history)"}
+    paged = "attn_bf16_kernel<128, balanced, paged> + attn_merge_kernel<128, paged>"
+    plain = "attn_bf16_kernel<128, balanced> + attn_merge_kernel<128>"
+    kernels = {
+        "paged": {"attention": f"fkv_chunk_attention_paged: {paged} (all heads, every kept history read in "
+                               "place from the cache)"},
+        "paged2": {"static_attention": f"fkv_chunk_attention_paged: {paged} (static heads, in place)",
+                   "dynamic_attention": f"fkv_chunk_attention_paged: {paged} (dynamic heads, kept segments "
+                                        "read in place)"},
+        "compact": {"static_attention": f"fkv_chunk_attention_static: {paged} (static heads, in place)",
+                    "dynamic_attention": f"fkv_chunk_attention_heads: {plain} (dynamic heads, compacted "
+                                         "history)"},
+        "serial": {"attention": f"fkv_chunk_attention: {plain} (all heads, compacted history)"},
+    }[mode]
     out = []
     for name, ms in launch_ms.items():
         flop = attention_flop(cfg, kv_all, groups[name])
@@ -310,6 +331,47 @@ def launch_rooflines(cfg, layer, launch_ms, traffic):
                     "avg_launch_ms": round(avg, 4),
                     "launch_ms_p10_p50_p90": [round(float(v), 4) for v in np.percentile(ms, [10, 50, 90])]})
     return out
+
+
+def measure_step_parts(cfg, layers, bufs, slots, stream, mode, reps=50):
+    """The paged step's two launches one after another with HIP events between
+    them: fkv_score_select (per-frame sums, the per-head reduction and the
+    BottomK selection in one kernel; algorithmic bytes = the dynamic heads'
+    keys of frames 0..H) and fkv_chunk_attention_paged over all heads."""
+    import numpy as np
+    import torch
+    import workloads as W
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+    for i in range(reps + 5):
+        L, b = layers[i % len(layers)], bufs[i % len(layers)]
+        e = ev[i - 5] if i >= 5 else None
+        if e:
+            e[0].record(stream)
+        L.score_select(b["K_hist"], slots, b["K_cur"])
+        if e:
+            e[1].record(stream)
+        L.attention_paged(b["K_hist"], b["V_hist"], slots, b["Q"], b["K_cur"], b["V_cur"], b["O"])
+        if e:
+            e[2].record(stream)
+    torch.cuda.synchronize()
+    t = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2])] for e in ev])
+    n_dyn = sum(1 for b in cfg.heads if b.type == W.DYNAMIC)
+    score_bytes = n_dyn * (cfg.hist_frames + 1) * cfg.frame_tokens * cfg.head_dim * cfg.esize
+    sm, am = float(t[:, 0].mean()), float(t[:, 1].mean())
+    kv = layers[0].kv_len.cpu().numpy().astype(np.int64)
+    st = static_kv_len(cfg, layer_budgets(layers[0]))
+    flop = attention_flop(cfg, [st[h] if st[h] is not None else int(kv[h]) for h in range(cfg.n_heads)])
+    return {"score_select_ms": round(sm, 4),
+            "score_select_GB_s": round(score_bytes / (sm * 1e-3) / 1e9, 1),
+            "score_select_frac_of_hbm_peak": round(score_bytes / (sm * 1e-3) / 1e9 / PEAK_HBM_GBS, 3),
+            "score_select_algorithmic_bytes": score_bytes,
+            "attention_paged_ms": round(am, 4),
+            "attention_paged_TFLOP_s": round(flop / (am * 1e-3) / 1e12, 1),
+            "attention_paged_frac_of_bf16_peak": round(flop / (am * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "serial_sum_ms": round(sm + am, 4),
+            "ms_p10_p50_p90": {"score_select": [round(float(v), 4) for v in np.percentile(t[:, 0], [10, 50, 90])],
+                               "attention_paged": [round(float(v), 4) for v in np.percentile(t[:, 1], [10, 50, 90])]},
+            "note": "HIP events between the two launches on one stream, rotating buffer copies"}
 
 
 def load_traffic(path, workload):
@@ -366,9 +428,11 @@ def main():
     breakdown = stage_report(cfg, layers[0], stage)
 
     traffic = load_traffic(args.traffic_json, cfg.name)
-    wall_ms, launch_ms = timed_steps(cfg, layers, bufs, slots, args, args.step)
-    launches = launch_rooflines(cfg, layers[0], launch_ms, traffic)
+    mode = args.step if args.step == "serial" else step_mode_of(args, cfg)
+    wall_ms, launch_ms = timed_steps(cfg, layers, bufs, slots, args, mode)
+    launches = launch_rooflines(cfg, layers[0], launch_ms, traffic, mode)
     dominant = max(launches, key=lambda r: r["avg_launch_ms"])
+    step_parts = measure_step_parts(cfg, layers, bufs, slots, stream, mode) if mode == "paged" else None
 
     d, F, H, Lq = cfg.head_dim, cfg.frame_tokens, cfg.hist_frames, cfg.lq
     out = {
@@ -393,17 +457,24 @@ def main():
                         "is rollout_480p",
             "rotating_copies": args.copies,
             "attention_schedule": args.schedule,
-            "step": (("static heads (attention read in place from the cache" if args.static == "in_place" else
-                      "static heads (gather + attention") +
-                     ") on a side stream, dynamic heads (score + select/compact + attention) on the main stream"
-                     if args.step == "pipelined" else
-                     "the four calls one after another on one stream"),
+            "step": {"paged": "fkv_score_select (dynamic heads: scores + kept segments, one launch), then one "
+                              "fkv_chunk_attention_paged launch over all 12 heads with every kept history read "
+                              "in place from the cache (no compaction, no gather)",
+                     "paged2": "static heads' in-place attention on a side stream; dynamic heads: "
+                               "fkv_score_select, then in-place attention",
+                     "compact": ("static heads (attention read in place from the cache" if args.static ==
+                                 "in_place" else "static heads (gather + attention") +
+                                ") on a side stream, dynamic heads (score + select/compact + attention) on the "
+                                "main stream",
+                     "serial": "the four calls of the compacting path one after another on one stream"}[mode],
         },
         "roofline": {k: v for k, v in dominant.items() if k != "launch_ms_p10_p50_p90"},
         "roofline_launches": launches,
         "breakdown_serial": breakdown,
         "attn_tflops": dominant["achieved"],
     }
+    if step_parts is not None:
+        out["step_parts"] = step_parts
     extras = None
     if not args.no_extras:
         extras = measure_extras(args, cfg, slots, bufs, layers, stream)
@@ -458,7 +529,7 @@ def measure_extras(args, cfg, slots, bufs, layers, stream):
     d, F, H, Lq = cfg.head_dim, cfg.frame_tokens, cfg.hist_frames, cfg.lq
     L0, b = layers[0], bufs[0]
     pooled = torch.empty((L0.n_seg,), dtype=torch.float32, device="cuda")
-    ws = torch.empty(max(fkv.fkv_score_pooled_workspace_size(L0.shape), 1), dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(max(fkv.fkv_score_pooled_workspace_size(L0.shape), 1), dtype=torch.uint8, device="cuda")
     pooled_ms = _time_ms(lambda: fkv.fkv_score_pooled(L0.shape, b["K_hist"], slots, b["K_cur"], pooled, ws),
                          20, stream)
     pooled_bytes = cfg.n_heads * (H + 1) * F * d * 2
@@ -515,8 +586,8 @@ def measure_extras(args, cfg, slots, bufs, layers, stream):
     del full
 
     return {
-        "step_parts": dict(parts, note="each timed alone over the rotated buffer copies; the step runs the "
-                                       "first two on two streams after the dynamic compression"),
+        "compact_step_launches": dict(parts, note="the compacting two-stream step's launches, each timed alone "
+                                                  "over the rotated buffer copies"),
         "fp8_attention": {
             "attention_ms": round(fp8_ms, 4), "TFLOP_s": round(attn_flop / (fp8_ms * 1e-3) / 1e12, 1),
             "peak_TFLOP_s": PEAK_FP8_TFLOPS,
@@ -539,10 +610,12 @@ def measure_extras(args, cfg, slots, bufs, layers, stream):
 
 def measure_sweep(args, b, stream, reps=30):
     """The keep-fraction x segment-length sweep at 480P: per point the four
-    calls one after another (score, select + compact, static gather, 12-head
-    attention), mean ms per kernel over `reps` units with HIP events, achieved
-    GB/s of the HBM kernels and attention TFLOP/s.  Keep 100% also keeps every
-    frame of the static heads (full-attention equivalence)."""
+    calls of the compacting path one after another (score, select + compact,
+    static gather, 12-head attention), mean ms per kernel over `reps` units
+    with HIP events, achieved GB/s of the HBM kernels and attention TFLOP/s;
+    and, where the shape allows it, the paged step (score + select, then one
+    in-place attention launch).  Keep 100% also keeps every frame of the
+    static heads (full-attention equivalence)."""
     import numpy as np
     import workloads as W
     out = []
@@ -554,11 +627,18 @@ def measure_sweep(args, b, stream, reps=30):
             layer = make_layers(cfg, 1, args)[0]
             stage = staged_breakdown([layer], [b], slots, reps, stream, warm=3)
             rep = stage_report(cfg, layer, stage)
-            out.append({"seg_tokens": L, "keep_fraction": frac, "unit_ms": rep["serial_unit_ms"],
-                        "ms": rep["ms"], "GB_s": rep["GB_s"], "frac_of_hbm_peak": rep["frac_of_hbm_peak"],
-                        "attention_TFLOP_s": rep["attention_TFLOP_s"],
-                        "attention_frac_of_bf16_peak": rep["attention_frac_of_bf16_peak"],
-                        "kv_len_dynamic": int(layer.kv_len[6].item())})
+            rec = {"seg_tokens": L, "keep_fraction": frac, "unit_ms_compact_serial": rep["serial_unit_ms"],
+                   "ms": rep["ms"], "GB_s": rep["GB_s"], "frac_of_hbm_peak": rep["frac_of_hbm_peak"],
+                   "attention_TFLOP_s": rep["attention_TFLOP_s"],
+                   "attention_frac_of_bf16_peak": rep["attention_frac_of_bf16_peak"],
+                   "kv_len_dynamic": int(layer.kv_len[6].item())}
+            if layer.step_mode == "paged":
+                parts = measure_step_parts(cfg, [layer], [b], slots, stream, "paged", reps=reps)
+                rec["paged_unit_ms"] = parts["serial_sum_ms"]
+                rec["paged"] = {k: parts[k] for k in ("score_select_ms", "score_select_GB_s",
+                                                      "attention_paged_ms", "attention_paged_TFLOP_s",
+                                                      "attention_paged_frac_of_bf16_peak")}
+            out.append(rec)
             del layer
     return {"points": out,
             "note": "one buffer set (cache 202 MB: the rotating copies are freed first), serial calls"}
@@ -581,11 +661,14 @@ def measure_1080p(args, stream):
     rep = stage_report(c10, layer, stage)
     a10 = argparse.Namespace(**vars(args))
     a10.steps, a10.warmup = 6, 2
-    wall, launch_ms = timed_steps(c10, [layer], [b], slots10, a10, "pipelined")
-    launches = launch_rooflines(c10, layer, launch_ms, None)
+    mode = step_mode_of(args, c10)
+    wall, launch_ms = timed_steps(c10, [layer], [b], slots10, a10, mode)
+    launches = launch_rooflines(c10, layer, launch_ms, None, mode)
+    parts = measure_step_parts(c10, [layer], [b], slots10, stream, mode, reps=6) if mode == "paged" else None
     del layer, b
     torch.cuda.empty_cache()
-    return {"step_ms": round(wall, 3), "breakdown_serial": rep, "step_launches": launches,
+    return {"step_ms": round(wall, 3), "step_mode": mode, "step_parts": parts, "breakdown_serial": rep,
+            "step_launches": launches,
             "workload": "wan1.3b-1080p-layer: 12 heads x d128, 8160 tokens/frame, 21-frame history, "
                         "3-frame chunk; heads 0-5 static (sink 1 + recent 6), 6-11 dynamic (sink 1 + 10 of 20)",
             "note": "device-generated inputs, one buffer set"}

@@ -122,7 +122,13 @@ fkv_status fkv_compress_static(const fkv_shape *shape, const fkv_head *heads,
                                int32_t slab, int32_t *kv_len, void *stream);
 
 /* Device workspace fkv_score_segments needs for `shape` and the dynamic heads
- * of `heads` (a multiple of 256 bytes; 0 when no head is dynamic or H = 0). */
+ * of `heads` (a multiple of 256 bytes; 0 when no head is dynamic or H = 0).
+ * Every scoring workspace (this one, fkv_score_pooled_workspace_size's) starts
+ * with the arrival counters of the one-launch reduction: it must be
+ * zero-filled once before its first use (e.g. hipMemset to 0), and every
+ * scoring call leaves the counters at zero again when it completes, so
+ * consecutive calls need nothing more.  Calls that share a workspace must be
+ * ordered (one stream). */
 fkv_status fkv_score_workspace_size(const fkv_shape *shape, const fkv_head *heads,
                                     size_t *bytes);
 
@@ -134,9 +140,10 @@ fkv_status fkv_score_workspace_size(const fkv_shape *shape, const fkv_head *head
  * fp64 and summed in fp64: dot = sum a*b, na = sum a*a, nb = sum b*b; then
  * scores[h][g] = (float)(dot / sqrt(na*nb)) rounded to nearest even, or 0 when
  * na*nb == 0.  The cosine is taken over the flattened segment (tokens x d).
- * `workspace` holds fp64 partial sums (device memory of at least
- * fkv_score_workspace_size bytes; its contents need no initialisation).  Rows
- * of static heads are not touched.  H = 0 enqueues nothing. */
+ * `workspace` holds the arrival counters and fp64 partial sums (device memory
+ * of at least fkv_score_workspace_size bytes, zero-filled before its first
+ * use, see above).  Sums are in a fixed order, so the result is the same on
+ * every run.  Rows of static heads are not touched.  H = 0 enqueues nothing. */
 fkv_status fkv_score_segments(const fkv_shape *shape, const fkv_head *heads,
                               const void *K_hist, const int32_t *frame_slot,
                               const void *K_cur, float *scores, void *workspace,
@@ -186,7 +193,8 @@ fkv_status fkv_score_pooled_workspace_size(const fkv_shape *shape, size_t *bytes
  * i.e. the cosine over heads x tokens x head_dim elements (0 when the
  * product of the sums is 0).  Same exact fp64 products, fp64 sums and single
  * rounding as fkv_score_segments.  scores: float [n_seg] (device).  The
- * workspace needs no initialisation.  H = 0 enqueues nothing. */
+ * workspace is zero-filled before its first use, as for fkv_score_segments.
+ * H = 0 enqueues nothing. */
 fkv_status fkv_score_pooled(const fkv_shape *shape, const void *K_hist,
                             const int32_t *frame_slot, const void *K_cur,
                             float *scores, void *workspace, size_t workspace_bytes,
@@ -201,9 +209,10 @@ fkv_status fkv_score_pooled(const fkv_shape *shape, const void *K_hist,
  * `stats`, a caller-owned device buffer of fkv_score_stats_size bytes.
  * fkv_score_segments_cached then streams frames H-1 and H only and writes the
  * same scores fkv_score_segments (pooled = 0) or fkv_score_pooled (pooled = 1)
- * would: per listed head [n_heads][n_seg] (rows of static heads untouched),
- * or one row [n_seg].  Sums are fp64 in a fixed order and the cosine is rounded
- * once to fp32; only the grouping of the fp64 sums differs from the full pass.
+ * would, bit for bit: per listed head [n_heads][n_seg] (rows of static heads
+ * untouched), or one row [n_seg].  Both reduce every per-frame sum with the
+ * same fixed-order tree, and fkv_score_segments sums a segment's per-frame
+ * terms in the same frame order as this call.
  * pooled = 0 lists the dynamic heads of `heads`; pooled = 1 lists every head
  * and `heads` may be NULL.  stats stays valid until the history (K_hist
  * contents or frame_slot) changes; the caller runs fkv_score_history again
@@ -232,6 +241,27 @@ fkv_status fkv_select_compact_pooled(const fkv_shape *shape, const fkv_head *hea
                                      const void *V_hist, const int32_t *frame_slot,
                                      int32_t *kept_seg, void *Kc, void *Vc,
                                      int32_t slab, int32_t *kv_len, void *stream);
+
+/* BottomK selection alone (Sec. 4.3, Eq. 3): the kept_seg and kv_len that
+ * fkv_select_compact writes for every FKV_DYNAMIC head, without copying any
+ * K/V row -- for attention that reads the kept segments in place
+ * (fkv_chunk_attention_paged).  scores is float [n_heads][n_seg], or, with
+ * shared_row = 1, one row [n_seg] shared by every dynamic head (the pooled
+ * first-block proxy).  Rows of static heads are not touched; with H = 0 every
+ * dynamic head gets kv_len 0. */
+fkv_status fkv_select(const fkv_shape *shape, const fkv_head *heads, const float *scores,
+                      int32_t shared_row, int32_t *kept_seg, int32_t *kv_len, void *stream);
+
+/* fkv_score_segments followed by fkv_select in ONE kernel launch: the
+ * workgroup that completes a dynamic head's scores also selects its kept
+ * segments.  scores, kept_seg and kv_len are written exactly as the two calls
+ * write them.  Workspace as in fkv_score_segments (same size; zero-filled
+ * before its first use).  With H = 0 the dynamic heads get kv_len 0. */
+fkv_status fkv_score_select(const fkv_shape *shape, const fkv_head *heads,
+                            const void *K_hist, const int32_t *frame_slot,
+                            const void *K_cur, float *scores, int32_t *kept_seg,
+                            int32_t *kv_len, void *workspace, size_t workspace_bytes,
+                            void *stream);
 
 /* Device workspace fkv_chunk_attention takes for its balanced schedule on the
  * CURRENT device (hipGetDevice): 2 x the device's compute units, rounded down
@@ -311,6 +341,33 @@ fkv_status fkv_chunk_attention_static(const fkv_shape *shape, const fkv_head *he
                                       const void *K_cur, const void *V_cur, float scale,
                                       void *O, float *lse, void *workspace,
                                       size_t workspace_bytes, void *stream);
+
+/* Chunk attention with every listed head's kept history read in place from
+ * the cache (Eq. 2 for static heads, Eq. 4 for dynamic heads), without a
+ * compressed copy.  The keys of head h are its kept history tokens in
+ * ascending logical order, then K_cur[h]; likewise the values:
+ *   FKV_STATIC:  the frames [0, min(sink, H)) U [max(H - recent, 0), H), as
+ *                in fkv_chunk_attention_static;
+ *   FKV_DYNAMIC: the segments kept_seg[h][0..] covering kv_len[h] tokens, as
+ *                fkv_select (or fkv_score_select) writes them (kv_len is read
+ *                on the device and clamped to H*F).
+ * The result is bit for bit what fkv_compress_static / fkv_select_compact
+ * followed by fkv_chunk_attention_heads computes for the same heads.
+ * head_list (HOST int32, n_list distinct heads) selects the heads; NULL means
+ * every head.  Only the listed heads' rows of O and lse are written.
+ * Workspace and schedule as in fkv_chunk_attention.  bf16 only, frame_tokens
+ * >= 64; when a dynamic head is listed, also min(seg_tokens, frame_tokens)
+ * >= 64 and cap_frames * (frame_tokens / min(seg_tokens, frame_tokens)) <=
+ * 256 (the page table holds one byte per piece): FKV_ERR_SHAPE otherwise.
+ * kept_seg [n_heads][n_seg] and kv_len [n_heads] are device arrays (needed
+ * when a dynamic head is listed and H > 0). */
+fkv_status fkv_chunk_attention_paged(const fkv_shape *shape, const fkv_head *heads,
+                                     const int32_t *head_list, int32_t n_list,
+                                     const void *K_hist, const void *V_hist,
+                                     const int32_t *frame_slot, const int32_t *kept_seg,
+                                     const int32_t *kv_len, const void *Q, const void *K_cur,
+                                     const void *V_cur, float scale, void *O, float *lse,
+                                     void *workspace, size_t workspace_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
  * Offline head profiling (Sec. 4.1, Eq. 1).  A profiling pass runs the layer

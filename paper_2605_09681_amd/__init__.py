@@ -45,10 +45,11 @@ FKV_MAX_HEADS, FKV_MAX_FRAMES, FKV_MAX_SEGMENTS = 64, 256, 4096
 EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_score_workspace_size", "fkv_score_segments", "fkv_select_compact",
             "fkv_append_frames", "fkv_score_pooled_workspace_size", "fkv_score_pooled",
-            "fkv_select_compact_pooled", "fkv_score_stats_size", "fkv_score_history",
+            "fkv_select_compact_pooled", "fkv_select", "fkv_score_select",
+            "fkv_score_stats_size", "fkv_score_history",
             "fkv_score_segments_cached",
             "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_chunk_attention_heads",
-            "fkv_chunk_attention_static",
+            "fkv_chunk_attention_static", "fkv_chunk_attention_paged",
             "fkv_fp8_sizes", "fkv_fp8_pack",
             "fkv_chunk_attention_fp8", "fkv_attention_mass_workspace_size", "fkv_attention_mass",
             "fkv_classify_heads", "fkv_last_error")
@@ -111,6 +112,10 @@ def lib():
         L.fkv_score_pooled.restype = ctypes.c_int
         L.fkv_select_compact_pooled.argtypes = [S, Hd, P, P, P, P, P, P, P, I32, P, P]
         L.fkv_select_compact_pooled.restype = ctypes.c_int
+        L.fkv_select.argtypes = [S, Hd, P, I32, P, P, P]
+        L.fkv_select.restype = ctypes.c_int
+        L.fkv_score_select.argtypes = [S, Hd, P, P, P, P, P, P, P, SZ, P]
+        L.fkv_score_select.restype = ctypes.c_int
         L.fkv_attention_workspace_size.argtypes = [S, ctypes.POINTER(SZ)]
         L.fkv_attention_workspace_size.restype = ctypes.c_int
         L.fkv_chunk_attention.argtypes = [S, P, P, P, I32, P, P, P, F, P, P, P, SZ, P]
@@ -125,6 +130,8 @@ def lib():
         L.fkv_chunk_attention_heads.restype = ctypes.c_int
         L.fkv_chunk_attention_static.argtypes = [S, Hd, P, P, P, P, P, P, F, P, P, P, SZ, P]
         L.fkv_chunk_attention_static.restype = ctypes.c_int
+        L.fkv_chunk_attention_paged.argtypes = [S, Hd, P, I32, P, P, P, P, P, P, P, P, F, P, P, P, SZ, P]
+        L.fkv_chunk_attention_paged.restype = ctypes.c_int
         L.fkv_fp8_sizes.argtypes = [S, I32] + [ctypes.POINTER(SZ)] * 4
         L.fkv_fp8_sizes.restype = ctypes.c_int
         L.fkv_fp8_pack.argtypes = [S, P, P, P, I32, P, P, P, P, P, P, P, P, SZ, P]
@@ -272,8 +279,8 @@ def fkv_score_segments(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, score
     kc = _check(K_cur, "K_cur", dt, (shape.n_heads, _lq(shape), shape.head_dim))
     sc = _check(scores, "scores", torch.float32, (shape.n_heads, n_seg))
     need = fkv_score_workspace_size(shape, heads)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=K_hist.device)
+    if workspace is None:   # zero-filled: the scoring workspace starts with arrival counters
+        workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=K_hist.device)
     ws = _check(workspace, "workspace", torch.uint8)
     _raise(lib().fkv_score_segments(ctypes.byref(shape), _heads(shape, heads), kh, sl, kc, sc, ws,
                                     workspace.numel(), _stream(stream)))
@@ -351,8 +358,8 @@ def fkv_score_pooled(shape: fkv_shape, K_hist, frame_slot, K_cur, scores,
     kc = _check(K_cur, "K_cur", dt, (shape.n_heads, _lq(shape), shape.head_dim))
     sc = _check(scores, "scores", torch.float32, (n_seg,))
     need = fkv_score_pooled_workspace_size(shape)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=K_hist.device)
+    if workspace is None:   # zero-filled: the scoring workspace starts with arrival counters
+        workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=K_hist.device)
     ws = _check(workspace, "workspace", torch.uint8)
     _raise(lib().fkv_score_pooled(ctypes.byref(shape), kh, sl, kc, sc, ws, workspace.numel(),
                                   _stream(stream)))
@@ -364,6 +371,39 @@ def fkv_select_compact_pooled(shape: fkv_shape, heads, scores, K_hist, V_hist, f
     """fkv_select_compact with one shared score row [n_seg]."""
     _select_compact(shape, heads, scores, K_hist, V_hist, frame_slot, kept_seg, Kc, Vc, kv_len,
                     stream, pooled=True)
+
+
+def fkv_select(shape: fkv_shape, heads, scores, kept_seg, kv_len, shared_row: bool = False, stream=None):
+    """BottomK only: kept_seg and kv_len of the dynamic heads, no copy.
+    scores is [n_heads][n_seg], or [n_seg] with shared_row (the pooled proxy)."""
+    n_seg = fkv_num_segments(shape)
+    sc = _check(scores, "scores", torch.float32, (n_seg,) if shared_row else (shape.n_heads, n_seg))
+    ks = _check(kept_seg, "kept_seg", torch.int32, (shape.n_heads, n_seg))
+    kl = _check(kv_len, "kv_len", torch.int32, (shape.n_heads,))
+    _raise(lib().fkv_select(ctypes.byref(shape), _heads(shape, heads), sc, int(bool(shared_row)), ks, kl,
+                            _stream(stream)))
+
+
+def fkv_score_select(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, scores, kept_seg, kv_len,
+                     workspace: Optional[torch.Tensor] = None, stream=None):
+    """fkv_score_segments + fkv_select in one launch.  If ``workspace`` is None
+    a zero-filled one is allocated (through torch's caching allocator)."""
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    n_seg = fkv_num_segments(shape)
+    kh = _check(K_hist, "K_hist", dt, hist)
+    sl = _slots(frame_slot, shape.hist_frames)
+    kc = _check(K_cur, "K_cur", dt, (shape.n_heads, _lq(shape), shape.head_dim))
+    sc = _check(scores, "scores", torch.float32, (shape.n_heads, n_seg))
+    ks = _check(kept_seg, "kept_seg", torch.int32, (shape.n_heads, n_seg))
+    kl = _check(kv_len, "kv_len", torch.int32, (shape.n_heads,))
+    need = fkv_score_workspace_size(shape, heads)
+    if workspace is None:
+        workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=K_hist.device)
+    ws = _check(workspace, "workspace", torch.uint8)
+    _raise(lib().fkv_score_select(ctypes.byref(shape), _heads(shape, heads), kh, sl, kc, sc, ks, kl, ws,
+                                  workspace.numel(), _stream(stream)))
+    return workspace
 
 
 def fkv_select_compact(shape: fkv_shape, heads, scores, K_hist, V_hist, frame_slot, kept_seg,
@@ -457,6 +497,37 @@ def fkv_chunk_attention_static(shape: fkv_shape, heads, K_hist, V_hist, frame_sl
         ws, nws = _check(workspace, "workspace", torch.uint8), workspace.numel()
     _raise(lib().fkv_chunk_attention_static(ctypes.byref(shape), _heads(shape, heads), kh, vh, sl, q, kq, vq,
                                             ctypes.c_float(scale), o, ls, ws, nws, _stream(stream)))
+
+
+def fkv_chunk_attention_paged(shape: fkv_shape, heads, K_hist, V_hist, frame_slot, kept_seg, kv_len, Q, K_cur,
+                              V_cur, scale: float, O, lse: Optional[torch.Tensor] = None,
+                              workspace: Optional[torch.Tensor] = None, head_list: Optional[Sequence[int]] = None,
+                              stream=None):
+    """Attention of the listed heads (all by default) with every head's kept
+    history read in place from K_hist / V_hist: the Eq. 2 frames of static
+    heads, the kept segments (kept_seg, kv_len from fkv_select) of dynamic
+    heads.  Only the listed heads' rows of O and lse are written."""
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    chunk = (shape.n_heads, _lq(shape), shape.head_dim)
+    n_seg = fkv_num_segments(shape)
+    kh, vh = _check(K_hist, "K_hist", dt, hist), _check(V_hist, "V_hist", dt, hist)
+    sl = _slots(frame_slot, shape.hist_frames)
+    ks = None if kept_seg is None else _check(kept_seg, "kept_seg", torch.int32, (shape.n_heads, n_seg))
+    kl = None if kv_len is None else _check(kv_len, "kv_len", torch.int32, (shape.n_heads,))
+    q = _check(Q, "Q", dt, chunk)
+    kq, vq = _check(K_cur, "K_cur", dt, chunk), _check(V_cur, "V_cur", dt, chunk)
+    o = _check(O, "O", dt, chunk)
+    ls = None if lse is None else _check(lse, "lse", torch.float32, (shape.n_heads, _lq(shape)))
+    ws, nws = None, 0
+    if workspace is not None:
+        ws, nws = _check(workspace, "workspace", torch.uint8), workspace.numel()
+    arr, n = None, 0
+    if head_list is not None:
+        ids = [int(h) for h in head_list]
+        arr, n = (ctypes.c_int32 * max(len(ids), 1))(*ids), len(ids)
+    _raise(lib().fkv_chunk_attention_paged(ctypes.byref(shape), _heads(shape, heads), arr, n, kh, vh, sl, ks, kl,
+                                           q, kq, vq, ctypes.c_float(scale), o, ls, ws, nws, _stream(stream)))
 
 
 def fkv_fp8_sizes(shape: fkv_shape, slab: int):

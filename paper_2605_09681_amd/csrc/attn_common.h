@@ -20,11 +20,14 @@ __device__ __forceinline__ int head_tiles(const AttnArgs &a, int h) {
     return (head_kvl(a, h) + a.Lq + BN - 1) / BN;
 }
 // The same for entry li of the launch's head list.  PAGED (a compile-time
-// switch): static heads read in place, whose history length follows from
-// their budgets, stored per list entry.
+// switch): heads read in place; a static entry's history length follows from
+// its budget (stored per list entry), a dynamic entry's is kv_len.
 template <bool PAGED = false>
 __device__ __forceinline__ int entry_kvl(const AttnArgs &a, int li) {
-    if constexpr (PAGED) return a.st_kept[li] * a.F;
+    if constexpr (PAGED) {
+        const int kept = a.st_kept[li];
+        if (kept >= 0) return kept * a.F;
+    }
     return head_kvl(a, a.heads.head[li]);
 }
 template <bool PAGED = false>
@@ -69,15 +72,18 @@ __device__ __forceinline__ int64_t readlane64(int64_t v, int l) {
 template <bool PAGED = false>
 __device__ __forceinline__ WorkList work_list(const AttnArgs &a) {
     const int lane = threadIdx.x & 63;
-    // entry l's head (or kept-frame count) into lane l, with uniform indices
-    // into the launch arguments (a per-lane index would copy them to private
-    // memory)
-    int e = 0;
+    // entry l's head (and, read in place, its kept-frame count) into lane l,
+    // with uniform indices into the launch arguments (a per-lane index would
+    // copy them to private memory)
+    int e = 0, kept = -1;
     for (int l = 0; l < a.heads.n; ++l)
-        if (lane == l) e = PAGED ? a.st_kept[l] : a.heads.head[l];
+        if (lane == l) {
+            e = a.heads.head[l];
+            if (PAGED) kept = a.st_kept[l];
+        }
     int T = 0;
     if (lane < a.heads.n) {
-        const int kvl = PAGED ? e * a.F : head_kvl(a, e);
+        const int kvl = kept >= 0 ? kept * a.F : head_kvl(a, e);
         T = (kvl + a.Lq + BN - 1) / BN;
     }
     long long v = (long long)a.n_qtiles * T;

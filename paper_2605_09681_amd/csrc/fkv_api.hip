@@ -195,22 +195,21 @@ fkv_status balanced_blocks(int *blocks) {
     return FKV_OK;
 }
 
-void score_geometry(const fkv_shape *s, int *unit_tokens, int *units, int64_t *unit_vecs,
-                           int *chunks) {
+// Scoring geometry: units of U = min(L, F) tokens per frame, their 16-byte
+// vectors, and the column groups (workgroups) per unit.
+void score_geometry(const fkv_shape *s, int *units, int64_t *unit_vecs, int *n_cg) {
     const int U = std::min(s->seg_tokens, s->frame_tokens);
-    *unit_tokens = U;
     *units = s->frame_tokens / U;
     *unit_vecs = (int64_t)U * s->head_dim * elem_size(s) / 16;
-    *chunks = (int)((*unit_vecs + fkv::kScoreThreads - 1) / fkv::kScoreThreads);
+    *n_cg = fkv::score_column_groups(*unit_vecs);
 }
 
 size_t score_bytes(const fkv_shape *shape, int n_list) {
     if (n_list == 0 || shape->hist_frames == 0) return 0;
-    int U, units, chunks;
+    int units, n_cg;
     int64_t uv;
-    score_geometry(shape, &U, &units, &uv, &chunks);
-    const size_t b = fkv::score_workspace_doubles(n_list, shape->hist_frames, units, chunks) * sizeof(double);
-    return (b + 255) & ~(size_t)255;
+    score_geometry(shape, &units, &uv, &n_cg);
+    return fkv::score_workspace_bytes(n_list, shape->hist_frames, units, n_cg);
 }
 
 }  // namespace
@@ -301,12 +300,18 @@ fkv_status fkv_score_workspace_size(const fkv_shape *shape, const fkv_head *head
 
 namespace {
 
-// Scoring of the heads in `list` (per head, or pooled into one row).
-enum ScoreMode { kScoreFull, kScoreHistory, kScoreCached };
+// Scoring of the heads in `list` (per head, or pooled into one row), in one
+// launch: the full pass, the history statistics or the cached scores, with an
+// optional BottomK selection of every listed head (per-head scores only).
+struct SelectOut {
+    const fkv_head *heads;
+    int32_t *kept_seg, *kv_len;
+};
 
 fkv_status score_impl(const fkv_shape *shape, const fkv::HeadList &list, bool pooled, const void *K_hist,
                       const int32_t *frame_slot, const void *K_cur, float *scores, void *workspace,
-                      void *stream, const char *what, ScoreMode mode = kScoreFull, double *stats = nullptr) {
+                      void *stream, const char *what, fkv::ScoreMode mode = fkv::kScoreModeFull,
+                      double *stats = nullptr, const SelectOut *select = nullptr) {
     fkv::ScoreArgs a;
     memset(&a, 0, sizeof a);
     a.heads = list;
@@ -316,25 +321,35 @@ fkv_status score_impl(const fkv_shape *shape, const fkv::HeadList &list, bool po
     a.K_hist = (const uint8_t *)K_hist;
     a.K_cur = (const uint8_t *)K_cur;
     a.scores = scores;
-    a.ws = (double *)workspace;
-    a.frame_bytes = (int64_t)shape->frame_tokens * shape->head_dim * es;
-    a.cur_vecs = (int64_t)shape->chunk_frames * a.frame_bytes / 16;
+    a.frame_vecs = (int64_t)shape->frame_tokens * shape->head_dim * es / 16;
+    a.cur_head_vecs = (int64_t)shape->chunk_frames * a.frame_vecs;
     a.F = shape->frame_tokens;
     a.L = shape->seg_tokens;
     a.H = shape->hist_frames;
     a.cap = shape->cap_frames;
     a.n_seg = fkv_num_segments(shape);
-    a.d = shape->head_dim;
-    a.esize = (int)es;
-    score_geometry(shape, &a.unit_tokens, &a.units_per_frame, &a.unit_vecs, &a.chunks_per_unit);
+    int64_t uv;
+    score_geometry(shape, &a.units, &uv, &a.n_cg);
+    a.unit_vecs = (int32_t)uv;
+    a.mode = mode;
+    a.t_begin = mode == fkv::kScoreModeCached ? a.H - 1 : 0;
+    a.n_frames = mode == fkv::kScoreModeFull ? a.H + 1 : mode == fkv::kScoreModeHistory ? a.H : 2;
+    fkv::score_workspace_layout(a, workspace, list.n, a.H, a.units, a.n_cg);
     for (int t = 0; t < shape->hist_frames; ++t) a.slots.slot[t] = frame_slot[t];
+    if (select) {
+        a.select = 1;
+        a.kept_seg = select->kept_seg;
+        a.kv_len = select->kv_len;
+        for (int li = 0; li < list.n; ++li) {
+            const fkv_head &b = select->heads[list.head[li]];
+            a.sink[li] = b.sink_frames;
+            a.recent[li] = b.recent_frames;
+            a.scope[li] = b.scope;
+            a.k[li] = dyn_plan(shape, b).kk;
+        }
+    }
     (void)hipGetLastError();
-    const bool f32 = shape->dtype == FKV_F32;
-    const hipStream_t st = (hipStream_t)stream;
-    hipError_t e = mode == kScoreHistory ? fkv::launch_score_history(a, f32, st)
-                 : mode == kScoreCached  ? fkv::launch_score_cached(a, f32, st)
-                                         : fkv::launch_score(a, f32, st);
-    return device_status(e, what);
+    return device_status(fkv::launch_score(a, shape->dtype == FKV_F32, (hipStream_t)stream), what);
 }
 
 // Heads of an incremental-rescoring call: every dynamic head, or every head
@@ -351,9 +366,9 @@ fkv_status stats_heads(const fkv_shape *shape, const fkv_head *heads, int32_t po
 }
 
 size_t stats_bytes(const fkv_shape *shape, int n_list) {
-    int U, units, chunks;
+    int units, n_cg;
     int64_t uv;
-    score_geometry(shape, &U, &units, &uv, &chunks);
+    score_geometry(shape, &units, &uv, &n_cg);
     return (size_t)n_list * shape->hist_frames * units * 2 * sizeof(double);
 }
 
@@ -424,7 +439,7 @@ fkv_status fkv_score_history(const fkv_shape *shape, const fkv_head *heads, int3
         return st;
     if (need == 0) return ok();
     return score_impl(shape, list, pooled, K_hist, frame_slot, K_hist, nullptr, workspace, stream,
-                      "fkv_score_history launch", kScoreHistory, stats);
+                      "fkv_score_history launch", fkv::kScoreModeHistory, stats);
 }
 
 fkv_status fkv_score_segments_cached(const fkv_shape *shape, const fkv_head *heads, int32_t pooled,
@@ -441,7 +456,7 @@ fkv_status fkv_score_segments_cached(const fkv_shape *shape, const fkv_head *hea
     if (need == 0) return ok();
     if (!K_cur || !scores) return fail(FKV_ERR_ARG, "NULL tensor pointer");
     return score_impl(shape, list, pooled, K_hist, frame_slot, K_cur, scores, workspace, stream,
-                      "fkv_score_segments_cached launch", kScoreCached, const_cast<double *>(stats));
+                      "fkv_score_segments_cached launch", fkv::kScoreModeCached, const_cast<double *>(stats));
 }
 
 fkv_status fkv_score_pooled_workspace_size(const fkv_shape *shape, size_t *bytes) {
@@ -469,6 +484,78 @@ fkv_status fkv_score_pooled(const fkv_shape *shape, const void *K_hist, const in
     for (int h = 0; h < shape->n_heads; ++h) list.head[list.n++] = h;
     return score_impl(shape, list, true, K_hist, frame_slot, K_cur, scores, workspace, stream,
                       "fkv_score_pooled launch");
+}
+
+}  // extern "C"
+
+namespace {
+
+// BottomK of the dynamic heads only (no copy): kept_seg and kv_len.
+fkv_status select_impl(const fkv_shape *shape, const fkv_head *heads, const float *scores, bool shared_row,
+                       int32_t *kept_seg, int32_t *kv_len, void *stream, const char *what) {
+    const int n_seg = fkv_num_segments(shape);
+    fkv::SelectArgs sa;
+    memset(&sa, 0, sizeof sa);
+    for (int h = 0; h < shape->n_heads; ++h) {
+        if (heads[h].type != FKV_DYNAMIC) continue;
+        const int li = sa.heads.n++;
+        sa.heads.head[li] = h;
+        sa.sink[li] = heads[h].sink_frames;
+        sa.recent[li] = heads[h].recent_frames;
+        sa.scope[li] = heads[h].scope;
+        sa.k[li] = shape->hist_frames > 0 ? dyn_plan(shape, heads[h]).kk : 0;
+    }
+    if (sa.heads.n == 0) return ok();
+    sa.scores = scores;
+    sa.score_stride = shared_row ? 0 : n_seg;
+    sa.kept_seg = kept_seg;
+    sa.kv_len = kv_len;
+    sa.F = shape->frame_tokens;
+    sa.L = shape->seg_tokens;
+    sa.H = shape->hist_frames;
+    sa.n_seg = n_seg;
+    (void)hipGetLastError();
+    return device_status(fkv::launch_select(sa, (hipStream_t)stream), what);
+}
+
+}  // namespace
+
+extern "C" {
+
+fkv_status fkv_select(const fkv_shape *shape, const fkv_head *heads, const float *scores, int32_t shared_row,
+                      int32_t *kept_seg, int32_t *kv_len, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if (shared_row != 0 && shared_row != 1) return fail(FKV_ERR_ARG, "shared_row %d is neither 0 nor 1", shared_row);
+    if (!kv_len) return fail(FKV_ERR_ARG, "kv_len is NULL");
+    if (fkv_num_segments(shape) > 0 && (!scores || !kept_seg)) return fail(FKV_ERR_ARG, "NULL scores or kept_seg");
+    return select_impl(shape, heads, scores, shared_row != 0, kept_seg, kv_len, stream, "fkv_select launch");
+}
+
+fkv_status fkv_score_select(const fkv_shape *shape, const fkv_head *heads, const void *K_hist,
+                            const int32_t *frame_slot, const void *K_cur, float *scores, int32_t *kept_seg,
+                            int32_t *kv_len, void *workspace, size_t workspace_bytes, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+    if (!kv_len) return fail(FKV_ERR_ARG, "kv_len is NULL");
+    size_t need = 0;
+    if ((st = fkv_score_workspace_size(shape, heads, &need)) != FKV_OK) return st;
+    if (need == 0)  // no dynamic head, or nothing cached: every dynamic head keeps nothing
+        return select_impl(shape, heads, nullptr, false, kept_seg, kv_len, stream, "fkv_score_select launch");
+    if (!K_hist || !K_cur || !scores || !kept_seg) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    if (!workspace) return fail(FKV_ERR_ARG, "workspace is NULL");
+    if (workspace_bytes < need)
+        return fail(FKV_ERR_CAPACITY, "workspace of %zu bytes, %zu needed", workspace_bytes, need);
+    fkv::HeadList list;
+    memset(&list, 0, sizeof list);
+    for (int h = 0; h < shape->n_heads; ++h)
+        if (heads[h].type == FKV_DYNAMIC) list.head[list.n++] = h;
+    const SelectOut out{heads, kept_seg, kv_len};
+    return score_impl(shape, list, false, K_hist, frame_slot, K_cur, scores, workspace, stream,
+                      "fkv_score_select launch", fkv::kScoreModeFull, nullptr, &out);
 }
 
 }  // extern "C"
@@ -631,13 +718,30 @@ fkv::HeadList all_heads(int n_heads) {
     return l;
 }
 
-// Static heads attended in place: the kept history frames are read from the
-// cache through the frame-slot map instead of from a compressed copy.
+// Heads attended in place: the kept history is read from the cache through the
+// frame-slot map instead of from a compressed copy -- the kept frames of a
+// static head (from its budget), the kept segments of a dynamic head (kept_seg
+// and kv_len as fkv_select writes them).
 struct PagedHistory {
     const void *K_hist, *V_hist;
     const int32_t *frame_slot;
     const fkv_head *heads;
+    const int32_t *kept_seg;   // dynamic heads only
 };
+
+// Can the paged kernel read dynamic heads of this shape in place?  Pieces of
+// min(L, F) >= 64 tokens (a key tile spans at most two), and a page-table
+// entry slot * (F / piece) + unit below 256 for every cache slot.
+fkv_status check_paged_dynamic(const fkv_shape *s) {
+    const int P = std::min(s->seg_tokens, s->frame_tokens);
+    if (P < fkv::kAttnKeysPerTile)
+        return fail(FKV_ERR_SHAPE, "in-place dynamic heads need min(seg_tokens, frame_tokens) = %d >= %d", P,
+                    fkv::kAttnKeysPerTile);
+    if ((int64_t)s->cap_frames * (s->frame_tokens / P) > 256)
+        return fail(FKV_ERR_SHAPE, "in-place dynamic heads need cap_frames * (F / min(L, F)) = %lld <= 256",
+                    (long long)s->cap_frames * (s->frame_tokens / P));
+    return FKV_OK;
+}
 
 fkv_status chunk_attention_impl(const fkv_shape *shape, const fkv::HeadList &list, const void *Q,
                                 const void *Kc, const void *Vc, int32_t slab, const int32_t *kv_len,
@@ -687,12 +791,26 @@ fkv_status chunk_attention_impl(const fkv_shape *shape, const fkv::HeadList &lis
         a.V_hist = paged->V_hist;
         a.F = shape->frame_tokens;
         a.cap = shape->cap_frames;
+        // a dynamic head's kv_len is clamped to the history, so its pieces never
+        // leave the cached frames whatever kv_len holds
+        a.slab = (int64_t)shape->hist_frames * shape->frame_tokens;
+        a.kept_seg = paged->kept_seg;
+        a.pg_L = shape->seg_tokens;
+        a.pg_nseg = fkv_num_segments(shape);
         for (int li = 0; li < list.n; ++li) {
             const int h = list.head[li];
-            const StaticPlan p = static_plan(shape->hist_frames, paged->heads[h]);
+            if (paged->heads[h].type == FKV_DYNAMIC && shape->hist_frames > 0) {
+                a.st_kept[li] = -1;
+                a.pg_piece[li] = std::min(shape->seg_tokens, shape->frame_tokens);
+                continue;
+            }
+            // static heads, and dynamic heads with nothing cached (no history, kv_len unread)
+            const StaticPlan p = paged->heads[h].type == FKV_DYNAMIC ? StaticPlan{0, 0, 0}
+                                                                     : static_plan(shape->hist_frames, paged->heads[h]);
             a.st_first[li] = p.n_first;
             a.st_gap[li] = p.gap;
             a.st_kept[li] = p.n_kept;
+            a.pg_piece[li] = shape->frame_tokens;
         }
         for (int t = 0; t < shape->hist_frames; ++t) a.slots.slot[t] = paged->frame_slot[t];
     }
@@ -756,8 +874,48 @@ fkv_status fkv_chunk_attention_static(const fkv_shape *shape, const fkv_head *he
     memset(&list, 0, sizeof list);
     for (int h = 0; h < shape->n_heads; ++h)
         if (heads[h].type == FKV_STATIC) list.head[list.n++] = h;
-    const PagedHistory paged{K_hist, V_hist, frame_slot, heads};
+    const PagedHistory paged{K_hist, V_hist, frame_slot, heads, nullptr};
     return chunk_attention_impl(shape, list, Q, nullptr, nullptr, 0, nullptr, K_cur, V_cur, scale, O, lse,
+                                workspace, workspace_bytes, stream, &paged);
+}
+
+fkv_status fkv_chunk_attention_paged(const fkv_shape *shape, const fkv_head *heads, const int32_t *head_list,
+                                     int32_t n_list, const void *K_hist, const void *V_hist,
+                                     const int32_t *frame_slot, const int32_t *kept_seg, const int32_t *kv_len,
+                                     const void *Q, const void *K_cur, const void *V_cur, float scale, void *O,
+                                     float *lse, void *workspace, size_t workspace_bytes, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if (shape->dtype != FKV_BF16) return fail(FKV_ERR_SHAPE, "in-place attention needs bf16");
+    if (shape->frame_tokens < fkv::kAttnKeysPerTile)
+        return fail(FKV_ERR_SHAPE, "in-place attention needs frame_tokens %d >= %d", shape->frame_tokens,
+                    fkv::kAttnKeysPerTile);
+    if (n_list < 0 || n_list > shape->n_heads)
+        return fail(FKV_ERR_ARG, "n_list %d outside [0, %d]", n_list, shape->n_heads);
+    fkv::HeadList list;
+    memset(&list, 0, sizeof list);
+    bool seen[FKV_MAX_HEADS] = {};
+    const int n = head_list ? n_list : shape->n_heads;
+    for (int i = 0; i < n; ++i) {
+        const int h = head_list ? head_list[i] : i;
+        if (h < 0 || h >= shape->n_heads)
+            return fail(FKV_ERR_ARG, "head_list[%d] = %d outside [0, %d)", i, h, shape->n_heads);
+        if (seen[h]) return fail(FKV_ERR_ARG, "head %d listed twice", h);
+        seen[h] = true;
+        list.head[list.n++] = h;
+    }
+    bool any_dynamic = false;
+    for (int i = 0; i < list.n; ++i) any_dynamic |= heads[list.head[i]].type == FKV_DYNAMIC;
+    if (any_dynamic) {
+        if ((st = check_paged_dynamic(shape)) != FKV_OK) return st;
+        if (!kv_len) return fail(FKV_ERR_ARG, "kv_len is NULL");
+        if (shape->hist_frames > 0 && !kept_seg) return fail(FKV_ERR_ARG, "kept_seg is NULL");
+    }
+    if (shape->hist_frames > 0 && (!K_hist || !V_hist)) return fail(FKV_ERR_ARG, "NULL K_hist/V_hist");
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+    const PagedHistory paged{K_hist, V_hist, frame_slot, heads, kept_seg};
+    return chunk_attention_impl(shape, list, Q, nullptr, nullptr, 0, kv_len, K_cur, V_cur, scale, O, lse,
                                 workspace, workspace_bytes, stream, &paged);
 }
 

@@ -84,26 +84,38 @@ struct SelectCopyArgs {
 };
 
 // ------------------------------------------------------------------ scoring
+// One kernel per scoring call (k_score.hip).  Workgroup (cg, u, li) streams
+// column group cg of unit u of listed head li over the frames [t_begin,
+// t_begin + n_frames) and writes its per-frame partial sums; the last
+// workgroup of a head to arrive (a counter in the workspace) reduces the
+// head's partials in a fixed order and finishes: statistics, scores, and
+// optionally the BottomK selection.
+enum ScoreMode : int32_t { kScoreModeFull = 0, kScoreModeHistory = 1, kScoreModeCached = 2 };
+
 struct ScoreArgs {
     const uint8_t *K_hist, *K_cur;
-    float *scores;                  // [n_heads][n_seg]
-    double *ws;                     // partial sums (see k_score.hip)
-    int64_t frame_bytes;            // F*d*esize
-    int64_t unit_vecs;              // 16-byte vectors per unit (U*d*esize/16)
-    int64_t cur_vecs;               // 16-byte vectors per head of K_cur (C*F*d*esize/16)
-    int32_t F, L, H, cap, n_seg, d;
-    int32_t unit_tokens;            // U = min(L, F)
-    int32_t units_per_frame;        // F / U
-    int32_t chunks_per_unit;        // ceil(unit_vecs / 256)
-    int32_t esize;
-    int32_t pooled;                 // 1: one score per segment over all listed heads, scores[n_seg]
-    int32_t t_begin, t_end;         // frames the partials pass streams (inclusive; frame H = K_cur's first)
-    int32_t n_parts;                // the streamed range split into parts of part_frames frames (the
-    int32_t part_frames;            // last part to t_end), one workgroup column per part
-    int32_t cached;                 // finalize: 1 = frames < H from `stats`, the last pair from partials
-    double *stats;                  // per-frame sums [list n][H][units][2]: SQ(t), DOT(t, t+1)
+    float *scores;                  // [n_heads][n_seg], or [n_seg] when pooled
+    uint32_t *counters;             // [heads.n + 1] arrivals per listed head, then finished heads
+    double *part;                   // [li][row][n_cg] partial sums, row = (u*n_frames + f)*2 + q
+    double *totals;                 // [li][row] per-head sums (pooled finish)
+    double *stats;                  // incremental rescoring: [li][H][units][2] = SQ(t), DOT(t, t+1)
+    int64_t frame_vecs;             // 16-byte vectors per frame (F*d*esize/16)
+    int64_t cur_head_vecs;          // 16-byte vectors per head of K_cur (C*F*d*esize/16)
+    int32_t F, L, H, cap, n_seg;
+    int32_t units;                  // units per frame, F / U with U = min(L, F)
+    int32_t unit_vecs;              // 16-byte vectors per unit
+    int32_t n_cg;                   // column groups (workgroups) per unit
+    int32_t mode;                   // ScoreMode
+    int32_t pooled;                 // 1: one score row over all listed heads
+    int32_t t_begin, n_frames;      // streamed frames (frame H is the first frame of K_cur)
+    int32_t select;                 // 1: also the BottomK selection (the fields at the end)
+    int32_t lds_rows;               // doubles of dynamic LDS for the finishing workgroup's row sums
     HeadList heads;
     SlotTable slots;
+    // BottomK parameters per listed head (fused selection)
+    int32_t *kept_seg, *kv_len;
+    int32_t sink[FKV_MAX_HEADS], recent[FKV_MAX_HEADS], scope[FKV_MAX_HEADS];
+    int32_t k[FKV_MAX_HEADS];       // kk = min(keep_k, |group|) per listed head
 };
 
 // ---------------------------------------------------------------- attention
@@ -128,15 +140,22 @@ struct AttnArgs {
     int64_t fp8_rows;               // FP8 path: key rows per head of the packed K / V^T
     float scale;                    // softmax scale
     float scale_log2;               // scale * log2(e)
-    // Paged static heads (fkv_chunk_attention_static): the retained history is
-    // read straight from the cache -- for head h = heads.head[li], kept frame y
-    // is logical frame y (y < st_first[li]) or y + st_gap[li], in slot
-    // slots.slot[t] of K_hist / V_hist [n_heads][cap][F][d] -- and its history
-    // length is st_kept[li] * F (kv_len is not read).
+    // Paged heads (fkv_chunk_attention_static, fkv_chunk_attention_paged): the
+    // retained history is read straight from the cache K_hist / V_hist
+    // [n_heads][cap][F][d] as a sequence of kept pieces of pg_piece[li] tokens.
+    // A static entry (st_kept[li] >= 0) keeps frames: kept frame y is logical
+    // frame y (y < st_first[li]) or y + st_gap[li], in slot slots.slot[t], and
+    // its history length is st_kept[li] * F (kv_len is not read).  A dynamic
+    // entry (st_kept[li] < 0) keeps the segments listed in kept_seg[h] (as
+    // fkv_select writes them), pieces of min(L, F) tokens, and its history
+    // length is kv_len[h].
     int32_t paged;
     const void *K_hist, *V_hist;
     int32_t F, cap;
+    int32_t pg_L, pg_nseg;          // segment length and segments per head (dynamic entries)
+    const int32_t *kept_seg;        // [n_heads][pg_nseg] (dynamic entries)
     int32_t st_first[FKV_MAX_HEADS], st_gap[FKV_MAX_HEADS], st_kept[FKV_MAX_HEADS];
+    int32_t pg_piece[FKV_MAX_HEADS];
     SlotTable slots;
 };
 
@@ -159,17 +178,18 @@ constexpr int kAttnKeysPerTile = 64; // keys per tile of the bf16 MFMA kernel
 constexpr int kAttnRowsF32 = 32;    // query rows per attention workgroup (fp32 kernel)
 constexpr int kScoreWaves = kScoreThreads / 64;
 
-size_t score_workspace_doubles(int n_dyn, int H, int units_per_frame, int chunks_per_unit);
+// Scoring workspace: counters, partials and per-head sums for n_list heads.
+size_t score_workspace_bytes(int n_list, int H, int units, int n_cg);
+int score_column_groups(int64_t unit_vecs);  // workgroups per unit
 
 hipError_t launch_static_copy(const StaticCopyArgs &a, int max_kept, hipStream_t s);
 hipError_t launch_dyn_copy(const DynCopyArgs &a, int max_pieces, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, int n_heads, hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, hipStream_t s);
 hipError_t launch_select_copy(const SelectCopyArgs &a, int max_pieces, hipStream_t s);
+// one scoring launch in a.mode (full pass, history statistics, or cached scores)
 hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s);
-// incremental rescoring: per-frame statistics of the history, then per-step scores
-hipError_t launch_score_history(const ScoreArgs &a, bool f32, hipStream_t s);
-hipError_t launch_score_cached(const ScoreArgs &a, bool f32, hipStream_t s);
+void score_workspace_layout(ScoreArgs &a, void *ws, int n_list, int H, int units, int n_cg);
 hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s);
 size_t attention_part_bytes(int head_dim);  // bytes of one partial-result slot (bf16 kernel)
 

@@ -5,9 +5,11 @@
 // history, then the current chunk) and likewise for values; every query row of
 // the chunk attends to all of it with no mask.  The per-head key count is
 // ragged (it comes from the device-side kv_len), and one key tile may straddle
-// the history/chunk boundary.  The PAGED instantiation attends static heads in
-// place: their retained history is the kept frames of Eq. 2 read straight from
-// the slot-permuted cache (load_tile_paged), with no compressed copy.
+// the history/chunk boundary.  The PAGED instantiation attends heads in place:
+// their retained history -- the kept frames of Eq. 2 for static heads, the
+// kept segments of Eq. 3 for dynamic heads -- is read straight from the
+// slot-permuted cache through a per-head page table (load_tile_paged), with no
+// compressed copy.
 //
 // Workgroup = 8 waves = 256 query rows of one head (32 per wave), in two
 // groups of four waves; one workgroup fills a CU.  Keys are processed in tiles
@@ -117,32 +119,65 @@ __device__ __forceinline__ void load_tile(const uint16_t *hist, const uint16_t *
     }
 }
 
-// Cache slots of a static head's kept frames, one byte each (cap <= 256):
-// kept frame y is logical frame y (y < st_first) or y + st_gap, and its slot
-// sits in byte y >> 6 of lane y & 63 -- up to 256 frames in one VGPR, looked
-// up with v_readlane, so the tile loop never waits on a scalar load (whose
-// counter it shares with the LDS reads).
-__device__ __forceinline__ uint32_t kept_slot_table(const AttnArgs &a, int li, int lane) {
-    const int n = a.st_kept[li], first = a.st_first[li], gap = a.st_gap[li];
+// Page table of a head read in place: the cache position of each kept piece,
+// one byte per piece -- piece y's entry sits in byte y >> 6 of lane y & 63, up
+// to 256 pieces in one VGPR, looked up with v_readlane, so the tile loop never
+// waits on a scalar load (whose counter it shares with the LDS reads).  Piece
+// y starts at cache row entry(y) * P of the head (P = the entry's piece
+// length), i.e. entry = slot * (F / P) + unit.
+//   static entry: pieces are frames; kept frame y is logical frame y
+//                 (y < st_first) or y + st_gap, entry = its slot;
+//   dynamic entry: pieces are the min(L, F)-token pieces of the segments in
+//                 kept_seg[h] (ascending, as the selection wrote them); the
+//                 host has checked that every entry fits in a byte.
+__device__ __forceinline__ uint32_t kept_piece_table(const AttnArgs &a, int li, int kvl, int lane) {
     uint32_t tab = 0;
+    const int n = a.st_kept[li];
+    if (n >= 0) {
+        const int first = a.st_first[li], gap = a.st_gap[li];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int y = lane + 64 * k;
+            if (y < n) tab |= (uint32_t)a.slots.slot[y < first ? y : y + gap] << (8 * k);
+        }
+        return tab;
+    }
+    const int P = a.pg_piece[li];
+    const int ppf = a.F / P;                                  // pieces per frame (1 when L >= F)
+    const int m = a.pg_L > a.F ? a.pg_L / a.F : 1;           // pieces per segment
+    const int n_pieces = kvl / P;
+    const int32_t *ks = a.kept_seg + (size_t)a.heads.head[li] * a.pg_nseg;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int y = lane + 64 * k;
-        if (y < n) tab |= (uint32_t)a.slots.slot[y < first ? y : y + gap] << (8 * k);
+        if (y < n_pieces) {
+            // a kept_seg row and kv_len that disagree must not address outside
+            // the head's cache: clamp the segment id
+            const int q = y / m, g = min(max(ks[q], 0), a.pg_nseg - 1);
+            int t, u;
+            if (a.pg_L <= a.F) {
+                t = g / ppf;
+                u = g - t * ppf;
+            } else {
+                t = min(g * m + (y - q * m), (int)(a.slab / a.F) - 1);   // a short last segment ends at H
+                u = 0;
+            }
+            tab |= (uint32_t)(a.slots.slot[t] * ppf + u) << (8 * k);
+        }
     }
     return tab;
 }
-__device__ __forceinline__ int kept_slot(uint32_t tab, int y) {
+__device__ __forceinline__ int kept_piece(uint32_t tab, int y) {
     return (int)((uint32_t)__builtin_amdgcn_readlane((int)tab, y & 63) >> (8 * (y >> 6))) & 255;
 }
 
-// The same for a static head read in place from the cache (paged): history
-// row p is row p mod F of kept frame y = p / F, in cache slot
-// kept_slot(tab, y).  With F >= 64 a tile touches at most two kept frames and
-// the chunk; each part has its own range-checked buffer and the three loads
-// are OR-ed, every row outside a part reading as zero.
+// The same for a head read in place from the cache (paged): history row p is
+// row p mod P of kept piece y = p / P, at cache row kept_piece(tab, y) * P.
+// With P >= 64 a tile touches at most two kept pieces and the chunk; each part
+// has its own range-checked buffer and the three loads are OR-ed, every row
+// outside a part reading as zero.
 template <int D, int N>
-__device__ __forceinline__ void load_tile_paged(const uint16_t *hist, uint32_t tab, int F,
+__device__ __forceinline__ void load_tile_paged(const uint16_t *hist, uint32_t tab, int P,
                                                 const uint16_t *chunk, int j0, int kvl, int Lk, int Lq,
                                                 u32x4 *dst, uint32_t off0, uint32_t step) {
     if (j0 >= kvl) {
@@ -151,19 +186,19 @@ __device__ __forceinline__ void load_tile_paged(const uint16_t *hist, uint32_t t
         for (int i = 0; i < N; ++i) dst[i] = bload(r, off0 + i * step);
         return;
     }
-    auto frame = [&](int y) { return hist + (size_t)kept_slot(tab, y) * F * D; };
-    const int y0 = j0 / F, r0 = j0 - y0 * F;
-    const int na = min(min(F - r0, kvl - j0), BN);            // rows of kept frame y0
-    const auto ra = rsrc(frame(y0) + (size_t)r0 * D, (uint32_t)na * D * 2);
+    auto piece = [&](int y) { return hist + (size_t)kept_piece(tab, y) * P * D; };
+    const int y0 = j0 / P, r0 = j0 - y0 * P;
+    const int na = min(min(P - r0, kvl - j0), BN);            // rows of kept piece y0
+    const auto ra = rsrc(piece(y0) + (size_t)r0 * D, (uint32_t)na * D * 2);
     if (na == BN) {
 #pragma unroll
         for (int i = 0; i < N; ++i) dst[i] = bload(ra, off0 + i * step);
         return;
     }
-    // the rest of the tile: the next kept frame while history lasts, then the chunk
+    // the rest of the tile: the next kept piece while history lasts, then the chunk
     const int nb = j0 + na < kvl ? min(BN - na, kvl - (j0 + na)) : 0;
     const int nc = j0 + na + nb >= kvl ? min(BN - na - nb, Lq) : 0;
-    const auto rb = rsrc(nb > 0 ? frame(y0 + 1) : hist, (uint32_t)nb * D * 2);
+    const auto rb = rsrc(nb > 0 ? piece(y0 + 1) : hist, (uint32_t)nb * D * 2);
     const auto rc = rsrc(chunk, (uint32_t)nc * D * 2);
     const uint32_t sb = (uint32_t)na * D * 2, sc = (uint32_t)(na + nb) * D * 2;
 #pragma unroll
@@ -273,7 +308,8 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
                                : (const uint16_t *)a.Vc + (size_t)h * a.slab * D;
     const uint16_t *Kq = (const uint16_t *)a.K_cur + (size_t)h * Lq * D;
     const uint16_t *Vq = (const uint16_t *)a.V_cur + (size_t)h * Lq * D;
-    const uint32_t ktab = PAGED ? kept_slot_table(a, li, lane) : 0u;
+    const uint32_t ktab = PAGED ? kept_piece_table(a, li, kvl, lane) : 0u;
+    const int piece_len = PAGED ? a.pg_piece[li] : 0;
 
     // Loop-invariant per-thread load geometry within the thread's group of 256:
     // rows r0 + RPP*i, chunk c (group 0 stages K tiles, group 1 V tiles).
@@ -294,14 +330,14 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
     };
     auto load_k = [&](int j0, u32x4 (&dst)[4]) {
         if (PAGED)
-            load_tile_paged<D, C::NV>(Kc, ktab, a.F, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
+            load_tile_paged<D, C::NV>(Kc, ktab, piece_len, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
         else
             load_tile<D, C::NV>(Kc, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
     };
     auto load_v = [&](int j0, u32x4 (&dst)[4]) {
         if (gtid < C::VUNITS) {
             if (PAGED)
-                load_tile_paged<D, 4>(Vc, ktab, a.F, Vq, j0, kvl, Lk, Lq, dst, voffv, D * 2);
+                load_tile_paged<D, 4>(Vc, ktab, piece_len, Vq, j0, kvl, Lk, Lq, dst, voffv, D * 2);
             else
                 load_tile<D, 4>(Vc, Vq, j0, kvl, Lk, Lq, dst, voffv, D * 2);
         }

@@ -1,61 +1,63 @@
 // k_score.hip -- segment-wise cosine similarity of adjacent frames for dynamic
-// heads (Sec. 4.3, Eq. 3), per head or pooled over all heads.
+// heads (Sec. 4.3, Eq. 3), per head or pooled over all heads, optionally
+// followed by the BottomK selection, in ONE kernel launch.
 //
 // Segment g of the history is compared with the same token range one frame
 // later.  Splitting every frame into units of U = min(L, F) tokens (a unit is
 // a segment when L <= F, a whole frame otherwise), each score is a sum of
-// per-(frame t, unit u) quantities:
-//   SQ[t][u]  = sum over the unit's elements of K_t^2          (t = 0..H, frame H
+// per-(frame t, unit u) quantities
+//   SQ(t, u)  = sum over the unit's elements of K_t^2           (t = 0..H, frame H
 //               being the first frame of the current chunk)
-//   DOT[t][u] = sum over the unit's elements of K_t * K_{t+1}   (t = 0..H-1)
-// with dot = sum DOT, na = sum SQ[t], nb = sum SQ[t+1] over the frames of the
-// segment.
+//   DOT(t, u) = sum over the unit's elements of K_t * K_{t+1}   (t = 0..H-1)
+// with dot = sum DOT, na = sum SQ(t), nb = sum SQ(t+1) over the frames of the
+// segment.  Every product is exact in fp64 (a bf16*bf16 or fp32*fp32 product
+// has at most 48 significant bits); every sum is fp64 in a fixed order, and
+// the cosine dot / sqrt(na*nb) (0 when na*nb == 0) is rounded once to fp32.
 //
-// Pass 1 (score_partials_kernel) streams the cache once: a workgroup owns a
-// 256-vector column chunk of one unit of one head and walks the frames t = 0..H
-// in order, keeping the previous frame's elements in registers, so every key
-// byte is read from HBM exactly once (16-byte coalesced loads, loads of the next
-// frames in flight while the current one is reduced).  Every product is exact
-// in fp64 (a bf16*bf16 or fp32*fp32 product has at most 48 significant bits);
-// sums are fp64.  Each wave reduces its per-frame sums with DPP row operations
-// and writes them to the workspace.
-// Pass 2 (score_finalize_kernel) sums the partials of each segment in a fixed
-// order, forms dot / sqrt(na*nb) in fp64 (0 when na*nb == 0) and rounds once
-// to fp32 (nearest even).  The result is deterministic run to run.
+// Streaming.  Workgroup (cg, u, li) owns column group cg -- 2 x 64 adjacent
+// 16-byte vectors -- of unit u of listed head li, and streams those columns of
+// every frame once: its four waves split the frames into four contiguous
+// runs, every lane loads up to four frames of its run at once (bf16),
+// so no key byte is read twice and every load is a full 1 KB-per-wave
+// coalesced access.  A lane accumulates, per frame, its columns' squares and
+// products with the previous frame (vector 0 then vector 1, elements in
+// order); the wave reduces each sum over its 64 lanes with DPP row scans in a
+// fixed order and writes one partial per (frame, column group).  The product
+// across a run boundary uses the next run's first frame, which its wave
+// leaves in LDS.
 //
-// The first-block proxy of Sec. 4.3 (scores pooled over heads) runs the same
-// two passes over every head and sums the partials of all heads of a segment
+// Finish.  After its partial stores each workgroup bumps its head's arrival
+// counter (agent-scope release / acquire); the last workgroup of the head
+// reduces the head's partials -- per (unit, frame, quantity), four sequential
+// sums over fixed quarters of the column groups, then (p0 + p1) + (p2 + p3) --
+// and then, by mode:
+//   full:    the head's scores (and, with `select`, its BottomK selection);
+//   history: per-frame statistics SQ(t), DOT(t) into `stats`, kept across the
+//            AR steps of a chunk (the history does not change, only K_cur);
+//   cached:  frames H-1 and H only were streamed; the scores take DOT(H-1) and
+//            SQ(H) from this pass and every other term from `stats`.
+// Because the history pass and the full pass reduce every (frame, unit) sum
+// with the same lanes, the same DPP order and the same column-group tree, the
+// cached scores equal the full pass's bit for bit.  Pooled scores (the
+// first-block proxy of Sec. 4.3): each head's finisher stores its per-frame
+// sums, and the last head to finish sums them over the heads (in list order)
 // before the cosine.
 //
-// Incremental rescoring.  During the AR steps of one chunk the history does not
-// change; only K_cur does, and with it only SQ[H] and DOT[H-1].  The history
-// pass streams frames 0..H-1 once and reduces each frame's partials into a
-// per-frame statistics buffer (SQ(t), and DOT(t) for t < H-1); each step then
-// streams frames H-1..H only (2 frames per head instead of H+1) and the
-// finalize takes every other term from the statistics.
-#include "fkv_internal.h"
+// The counters live at the start of the workspace; the caller zero-fills the
+// workspace once and every call returns the counters to zero.
+#include "select_common.h"
 
 namespace fkv {
 namespace {
 
-constexpr int kThreads = kScoreThreads;
+constexpr int kThreads = kScoreThreads;  // 4 waves
 constexpr int kWaves = kScoreWaves;
-// Frames in flight per thread.  Four keep the pass within 64 VGPRs (the
-// launch bound below), so its waves fit on a CU next to the two 224-VGPR
-// waves per SIMD of a running attention workgroup: in the two-stream layer
-// step the scoring of the dynamic heads then runs beside the static heads'
-// attention instead of waiting for CUs (8 frames took 88 VGPRs).
-constexpr int kDepth = 4;
-// Frames per part when a long range is split over several workgroup columns:
-// more waves in flight per CU hide the fp64 products and reductions behind the
-// loads.  At 480P (22 frames) 6-frame parts (4 columns, 3 frames read twice)
-// took the partials pass from 19.0 to 16.7 us with 8 frames in flight (11- and
-// 8-frame parts: 17.6 and 17.8 us); with 4 in flight 4-, 6-, 8- and 11-frame
-// parts are within 3% of each other.
-#ifndef FKV_SCORE_PART_FRAMES
-#define FKV_SCORE_PART_FRAMES 6
-#endif
-constexpr int kScorePartFrames = FKV_SCORE_PART_FRAMES;
+constexpr int kV = 2;                    // 16-byte vectors per lane and frame
+constexpr int kCols = 64 * kV;           // vectors (columns) per workgroup
+// Frames a lane loads at once: four bf16 frames keep the kernel within 96
+// VGPRs (five waves per SIMD, every workgroup of a 480P layer resident).
+template <bool F32> constexpr int kMaxF = F32 ? 6 : 4;
+constexpr int kRowBatch = kThreads / 4;  // partial rows reduced per pass of the finisher
 
 // One DPP step on a double (both 32-bit halves moved with the same control);
 // lanes without a source, or outside row_mask, contribute 0.
@@ -80,7 +82,7 @@ __device__ __forceinline__ double wave_sum(double v) {
     return v;  // valid in lane 63
 }
 
-// Widen the 16-byte vector to fp64 elements (exact).
+// Widen a 16-byte vector to fp64 elements (exact).
 template <bool F32>
 struct Vec;
 
@@ -88,11 +90,10 @@ template <>
 struct Vec<false> {  // 8 bf16
     static constexpr int N = 8;
     __device__ static __forceinline__ void widen(const u32x4 &v, double *x) {
-        const uint32_t w[4] = {v[0], v[1], v[2], v[3]};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            x[2 * i] = (double)__uint_as_float(w[i] << 16);
-            x[2 * i + 1] = (double)__uint_as_float(w[i] & 0xffff0000u);
+            x[2 * i] = (double)__uint_as_float(v[i] << 16);
+            x[2 * i + 1] = (double)__uint_as_float(v[i] & 0xffff0000u);
         }
     }
 };
@@ -101,251 +102,289 @@ template <>
 struct Vec<true> {  // 4 fp32
     static constexpr int N = 4;
     __device__ static __forceinline__ void widen(const u32x4 &v, double *x) {
-        x[0] = (double)__uint_as_float(v[0]);
-        x[1] = (double)__uint_as_float(v[1]);
-        x[2] = (double)__uint_as_float(v[2]);
-        x[3] = (double)__uint_as_float(v[3]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x[i] = (double)__uint_as_float(v[i]);
     }
 };
 
-// Workspace layout: ws[(((li*(H+1) + t)*units + u)*chunks + c)*kWaves + w][2]
-// with [0] = SQ of frame t and [1] = DOT of frames (t, t+1).
-__device__ __forceinline__ int64_t ws_index(const ScoreArgs &a, int li, int t, int u, int c, int w) {
-    return ((((int64_t)li * (a.H + 1) + t) * a.units_per_frame + u) * a.chunks_per_unit + c) * kWaves + w;
-}
-
-// Statistics layout: stats[((li*H + t)*units + u)][2], [0] = SQ(t), [1] = DOT(t, t+1)
-// (DOT(H-1) is not part of the history and never stored).
-__device__ __forceinline__ int64_t stats_index(const ScoreArgs &a, int li, int t, int u) {
-    return ((int64_t)li * a.H + t) * a.units_per_frame + u;
+// sum over the lane's columns of a*b, vector 0 then vector 1, elements in order
+template <bool F32>
+__device__ __forceinline__ double lane_dot(const u32x4 (&a)[kV], const u32x4 (&b)[kV]) {
+    using V = Vec<F32>;
+    double acc = 0.0;
+#pragma unroll
+    for (int j = 0; j < kV; ++j) {
+        double x[V::N], y[V::N];
+        V::widen(a[j], x);
+        V::widen(b[j], y);
+#pragma unroll
+        for (int e = 0; e < V::N; ++e) acc = fma(x[e], y[e], acc);
+    }
+    return acc;
 }
 
 template <bool F32>
-__global__ __launch_bounds__(kThreads, 8) void score_partials_kernel(ScoreArgs a) {
+__device__ __forceinline__ double lane_sq(const u32x4 (&a)[kV]) {
     using V = Vec<F32>;
-    const int c = blockIdx.x, u = blockIdx.y, li = blockIdx.z / a.n_parts, part = blockIdx.z % a.n_parts;
-    const int h = a.heads.head[li];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int64_t v = (int64_t)c * kThreads + tid;       // vector within the unit
-    const bool active = v < a.unit_vecs;
-    const int64_t frame_vecs = a.frame_bytes / 16;
-    const int64_t off = (int64_t)u * a.unit_vecs + v;   // vector within a frame
-    const u32x4 *hist = (const u32x4 *)a.K_hist + (int64_t)h * a.cap * frame_vecs;
-    const u32x4 *cur = (const u32x4 *)a.K_cur + (int64_t)h * a.cur_vecs;
-    const int H = a.H;
-    // This workgroup streams frames [tb, te] of the range [t_begin, t_end]:
-    // parts overlap by one frame, whose SQ the later part writes and whose DOT
-    // with the previous frame the earlier part writes, so every per-frame
-    // partial is computed exactly as by a single pass.
-    const bool last_part = part == a.n_parts - 1;
-    const int tb = a.t_begin + part * a.part_frames;
-    const int te = last_part ? a.t_end : tb + a.part_frames;
-
-    auto load = [&](int t) -> u32x4 {
-        u32x4 r = u32x4{0, 0, 0, 0};
-        if (active && t <= te) {
-            const u32x4 *base = t < H ? hist + (int64_t)a.slots.slot[t] * frame_vecs : cur;
-            r = __builtin_nontemporal_load(base + off);
-        }
-        return r;
-    };
-
-    u32x4 ring[kDepth];
+    double acc = 0.0;
 #pragma unroll
-    for (int i = 0; i < kDepth; ++i) ring[i] = load(tb + i);
+    for (int j = 0; j < kV; ++j) {
+        double x[V::N];
+        V::widen(a[j], x);
+#pragma unroll
+        for (int e = 0; e < V::N; ++e) acc = fma(x[e], x[e], acc);
+    }
+    return acc;
+}
 
-    double prev[V::N];
-#pragma unroll
-    for (int i = 0; i < V::N; ++i) prev[i] = 0.0;
+// Partial row of (unit u, streamed frame f, quantity q: 0 = SQ, 1 = DOT).
+__device__ __forceinline__ int row_of(const ScoreArgs &a, int u, int f, int q) {
+    return (u * a.n_frames + f) * 2 + q;
+}
 
-    for (int t0 = tb; t0 <= te; t0 += kDepth) {
-#pragma unroll
-        for (int i = 0; i < kDepth; ++i) {
-            const int t = t0 + i;
-            if (t > te) break;
-            double x[V::N];
-            V::widen(ring[i], x);
-            ring[i] = load(t + kDepth);
-            double sq = 0.0, dot = 0.0;
-#pragma unroll
-            for (int e = 0; e < V::N; ++e) {
-                sq = fma(x[e], x[e], sq);
-                dot = fma(prev[e], x[e], dot);
-                prev[e] = x[e];
-            }
-            sq = wave_sum(sq);
-            dot = wave_sum(dot);
-            if (lane == 63) {
-                if (t < te || last_part) a.ws[ws_index(a, li, t, u, c, w) * 2 + 0] = sq;
-                if (t > tb) a.ws[ws_index(a, li, t - 1, u, c, w) * 2 + 1] = dot;
-            }
-        }
+// Per-(unit, frame) sums of one head as the scores read them, with the frame
+// given as a logical frame t: T holds this pass's rows (streamed frames
+// [t_begin, t_begin + n_frames)), stats the history statistics (cached mode).
+struct Terms {
+    const ScoreArgs &a;
+    const double *T;      // rows of this head
+    const double *stats;  // [H][units][2] of this head (cached mode)
+    __device__ __forceinline__ double sq(int t, int u) const {
+        if (a.mode == kScoreModeCached && t < a.H) return stats[((int64_t)t * a.units + u) * 2];
+        return T[row_of(a, u, t - a.t_begin, 0)];
+    }
+    __device__ __forceinline__ double dot(int t, int u) const {
+        if (a.mode == kScoreModeCached && t < a.H - 1) return stats[((int64_t)t * a.units + u) * 2 + 1];
+        return T[row_of(a, u, t - a.t_begin, 1)];
+    }
+};
+
+// Segment g -> its unit and frames [t0, t1).
+__device__ __forceinline__ void seg_span(const ScoreArgs &a, int g, int *u, int *t0, int *t1) {
+    if (a.L <= a.F) {
+        *t0 = g / a.units;
+        *u = g - *t0 * a.units;
+        *t1 = *t0 + 1;
+    } else {
+        const int m = a.L / a.F;
+        *t0 = g * m;
+        *t1 = min(*t0 + m, a.H);
+        *u = 0;
     }
 }
 
-// One workgroup per (segment, listed head), or per segment when the score is
-// pooled over all listed heads: every thread sums a strided slice of the
-// segment's partials, then a fixed-order tree over the workgroup; the result
-// does not depend on timing.
-__global__ __launch_bounds__(kThreads) void score_finalize_kernel(ScoreArgs a) {
-    __shared__ double red[3][kThreads];
-    const int g = blockIdx.x;
+__device__ __forceinline__ float cosine(double dot, double na, double nb) {
+    const double prod = na * nb;
+    return (float)(prod == 0.0 ? 0.0 : dot / sqrt(prod));
+}
+
+// The last workgroup of listed head li: reduce the head's partials into T
+// (LDS, lds_rows doubles) and finish by mode.
+__device__ void finish_head(const ScoreArgs &a, int li, double *T, float *s_scores, unsigned char *s_forced,
+                            unsigned char *s_keep) {
+    __shared__ double red[4][kRowBatch];
     const int tid = threadIdx.x;
-    const int nparts = a.chunks_per_unit * kWaves;
-    int t0, t1, u;
-    if (a.L <= a.F) {  // one unit = one segment inside frame t0
-        t0 = g / a.units_per_frame;
-        u = g - t0 * a.units_per_frame;
-        t1 = t0 + 1;
-    } else {           // the segment spans frames [t0, t1), one unit each
-        const int m = a.L / a.F;
-        t0 = g * m;
-        t1 = min(t0 + m, a.H);
-        u = 0;
-    }
-    const int li0 = a.pooled ? 0 : blockIdx.y;
-    const int nli = a.pooled ? a.heads.n : 1;
-    double dot = 0.0, na = 0.0, nb = 0.0;
-    if (!a.cached) {
-        const int per_head = (t1 - t0) * nparts;
-        const int n = nli * per_head;
-        for (int i = tid; i < n; i += kThreads) {
-            const int li = li0 + i / per_head, j = i % per_head;
-            const int t = t0 + j / nparts, k = j % nparts;
-            const double *pa = a.ws + ws_index(a, li, t, u, 0, 0) * 2;
-            const double *pb = a.ws + ws_index(a, li, t + 1, u, 0, 0) * 2;
-            na += pa[2 * k];
-            dot += pa[2 * k + 1];
-            nb += pb[2 * k];
+    const int h = a.heads.head[li];
+    const int n_rows = a.units * a.n_frames * 2;
+    const double *part = a.part + (int64_t)li * n_rows * a.n_cg;
+    // fixed quarters of the column groups: [q*n_cg/4, (q+1)*n_cg/4)
+    const int rr = tid % kRowBatch, qq = tid / kRowBatch;
+    const int c_lo = qq * a.n_cg / 4, c_hi = (qq + 1) * a.n_cg / 4;
+    for (int r0 = 0; r0 < n_rows; r0 += kRowBatch) {
+        const int r = r0 + rr;
+        double acc = 0.0;
+        if (r < n_rows) {
+            const double *p = part + (int64_t)r * a.n_cg;
+            for (int c = c_lo; c < c_hi; ++c) acc += p[c];
         }
-    } else {
-        // every term from the statistics, except the pair (H-1, H): DOT(H-1)
-        // and SQ(H) come from this step's partials
-        const int per_head = t1 - t0;
-        for (int i = tid; i < nli * per_head; i += kThreads) {
-            const int li = li0 + i / per_head, t = t0 + i % per_head;
-            const double *st = a.stats + stats_index(a, li, t, u) * 2;
-            na += st[0];
-            if (t + 1 < a.H) {
-                dot += st[1];
-                nb += st[2 * a.units_per_frame];  // SQ(t + 1)
-            }
-        }
-        if (t1 == a.H) {
-            for (int i = tid; i < nli * nparts; i += kThreads) {
-                const int li = li0 + i / nparts, k = i % nparts;
-                dot += a.ws[ws_index(a, li, a.H - 1, u, 0, 0) * 2 + 2 * k + 1];
-                nb += a.ws[ws_index(a, li, a.H, u, 0, 0) * 2 + 2 * k];
-            }
-        }
-    }
-    red[0][tid] = dot;
-    red[1][tid] = na;
-    red[2][tid] = nb;
-    __syncthreads();
-    for (int w = kThreads / 2; w > 0; w >>= 1) {
-        if (tid < w) {
-            red[0][tid] += red[0][tid + w];
-            red[1][tid] += red[1][tid + w];
-            red[2][tid] += red[2][tid + w];
-        }
+        red[qq][rr] = acc;
+        __syncthreads();
+        if (tid < kRowBatch && r0 + tid < n_rows) T[r0 + tid] = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
         __syncthreads();
     }
-    if (tid == 0) {
-        const double prod = red[1][0] * red[2][0];
-        const double cosv = prod == 0.0 ? 0.0 : red[0][0] / sqrt(prod);
-        const int64_t row = a.pooled ? 0 : (int64_t)a.heads.head[li0] * a.n_seg;
-        a.scores[row + g] = (float)cosv;
+
+    if (a.mode == kScoreModeHistory) {
+        // SQ(t) for t < H, DOT(t) for t < H - 1 (t_begin = 0)
+        double *st = a.stats + (int64_t)li * a.H * a.units * 2;
+        for (int i = tid; i < a.H * a.units; i += kThreads) {
+            const int t = i / a.units, u = i - t * a.units;
+            st[(int64_t)i * 2] = T[row_of(a, u, t, 0)];
+            if (t + 1 < a.H) st[(int64_t)i * 2 + 1] = T[row_of(a, u, t, 1)];
+        }
+        return;
+    }
+    if (a.pooled) {
+        double *tot = a.totals + (int64_t)li * n_rows;
+        for (int r = tid; r < n_rows; r += kThreads) tot[r] = T[r];
+        return;  // the caller counts finished heads; the last one scores
+    }
+    const Terms tm{a, T, a.stats + (int64_t)li * a.H * a.units * 2};
+    for (int g = tid; g < a.n_seg; g += kThreads) {
+        int u, t0, t1;
+        seg_span(a, g, &u, &t0, &t1);
+        double dot = 0.0, na = 0.0, nb = 0.0;
+        for (int t = t0; t < t1; ++t) {
+            dot += tm.dot(t, u);
+            na += tm.sq(t, u);
+            nb += tm.sq(t + 1, u);
+        }
+        const float sc = cosine(dot, na, nb);
+        a.scores[(int64_t)h * a.n_seg + g] = sc;
+        if (a.select) s_scores[g] = sc;
+    }
+    if (a.select) {
+        __syncthreads();
+        sel::select_from_lds(a, li, h, s_scores, s_forced, s_keep, a.kept_seg, a.kv_len, tid, kThreads);
     }
 }
 
-// History statistics: one wave per (unit u, frame t < H, listed head li) sums
-// the frame's partials in a fixed order (lanes stride over the parts, then the
-// DPP tree) into SQ(t) and, for t < H-1, DOT(t).
-__global__ __launch_bounds__(64) void score_stats_kernel(ScoreArgs a) {
-    const int u = blockIdx.x, t = blockIdx.y, li = blockIdx.z;
-    const int lane = threadIdx.x;
-    const int nparts = a.chunks_per_unit * kWaves;
-    const double *p = a.ws + ws_index(a, li, t, u, 0, 0) * 2;
-    const bool has_dot = t + 1 < a.H;
-    double sq = 0.0, dot = 0.0;
-    for (int k = lane; k < nparts; k += 64) {
-        sq += p[2 * k];
-        if (has_dot) dot += p[2 * k + 1];
+// The last head to finish (pooled): one score per segment from every listed
+// head's per-frame sums, summed over the heads in list order.
+__device__ void finish_pooled(const ScoreArgs &a) {
+    const int n_rows = a.units * a.n_frames * 2;
+    for (int g = threadIdx.x; g < a.n_seg; g += kThreads) {
+        int u, t0, t1;
+        seg_span(a, g, &u, &t0, &t1);
+        double dot = 0.0, na = 0.0, nb = 0.0;
+        for (int li = 0; li < a.heads.n; ++li) {
+            const Terms tm{a, a.totals + (int64_t)li * n_rows, a.stats + (int64_t)li * a.H * a.units * 2};
+            for (int t = t0; t < t1; ++t) {
+                dot += tm.dot(t, u);
+                na += tm.sq(t, u);
+                nb += tm.sq(t + 1, u);
+            }
+        }
+        a.scores[g] = cosine(dot, na, nb);
     }
-    sq = wave_sum(sq);
-    dot = wave_sum(dot);
-    if (lane == 63) {
-        double *st = a.stats + stats_index(a, li, t, u) * 2;
-        st[0] = sq;
-        if (has_dot) st[1] = dot;
+}
+
+// Agent-scope arrival on a counter; true in every thread of the workgroup
+// that arrives last (the counter is then reset to zero for the next call).
+__device__ __forceinline__ bool arrive_last(uint32_t *counter, uint32_t expected, uint32_t *flag) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // this wave's stores before the arrival
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t old = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const bool last = old + 1 == expected;
+        if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *flag = last ? 1u : 0u;
+    }
+    __syncthreads();
+    const bool last = *flag != 0;
+    if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    return last;
+}
+
+template <bool F32>
+__global__ __launch_bounds__(kThreads, 5) void score_kernel(ScoreArgs a) {
+    extern __shared__ double dyn[];            // finisher: lds_rows doubles, then n_seg floats + 2 n_seg bytes
+    __shared__ u32x4 edge[kWaves][kV][64];     // first frame of each wave's run
+    __shared__ uint32_t flag;
+
+    const int cg = blockIdx.x, u = blockIdx.y, li = blockIdx.z;
+    const int h = a.heads.head[li];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int nf = a.n_frames;
+    const int nw = min(kWaves, nf);            // waves with frames
+    const int fa = w < nw ? (w * nf) / nw : nf;
+    const int fb = w < nw ? ((w + 1) * nf) / nw : nf;
+
+    int col[kV];
+    bool ok[kV];
+#pragma unroll
+    for (int j = 0; j < kV; ++j) {
+        col[j] = cg * kCols + j * 64 + lane;
+        ok[j] = col[j] < a.unit_vecs;
+    }
+    const u32x4 *hist = (const u32x4 *)a.K_hist + (int64_t)h * a.cap * a.frame_vecs + (int64_t)u * a.unit_vecs;
+    const u32x4 *cur = (const u32x4 *)a.K_cur + (int64_t)h * a.cur_head_vecs + (int64_t)u * a.unit_vecs;
+    auto load = [&](int f, u32x4 (&x)[kV]) {
+        const int t = a.t_begin + f;
+        const u32x4 *base = t < a.H ? hist + (int64_t)a.slots.slot[t] * a.frame_vecs : cur;
+#pragma unroll
+        for (int j = 0; j < kV; ++j) x[j] = ok[j] ? __builtin_nontemporal_load(base + col[j]) : u32x4{0, 0, 0, 0};
+    };
+    double *part = a.part + (int64_t)li * (a.units * nf * 2) * a.n_cg + cg;
+    auto put = [&](int f, int q, double v) {
+        if (lane == 63) part[(int64_t)row_of(a, u, f, q) * a.n_cg] = v;
+    };
+
+    u32x4 prev[kV] = {};
+    constexpr int MF = kMaxF<F32>;
+    for (int f0 = fa; f0 < fb; f0 += MF) {
+        const int nb = min(MF, fb - f0);
+        u32x4 x[MF][kV];
+#pragma unroll
+        for (int i = 0; i < MF; ++i)
+            if (i < nb) load(f0 + i, x[i]);
+        if (f0 == fa) {
+#pragma unroll
+            for (int j = 0; j < kV; ++j) edge[w][j][lane] = x[0][j];
+        }
+#pragma unroll
+        for (int i = 0; i < MF; ++i) {
+            if (i < nb) {
+                const int f = f0 + i;
+                put(f, 0, wave_sum(lane_sq<F32>(x[i])));
+                if (f > fa) put(f - 1, 1, wave_sum(lane_dot<F32>(prev, x[i])));
+#pragma unroll
+                for (int j = 0; j < kV; ++j) prev[j] = x[i][j];
+            }
+        }
+    }
+    __syncthreads();
+    // the product across the run boundary: this run's last frame with the next run's first
+    if (w + 1 < nw) {
+        u32x4 nx[kV];
+#pragma unroll
+        for (int j = 0; j < kV; ++j) nx[j] = edge[w + 1][j][lane];
+        put(fb - 1, 1, wave_sum(lane_dot<F32>(prev, nx)));
+    }
+
+    if (!arrive_last(a.counters + li, (uint32_t)(a.units * a.n_cg), &flag)) return;
+    double *T = dyn;
+    float *s_scores = (float *)(dyn + a.lds_rows);
+    unsigned char *s_forced = (unsigned char *)(s_scores + a.n_seg);
+    finish_head(a, li, T, s_scores, s_forced, s_forced + a.n_seg);
+    if (a.pooled && a.mode != kScoreModeHistory) {
+        if (!arrive_last(a.counters + a.heads.n, (uint32_t)a.heads.n, &flag)) return;
+        finish_pooled(a);
     }
 }
 
 }  // namespace
 
-size_t score_workspace_doubles(int n_dyn, int H, int units_per_frame, int chunks_per_unit) {
-    return (size_t)n_dyn * (H + 1) * units_per_frame * chunks_per_unit * kWaves * 2;
+int score_column_groups(int64_t unit_vecs) { return (int)((unit_vecs + kCols - 1) / kCols); }
+
+size_t score_workspace_bytes(int n_list, int H, int units, int n_cg) {
+    if (n_list == 0 || H == 0) return 0;
+    const size_t rows = (size_t)units * (H + 1) * 2;  // the full pass streams H + 1 frames
+    const size_t counters = ((size_t)(n_list + 1) * sizeof(uint32_t) + 255) & ~(size_t)255;
+    const size_t b = counters + ((size_t)n_list * rows * n_cg + (size_t)n_list * rows) * sizeof(double);
+    return (b + 255) & ~(size_t)255;
 }
 
-namespace {
-
-// Frames per part of a streamed range of `frames` frames (kScorePartFrames,
-// or the whole range when it is short).
-int split_parts(int frames, int *part_frames) {
-    if (frames <= kScorePartFrames + 1) {
-        *part_frames = frames;
-        return 1;
-    }
-    *part_frames = kScorePartFrames;
-    return (frames - 1 + kScorePartFrames - 1) / kScorePartFrames;  // parts share a boundary frame
+// The workspace of score_workspace_bytes split into counters, partials, sums.
+void score_workspace_layout(ScoreArgs &a, void *ws, int n_list, int H, int units, int n_cg) {
+    const size_t rows = (size_t)units * (H + 1) * 2;
+    const size_t counters = ((size_t)(n_list + 1) * sizeof(uint32_t) + 255) & ~(size_t)255;
+    a.counters = (uint32_t *)ws;
+    a.part = (double *)((char *)ws + counters);
+    a.totals = a.part + (size_t)n_list * rows * n_cg;
 }
 
-hipError_t launch_partials(const ScoreArgs &a0, bool f32, hipStream_t s) {
+hipError_t launch_score(const ScoreArgs &a0, bool f32, hipStream_t s) {
     ScoreArgs a = a0;
-    a.n_parts = split_parts(a.t_end - a.t_begin + 1, &a.part_frames);
-    dim3 grid((unsigned)a.chunks_per_unit, (unsigned)a.units_per_frame, (unsigned)(a.heads.n * a.n_parts));
+    if (a.heads.n == 0 || a.n_frames <= 0) return hipSuccess;
+    a.lds_rows = a.units * a.n_frames * 2;
+    size_t lds = (size_t)a.lds_rows * sizeof(double);
+    if (a.select) lds += (size_t)a.n_seg * (sizeof(float) + 2);
+    lds = (lds + 15) & ~(size_t)15;
+    const dim3 grid((unsigned)a.n_cg, (unsigned)a.units, (unsigned)a.heads.n);
     if (f32)
-        hipLaunchKernelGGL(score_partials_kernel<true>, grid, dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(score_kernel<true>, grid, dim3(kThreads), lds, s, a);
     else
-        hipLaunchKernelGGL(score_partials_kernel<false>, grid, dim3(kThreads), 0, s, a);
-    return hipGetLastError();
-}
-
-}  // namespace
-
-hipError_t launch_score_history(const ScoreArgs &a, bool f32, hipStream_t s) {
-    if (a.heads.n == 0 || a.H == 0) return hipSuccess;
-    ScoreArgs h = a;
-    h.t_begin = 0;
-    h.t_end = a.H - 1;
-    hipError_t e = launch_partials(h, f32, s);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(score_stats_kernel, dim3(a.units_per_frame, a.H, a.heads.n), dim3(64), 0, s, h);
-    return hipGetLastError();
-}
-
-hipError_t launch_score_cached(const ScoreArgs &a, bool f32, hipStream_t s) {
-    if (a.heads.n == 0 || a.H == 0) return hipSuccess;
-    ScoreArgs c = a;
-    c.t_begin = a.H - 1;
-    c.t_end = a.H;
-    c.cached = 1;
-    hipError_t e = launch_partials(c, f32, s);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(score_finalize_kernel, dim3(a.n_seg, a.pooled ? 1 : a.heads.n), dim3(kThreads), 0, s, c);
-    return hipGetLastError();
-}
-
-hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s) {
-    if (a.heads.n == 0 || a.H == 0) return hipSuccess;
-    ScoreArgs f = a;  // the full pass: frames 0..H, finalize from the partials
-    f.t_begin = 0;
-    f.t_end = a.H;
-    f.cached = 0;
-    hipError_t e = launch_partials(f, f32, s);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(score_finalize_kernel, dim3(a.n_seg, a.pooled ? 1 : a.heads.n), dim3(kThreads), 0, s, f);
+        hipLaunchKernelGGL(score_kernel<false>, grid, dim3(kThreads), lds, s, a);
     return hipGetLastError();
 }
 

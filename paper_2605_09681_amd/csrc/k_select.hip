@@ -7,7 +7,8 @@
 // select_common.h (rank inside the selection group below kk, forced segments
 // always kept).  Wave 0 then walks the segments in ascending order 64 at a
 // time, turning the keep flags into output positions with a ballot and a
-// masked bit count (mbcnt), and writes kept_seg and kv_len.
+// masked bit count (mbcnt), and writes kept_seg and kv_len
+// (sel::select_from_lds, which the fused score + select kernel also runs).
 #include "select_common.h"
 
 namespace fkv {
@@ -22,39 +23,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
 
     const int li = blockIdx.x;
     const int h = a.heads.head[li];
-    const int n = a.n_seg;
     const int tid = threadIdx.x;
-
-    for (int g = tid; g < n; g += kThreads) {
-        s[g] = a.scores[(int64_t)h * a.score_stride + g];
-        forced[g] = sel::is_forced(a, li, g) ? 1 : 0;
-    }
+    for (int g = tid; g < a.n_seg; g += kThreads) s[g] = a.scores[(int64_t)h * a.score_stride + g];
     __syncthreads();
-
-    for (int g = tid; g < n; g += kThreads)
-        keep[g] = (forced[g] || sel::keep_by_rank(a, li, s, forced, g)) ? 1 : 0;
-    __syncthreads();
-
-    if (tid < 64) {
-        int base = 0;
-        int tokens = 0;
-        for (int c0 = 0; c0 < n; c0 += 64) {
-            const int g = c0 + tid;
-            const bool kp = g < n && keep[g];
-            const uint64_t mask = __ballot(kp);
-            const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
-            if (kp) {
-                a.kept_seg[(int64_t)h * n + base + below] = g;
-                tokens += sel::seg_tokens(a, g);
-            }
-            base += __popcll(mask);
-        }
-        for (int p = base + tid; p < n; p += 64) a.kept_seg[(int64_t)h * n + p] = -1;
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) tokens += __shfl_xor(tokens, off);
-        if (tid == 0) a.kv_len[h] = tokens;
-    }
+    sel::select_from_lds(a, li, h, s, forced, keep, a.kept_seg, a.kv_len, tid, kThreads);
 }
 
 }  // namespace

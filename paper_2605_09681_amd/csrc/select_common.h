@@ -29,7 +29,8 @@ __device__ __forceinline__ bool key_less(float sa, int ga, float sb, int gb) {
 // another (the host checks it), so this is small 32-bit arithmetic: a
 // segment is a 1/(F/L) share of one frame, or L/F whole frames (the last
 // segment of the history possibly fewer).
-__device__ __forceinline__ void seg_frames(const SelectArgs &a, int g, int *first, int *last) {
+template <class A>
+__device__ __forceinline__ void seg_frames(const A &a, int g, int *first, int *last) {
     if (a.L <= a.F) {
         *first = *last = g / (a.F / a.L);
     } else {
@@ -40,25 +41,31 @@ __device__ __forceinline__ void seg_frames(const SelectArgs &a, int g, int *firs
 }
 
 // Does segment g intersect logical frames [0, sink) or [H - recent, H)?
-__device__ __forceinline__ bool is_forced(const SelectArgs &a, int li, int g) {
+template <class A>
+__device__ __forceinline__ bool is_forced(const A &a, int li, int g) {
     int first, last;
     seg_frames(a, g, &first, &last);
     return first < a.sink[li] || last >= a.H - a.recent[li];
 }
 
 // Tokens of segment g (only the last segment of the history can be short).
-__device__ __forceinline__ int seg_tokens(const SelectArgs &a, int g) {
+template <class A>
+__device__ __forceinline__ int seg_tokens(const A &a, int g) {
     if (a.L <= a.F) return a.L;
     int first, last;
     seg_frames(a, g, &first, &last);
     return (last - first + 1) * a.F;
 }
 
+// The helpers take any argument block with the fields F, L, H, n_seg and the
+// per-list-entry arrays sink, recent, scope and k (SelectArgs, ScoreArgs).
+
 // Keep decision of a non-forced segment g with score sg, given the scores s[]
 // and forced flags of all n_seg segments (in LDS): its rank inside its group
 // (one frame's segments for FKV_SCOPE_FRAME, all segments otherwise) is below
 // kk.
-__device__ __forceinline__ bool keep_by_rank(const SelectArgs &a, int li, const float *s,
+template <class A>
+__device__ __forceinline__ bool keep_by_rank(const A &a, int li, const float *s,
                                              const unsigned char *forced, int g) {
     int lo = 0, hi = a.n_seg;
     if (a.scope[li] == FKV_SCOPE_FRAME) {
@@ -72,6 +79,43 @@ __device__ __forceinline__ bool keep_by_rank(const SelectArgs &a, int li, const 
     for (int g2 = lo; g2 < hi && rank < kk; ++g2)
         rank += (!forced[g2] && g2 != g && key_less(s[g2], g2, sg, g)) ? 1 : 0;
     return rank < kk;
+}
+
+// One workgroup decides head h's keep set from its scores s[0..n_seg) in LDS
+// and writes kept_seg[h] (ascending, -1 padded) and kv_len[h].  forced and
+// keep are LDS scratch of n_seg bytes.  Every thread of the workgroup calls
+// it (it contains barriers); nthreads is the workgroup size.
+template <class A>
+__device__ __forceinline__ void select_from_lds(const A &a, int li, int h, const float *s,
+                                                unsigned char *forced, unsigned char *keep,
+                                                int32_t *kept_seg, int32_t *kv_len, int tid,
+                                                int nthreads) {
+    const int n = a.n_seg;
+    for (int g = tid; g < n; g += nthreads) forced[g] = is_forced(a, li, g) ? 1 : 0;
+    __syncthreads();
+    for (int g = tid; g < n; g += nthreads)
+        keep[g] = (forced[g] || keep_by_rank(a, li, s, forced, g)) ? 1 : 0;
+    __syncthreads();
+    if (tid < 64) {
+        int base = 0;
+        int tokens = 0;
+        for (int c0 = 0; c0 < n; c0 += 64) {
+            const int g = c0 + tid;
+            const bool kp = g < n && keep[g];
+            const uint64_t mask = __ballot(kp);
+            const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+            if (kp) {
+                kept_seg[(int64_t)h * n + base + below] = g;
+                tokens += seg_tokens(a, g);
+            }
+            base += __popcll(mask);
+        }
+        for (int p = base + tid; p < n; p += 64) kept_seg[(int64_t)h * n + p] = -1;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) tokens += __shfl_xor(tokens, off);
+        if (tid == 0) kv_len[h] = tokens;
+    }
 }
 
 }  // namespace sel

@@ -1,26 +1,28 @@
-"""One attention layer's Forcing-KV step: the four C-ABI calls in order.
+"""One attention layer's Forcing-KV step, and a multi-layer rollout driver.
 
 :class:`CompressedLayer` owns the per-layer intermediate device buffers
 (scores, kept segment ids, compressed K/V slabs, kv_len, the scoring and
 attention workspaces) sized from the shape and budgets, and runs one AR step
-of one layer:
+of one layer.  The four stages of the method:
 
 1. ``fkv_score_segments``  (dynamic heads, Eq. 3 similarity)
 2. ``fkv_select_compact``  (dynamic heads, Eq. 3 BottomK + compaction)
 3. ``fkv_compress_static`` (static heads, Eq. 2)
 4. ``fkv_chunk_attention`` (all heads, Eq. 2 / Eq. 4)
 
-Steps 1-2 and step 3 touch disjoint heads.  :meth:`CompressedLayer.step`
-therefore runs, on a second stream (default priority), the static heads'
-attention, while the current stream scores and compacts the dynamic heads and
-then attends them (``fkv_chunk_attention_heads``): the HBM-bound compression
-of the dynamic heads runs under the MFMA-bound attention of the static heads.
-For bf16 with frames of at least 64 tokens the static heads are attended in
-place (``fkv_chunk_attention_static``: their kept frames are read straight
-from the cache, so step 3 is skipped and their rows of Kc/Vc/kv_len are left
-unwritten); otherwise the side stream gathers them first.
-:meth:`CompressedLayer.compress` alone overlaps the static gather with the
-dynamic compression the same way.
+:meth:`CompressedLayer.step` runs them in one of three ways (``step_mode``):
+
+* ``"paged"`` (the default where the shape allows it: bf16, frames and
+  segment pieces of at least 64 tokens): ``fkv_score_select`` scores the
+  dynamic heads and selects their kept segments in one launch, then ONE
+  ``fkv_chunk_attention_paged`` launch attends every head with its kept
+  history read in place from the cache -- no compacted copy, no gather;
+* ``"paged2"``: the same, with the static heads' attention on a second stream
+  (default priority) next to the dynamic heads' scoring and attention;
+* ``"compact"``: the static heads attended in place (or gathered first) on a
+  side stream while the dynamic heads are scored, compacted into Kc/Vc and
+  attended on the current stream.
+
 The individual stages enqueue on the current torch stream; nothing
 synchronises with the host.
 """
@@ -33,7 +35,8 @@ import torch
 
 from . import (FKV_DYNAMIC, FKV_STATIC, fkv_append_frames, fkv_attention_mass,
                fkv_attention_workspace_size, fkv_chunk_attention, fkv_chunk_attention_heads,
-               fkv_chunk_attention_static, fkv_classify_heads,
+               fkv_chunk_attention_paged, fkv_chunk_attention_static, fkv_classify_heads, fkv_score_select,
+               fkv_select,
                fkv_chunk_attention_fp8, fkv_compress_static, fkv_fp8_pack, fkv_fp8_sizes,
                fkv_num_segments, fkv_score_pooled, fkv_score_pooled_workspace_size,
                fkv_score_history, fkv_score_segments, fkv_score_segments_cached,
@@ -46,11 +49,21 @@ def static_in_place_supported(dtype, frame_tokens: int) -> bool:
     return dtype in ("bf16", 0) and frame_tokens >= 64
 
 
+def paged_supported(dtype, frame_tokens: int, seg_tokens: int, cap_frames: int) -> bool:
+    """Whether fkv_chunk_attention_paged reads dynamic heads of this shape in
+    place: bf16, pieces of min(L, F) >= 64 tokens, at most 256 pieces in the
+    cache."""
+    piece = min(seg_tokens, frame_tokens)
+    return (static_in_place_supported(dtype, frame_tokens) and piece >= 64
+            and cap_frames * (frame_tokens // piece) <= 256)
+
+
 class CompressedLayer:
     def __init__(self, n_heads: int, head_dim: int, frame_tokens: int, hist_frames: int,
                  cap_frames: int, chunk_frames: int, seg_tokens: int, dtype: str,
                  budgets: Sequence, device="cuda", slab: Optional[int] = None,
-                 balanced: bool = True, overlap: bool = True, in_place: Optional[bool] = None):
+                 balanced: bool = True, overlap: bool = True, in_place: Optional[bool] = None,
+                 step_mode: Optional[str] = None):
         if len(budgets) != n_heads:
             raise ValueError(f"{len(budgets)} head budgets for {n_heads} heads")
         self.shape = make_shape(n_heads, head_dim, frame_tokens, hist_frames, cap_frames,
@@ -69,7 +82,8 @@ class CompressedLayer:
         self.Vc = torch.zeros((n_heads, self.slab, head_dim), dtype=dt, device=dev)
         self.kv_len = torch.zeros((n_heads,), dtype=torch.int32, device=dev)
         self.ws_bytes = fkv_score_workspace_size(self.shape, self.heads)
-        self.workspace = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
+        # scoring workspace: zero-filled once (its arrival counters), every call leaves it so
+        self.workspace = torch.zeros(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
         self.attn_workspace = self.attn_workspace2 = None
         if balanced:
             with torch.cuda.device(dev):
@@ -91,6 +105,17 @@ class CompressedLayer:
         if in_place and not can:
             raise ValueError("in-place static attention needs bf16 and frame_tokens >= 64")
         self.static_in_place = can if in_place is None else bool(in_place)
+        can_paged = paged_supported(dtype, frame_tokens, seg_tokens, cap_frames)
+        if step_mode is None:
+            step_mode = "paged" if can_paged and (in_place is None or in_place) else "compact"
+        if step_mode not in ("paged", "paged2", "compact"):
+            raise ValueError(f"step_mode {step_mode!r}")
+        if step_mode != "compact" and not can_paged:
+            raise ValueError("paged steps need bf16, frame and segment pieces of >= 64 tokens and "
+                             "cap_frames * F / min(L, F) <= 256")
+        self.step_mode = step_mode
+        if step_mode == "paged2" and self.side is None and overlap and self.has_static and self.has_dynamic:
+            self.side = torch.cuda.Stream(device=dev)
 
     # individual stages -------------------------------------------------------
     def score(self, K_hist, frame_slot, K_cur):
@@ -158,14 +183,52 @@ class CompressedLayer:
         fkv_chunk_attention_static(self.shape, self.heads, K_hist, V_hist, frame_slot, Q, K_cur, V_cur,
                                    self.scale, O, lse, workspace)
 
+    def score_select(self, K_hist, frame_slot, K_cur):
+        """Scores and kept segments of the dynamic heads in one launch (no copy)."""
+        fkv_score_select(self.shape, self.heads, K_hist, frame_slot, K_cur, self.scores, self.kept_seg,
+                         self.kv_len, self.workspace)
+
+    def attention_paged(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse=None, head_list=None,
+                        workspace=None):
+        """Attention of the listed heads (all by default), every kept history
+        read in place from the cache."""
+        fkv_chunk_attention_paged(self.shape, self.heads, K_hist, V_hist, frame_slot, self.kept_seg, self.kv_len,
+                                  Q, K_cur, V_cur, self.scale, O, lse,
+                                  self.attn_workspace if workspace is None else workspace, head_list)
+
     def step(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse=None, events=None):
-        """One AR step of the layer.  ``events`` (optional) maps a launch name to
-        a pair of torch.cuda.Events that are recorded around that attention
-        launch on the stream it runs on ("attention", or "static_attention" and
-        "dynamic_attention" in the two-stream step), for per-launch timing."""
+        """One AR step of the layer (see the module docstring for the modes).
+        ``events`` (optional) maps a launch name to a pair of torch.cuda.Events
+        recorded around that attention launch on the stream it runs on
+        ("attention" for one launch, "static_attention" and "dynamic_attention"
+        for the two-stream steps), for per-launch timing."""
         def mark(name, i, stream):
             if events is not None and name in events:
                 events[name][i].record(stream)
+        if self.step_mode == "paged" or (self.step_mode == "paged2" and self.side is None):
+            cur = torch.cuda.current_stream(self.device)
+            if self.has_dynamic:
+                self.score_select(K_hist, frame_slot, K_cur)
+            mark("attention", 0, cur)
+            self.attention_paged(K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse)
+            mark("attention", 1, cur)
+            return
+        if self.step_mode == "paged2":
+            main = torch.cuda.current_stream(self.device)
+            self.side.wait_stream(main)
+            with torch.cuda.stream(self.side):
+                mark("static_attention", 0, self.side)
+                self.attention_paged(K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse, self.static_heads,
+                                     self.attn_workspace2)
+                mark("static_attention", 1, self.side)
+            for t in (K_hist, V_hist, Q, K_cur, V_cur, O) + ((lse,) if lse is not None else ()):
+                t.record_stream(self.side)
+            self.score_select(K_hist, frame_slot, K_cur)
+            mark("dynamic_attention", 0, main)
+            self.attention_paged(K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse, self.dynamic_heads)
+            mark("dynamic_attention", 1, main)
+            main.wait_stream(self.side)
+            return
         if self.side is None:
             cur = torch.cuda.current_stream(self.device)
             if self.static_in_place and not self.has_dynamic:
@@ -247,14 +310,16 @@ class RolloutStack:
     chunk's frames back with :meth:`append`.  Layers run one after another, so
     they share one set of compressed-cache buffers, sized for a full window;
     the history length H = len(frame_slot) may grow from chunk to chunk (0 on
-    the first one).  Per layer and AR step :meth:`run_layer` runs the static
-    heads' attention on a side stream (read in place from the cache for bf16
-    and frames of at least 64 tokens, else gathered first) next to the
-    dynamic heads' scoring, compaction and attention, or -- with a shared
-    score row from :meth:`score_pooled` -- the first-block proxy of Sec. 4.3:
-    the dynamic heads of every layer select with one similarity row computed
-    from one layer's keys pooled over all heads.  ``budgets`` are per-head
-    objects with
+    the first one).  Per layer and AR step :meth:`run_layer` either (step_mode
+    "paged", the default where the shape allows it) scores and selects the
+    dynamic heads in one launch and then attends every head in one launch with
+    its kept history read in place from the cache, or ("compact") runs the
+    static heads' attention on a side stream (read in place for bf16 and
+    frames of at least 64 tokens, else gathered first) next to the dynamic
+    heads' scoring, compaction and attention.  With a shared score row from
+    :meth:`score_pooled` -- the first-block proxy of Sec. 4.3 -- the dynamic
+    heads of every layer select with one similarity row computed from one
+    layer's keys pooled over all heads.  ``budgets`` are per-head objects with
     type/sink_frames/recent_frames/keep_k/scope for the given H.
 
     Incremental rescoring: :meth:`history` stores a layer's per-frame
@@ -265,7 +330,7 @@ class RolloutStack:
 
     def __init__(self, n_layers: int, n_heads: int, head_dim: int, frame_tokens: int, window: int,
                  chunk_frames: int, seg_tokens: int, dtype: str = "bf16", device="cuda",
-                 overlap: bool = True):
+                 overlap: bool = True, step_mode: Optional[str] = None):
         self.n_layers, self.n_heads, self.d = n_layers, n_heads, head_dim
         self.F, self.window, self.C, self.L = frame_tokens, window, chunk_frames, seg_tokens
         self.dtype_name = dtype
@@ -286,8 +351,9 @@ class RolloutStack:
         self.pooled_row = torch.zeros((max(self.n_seg_max, 1),), dtype=torch.float32, device=dev)
         # workspaces: the largest history with every head dynamic bounds the scoring workspace
         all_dyn = make_heads([_Budget(FKV_DYNAMIC, 0, 0, 0, 1)] * n_heads)
-        self.score_ws = torch.empty(max(fkv_score_workspace_size(full, all_dyn), 1), dtype=torch.uint8, device=dev)
-        self.pooled_ws = torch.empty(max(fkv_score_pooled_workspace_size(full), 1), dtype=torch.uint8, device=dev)
+        # (scoring workspaces are zero-filled once: the one-launch reduction's arrival counters)
+        self.score_ws = torch.zeros(max(fkv_score_workspace_size(full, all_dyn), 1), dtype=torch.uint8, device=dev)
+        self.pooled_ws = torch.zeros(max(fkv_score_pooled_workspace_size(full), 1), dtype=torch.uint8, device=dev)
         with torch.cuda.device(dev):
             n = fkv_attention_workspace_size(full)
         self.attn_ws = torch.empty(max(n, 1), dtype=torch.uint8, device=dev) if n > 0 else None
@@ -295,6 +361,12 @@ class RolloutStack:
         self.scale = 1.0 / math.sqrt(head_dim)
         self.side = torch.cuda.Stream(device=dev) if overlap else None
         self.static_in_place = static_in_place_supported(dtype, frame_tokens)
+        can_paged = paged_supported(dtype, frame_tokens, seg_tokens, window)
+        if step_mode is None:
+            step_mode = "paged" if can_paged else "compact"
+        if step_mode not in ("paged", "compact") or (step_mode == "paged" and not can_paged):
+            raise ValueError(f"step_mode {step_mode!r} is not available for this shape")
+        self.step_mode = step_mode
         self._shapes, self._heads = {}, {}
         # per-layer statistics of incremental rescoring (listed heads x window x units x 2)
         units = frame_tokens // min(seg_tokens, frame_tokens)
@@ -370,6 +442,21 @@ class RolloutStack:
         Kh, Vh = self.K_hist[layer], self.V_hist[layer]
         scores, kept = self.views(H)
         has_static, has_dynamic = FKV_STATIC in types, FKV_DYNAMIC in types
+        if self.step_mode == "paged":
+            # one stream: scores + kept segments, then one attention launch over
+            # every head with its kept history read in place (no copy)
+            if has_dynamic:
+                if pooled is not None:
+                    fkv_select(shape, heads, pooled, kept, self.kv_len, shared_row=True)
+                elif incremental and H > 0:
+                    fkv_score_segments_cached(shape, heads, Kh, frame_slot, K_cur, self._stats[layer], scores,
+                                              self.score_ws)
+                    fkv_select(shape, heads, scores, kept, self.kv_len)
+                else:
+                    fkv_score_select(shape, heads, Kh, frame_slot, K_cur, scores, kept, self.kv_len, self.score_ws)
+            fkv_chunk_attention_paged(shape, heads, Kh, Vh, frame_slot, kept, self.kv_len, Q, K_cur, V_cur,
+                                      self.scale, O, lse, self.attn_ws)
+            return
         main = torch.cuda.current_stream(self.device)
         side = self.side if (self.side is not None and has_static and has_dynamic) else None
         att = (self.Kc, self.Vc, self.kv_len, K_cur, V_cur, self.scale, O)

@@ -371,3 +371,52 @@ def test_binding_rejects_wrong_head_count(fkv):
     with pytest.raises(TypeError):
         fkv.fkv_score_workspace_size(shape, [W.HeadBudget(W.STATIC, 1, 1)] * 2)
     assert fkv.fkv_score_stats_size(shape, None, pooled=True) > 0
+
+
+def test_paged_attention_arg_errors(fkv):
+    """fkv_chunk_attention_paged validates before any device work: bf16 and
+    F >= 64; with a dynamic head listed, pieces of min(L, F) >= 64 tokens and at
+    most 256 pieces in the cache, kv_len and (H > 0) kept_seg present; the head
+    list like fkv_chunk_attention_heads."""
+    L = fkv.lib()
+
+    def call(shape, heads=None, ids=None, kept=FAKE, kv=FAKE, K=FAKE, scale=0.1):
+        H = shape.hist_frames
+        sl = (ctypes.c_int32 * max(H, 1))(*range(H))
+        arr = None if ids is None else (ctypes.c_int32 * max(len(ids), 1))(*ids)
+        return L.fkv_chunk_attention_paged(ctypes.byref(shape), heads or _heads(fkv), arr,
+                                           0 if ids is None else len(ids), K, FAKE, sl, kept, kv, FAKE, FAKE, FAKE,
+                                           ctypes.c_float(scale), FAKE, None, None, 0, None)
+    assert call(_shape(fkv, dtype="f32")) == 2
+    assert call(_shape(fkv, frame_tokens=32, seg_tokens=32)) == 2
+    assert call(_shape(fkv, seg_tokens=32)) == 2                       # dynamic pieces of 32 tokens
+    assert "min(seg_tokens" in fkv.fkv_last_error()
+    assert call(_shape(fkv, seg_tokens=32), ids=[0], scale=-1.0) == 1   # static head only: past the piece rule
+    big = _shape(fkv, frame_tokens=256, seg_tokens=64, hist_frames=4, cap_frames=65)  # 65 x 4 pieces
+    assert call(big) == 2 and "256" in fkv.fkv_last_error()
+    assert call(_shape(fkv), kv=None) == 1
+    assert call(_shape(fkv), kept=None) == 1
+    assert call(_shape(fkv, hist_frames=0), kept=None, K=None, scale=0.0) == 1   # H = 0: kept_seg not needed
+    assert "scale" in fkv.fkv_last_error()
+    assert call(_shape(fkv), ids=[0, 0]) == 1
+    assert call(_shape(fkv), ids=[2]) == 1
+    assert call(_shape(fkv), scale=0.0) == 1
+    assert call(_shape(fkv), K=None) == 1
+
+
+def test_select_entry_points_arg_errors(fkv):
+    """fkv_select and fkv_score_select validate before any device work."""
+    L = fkv.lib()
+    shape = _shape(fkv)
+    heads = _heads(fkv)
+    assert L.fkv_select(ctypes.byref(shape), heads, FAKE, 2, FAKE, FAKE, None) == 1       # shared_row not 0/1
+    assert L.fkv_select(ctypes.byref(shape), heads, None, 0, FAKE, FAKE, None) == 1
+    assert L.fkv_select(ctypes.byref(shape), heads, FAKE, 0, FAKE, None, None) == 1
+    need = fkv.fkv_score_workspace_size(shape, heads)
+    sl = (ctypes.c_int32 * 4)(0, 1, 2, 3)
+    call = lambda ws=FAKE, n=need, kept=FAKE, slots=sl: L.fkv_score_select(
+        ctypes.byref(shape), heads, FAKE, slots, FAKE, FAKE, kept, FAKE, ws, n, None)
+    assert call(n=need - 1) == 3
+    assert call(ws=None) == 1
+    assert call(kept=None) == 1
+    assert call(slots=(ctypes.c_int32 * 4)(0, 1, 2, 4)) == 1

@@ -5,14 +5,16 @@ ring of rotating slots wrapping many times, every step checked against the
 oracle, which keeps its own copy of every layer's cache through its own
 append.
 
-* small shape (4 heads, F = 64, window 7, 2-frame chunks): every chunk of
-  every layer, compression bit-exact and attention on every query row; layer
-  1 scores incrementally (history statistics once per chunk);
+* small shape (4 heads, F = 64, window 7, 2-frame chunks; half-frame
+  segments through the compacting step, one- and two-frame segments through
+  the paged step): every chunk of every layer, selection (and compaction)
+  bit-exact and attention on every query row; layer 1 scores incrementally
+  (history statistics once per chunk);
 * 480P shape (12 heads, F = 1560, window 21, 3-frame chunks: 180 frames, the
   20 rotating slots wrap 8 times): kept segments and kv_len of every chunk of
-  every layer bit-exact; compacted K/V bit-exact and attention on sampled
-  rows at sampled (chunk, layer) units; both layers' caches bit-exact at the
-  end.
+  every layer bit-exact; the paged step's attention (kept history read in
+  place) on sampled rows at sampled (chunk, layer) units; both layers' caches
+  bit-exact at the end.
 """
 import math
 
@@ -50,19 +52,26 @@ def _budgets(mask_row, H, F, L, recent_static):
 
 
 def _wraps(n_chunks, C, window, sink=1):
-    """How many times the rotating part of the ring is overwritten."""
+    """How many times the write pointer returns to the first rotating slot:
+    video frame v >= sink goes to slot sink + (v - sink) % (window - sink), so
+    it wraps at v = sink + j * (window - sink), j >= 1."""
     frames = n_chunks * C
-    return (frames - window) / (window - sink)
+    return (frames - 1 - sink) // (window - sink)
 
 
-def test_long_rollout_60_chunks_small_every_step():
+@pytest.mark.parametrize("L", [32, 64, 128])
+def test_long_rollout_60_chunks_small_every_step(L):
+    """L = 32: the compacting step (pieces below 64 tokens); L = 64 and 128 (one
+    and two frames per segment): the paged step, every head read in place."""
     from paper_2605_09681_amd.layer import RolloutStack
     from types import SimpleNamespace
-    n_layers, nh, d, F, window, C, L = 2, 4, 64, 64, 7, 2, 32
+    n_layers, nh, d, F, window, C = 2, 4, 64, 64, 7, 2
     n_chunks = 60
     assert _wraps(n_chunks, C, window) >= 8
     masks = W.rollout_head_masks(31, n_layers=n_layers, n_heads=nh, n_dynamic=2)
     stack = RolloutStack(n_layers, nh, d, F, window, C, L)
+    assert stack.step_mode == ("compact" if L < 64 else "paged")
+    paged = stack.step_mode == "paged"
     keys = W.ar1_key_frames(61, nh, n_chunks * C, F, d, 0.9, "bf16")     # [nh][frames][F][d]
     vals = W.normal_tensor(61, 7, (nh, n_chunks * C, F, d), "bf16")
     qs = W.normal_tensor(61, 8, (nh, n_chunks * C * F, d), "bf16")
@@ -76,7 +85,7 @@ def test_long_rollout_60_chunks_small_every_step():
         Q = np.ascontiguousarray(qs[:, i * C * F:(i + 1) * C * F])
         Kq_d, Vq_d, Q_d = to_dev(Kq, "bf16"), to_dev(Vq, "bf16"), to_dev(Q, "bf16")
         for layer in range(n_layers):
-            _print("long-rollout-small", chunk=i, layer=layer, H=H)
+            _print("long-rollout-small", L=L, chunk=i, layer=layer, H=H)
             heads = _budgets(masks[layer], H, F, L, 2)
             incremental = layer == 1 and H > 0
             if incremental:
@@ -90,7 +99,8 @@ def test_long_rollout_60_chunks_small_every_step():
             ref = oracle.run_layer(cfg, x, scale=1 / math.sqrt(d))
             scores, kept = stack.views(H)
             got = SimpleNamespace(kv_len=stack.kv_len, scores=scores, kept_seg=kept, Kc=stack.Kc, Vc=stack.Vc)
-            assert_compression_exact(cfg, got, ref, skip_static=stack.static_in_place)
+            assert_compression_exact(cfg, got, ref, skip_static=stack.static_in_place or paged,
+                                     skip_dynamic_copy=paged)
             assert_attention_close(O, ref, "bf16", lse)
         dst = W.chunk_write_slots(i, C, window)
         for layer in range(n_layers):
@@ -127,6 +137,8 @@ def test_long_rollout_60_chunks_480p_sampled():
     sampled = {(7, 1), (15, 0), (29, 1), (44, 0), (59, 1)}
     masks = W.rollout_head_masks(0, n_layers=n_layers)
     stack = RolloutStack(n_layers, nh, d, F, window, C, L)
+    paged = stack.step_mode == "paged"
+    assert paged
     K_o = np.zeros((n_layers, nh, window, F, d), np.uint16)
     V_o = np.zeros_like(K_o)
     for i in range(n_chunks):
@@ -151,7 +163,7 @@ def test_long_rollout_60_chunks_480p_sampled():
                 ref = oracle.run_layer(cfg, x, rows=rows, scale=1 / math.sqrt(d))
                 got = SimpleNamespace(kv_len=stack.kv_len, scores=scores, kept_seg=kept, Kc=stack.Kc,
                                       Vc=stack.Vc)
-                assert_compression_exact(cfg, got, ref, skip_static=stack.static_in_place)
+                assert_compression_exact(cfg, got, ref, skip_static=True, skip_dynamic_copy=paged)
                 assert_attention_close(O, ref, "bf16", lse)
             else:
                 # selection only: scores, kept segment ids and kv_len of the dynamic heads

@@ -179,7 +179,7 @@ def test_pipelined_step(case):
         x = W.make_layer_inputs(cfg, seed=31, frame_slot=slot)
         rows = sample_rows(cfg.lq, 8 if case != "1080p" else 4, seed=31)
     _print_case("pipelined-step", case=case)
-    layer = make_layer(cfg, in_place=False if case == "480p-gather" else None)
+    layer = make_layer(cfg, in_place=False if case == "480p-gather" else None, step_mode="compact")
     assert layer.side is not None and (cfg.dtype == "f32" or layer.attn_workspace2 is not None)
     assert layer.static_in_place == (cfg.dtype == "bf16" and case != "480p-gather")
     d = dev_inputs(x)
@@ -308,7 +308,7 @@ def test_incremental_rescoring(dtype, F, L, pooled):
     shape = fkv.make_shape(cfg.n_heads, cfg.head_dim, F, cfg.hist_frames, cfg.cap_frames, cfg.chunk_frames, L, dtype)
     heads = fkv.make_heads(cfg.heads)
     ws_bytes = fkv.fkv_score_pooled_workspace_size(shape) if pooled else fkv.fkv_score_workspace_size(shape, heads)
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")   # scoring workspaces start zero-filled
     stats = torch.empty(fkv.fkv_score_stats_size(shape, heads, pooled) // 8, dtype=torch.float64, device="cuda")
     Kh = to_dev(x.K_hist, dtype)
     fkv.fkv_score_history(shape, heads, Kh, slot, stats, ws, pooled=pooled)
@@ -444,15 +444,17 @@ def test_determinism():
     np.testing.assert_array_equal(from_dev(a[2]), from_dev(b[2]))
 
 
-def test_determinism_pipelined_step():
-    """The two-stream step (static heads in place on a side stream) gives the
-    same bits on repeated runs: the streams touch disjoint heads, each has its
-    own workspace, and nothing depends on how they interleave."""
+@pytest.mark.parametrize("mode", ["paged", "paged2", "compact"])
+def test_determinism_pipelined_step(mode):
+    """Every step mode gives the same bits on repeated runs: the one-launch
+    scoring reduces in a fixed order, the two-stream steps touch disjoint heads
+    on their streams, each with its own workspace, and nothing depends on how
+    they interleave."""
     cfg = W.wan_layer_config("480p")
-    _print_case("determinism-pipelined")
+    _print_case("determinism-step", mode=mode)
     x = W.make_layer_inputs(cfg, seed=13)
     d = dev_inputs(x)
-    layer = make_layer(cfg)
+    layer = make_layer(cfg, step_mode=mode)
     assert layer.static_in_place and layer.side is not None
     outs = []
     for _ in range(3):
