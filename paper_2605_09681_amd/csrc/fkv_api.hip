@@ -797,11 +797,22 @@ fkv_status chunk_attention_impl(const fkv_shape *shape, const fkv::HeadList &lis
         a.kept_seg = paged->kept_seg;
         a.pg_L = shape->seg_tokens;
         a.pg_nseg = fkv_num_segments(shape);
+        // one piece length for the launch: a frame, or min(L, F) when a dynamic
+        // head is read in place (static frames are then split into pieces too)
+        bool dyn = false;
+        for (int li = 0; li < list.n; ++li)
+            dyn |= paged->heads[list.head[li]].type == FKV_DYNAMIC && shape->hist_frames > 0;
+        a.pg_P = dyn ? std::min(shape->seg_tokens, shape->frame_tokens) : shape->frame_tokens;
+        a.pg_ppf = shape->frame_tokens / a.pg_P;
+        {   // M = floor(2^64 / P) + 1 (P >= 64, not a power of two in general)
+            const unsigned __int128 m = (((unsigned __int128)1) << 64) / (uint64_t)a.pg_P + 1;
+            a.pg_magic_hi = (uint32_t)(uint64_t)(m >> 32);
+            a.pg_magic_lo = (uint32_t)(uint64_t)m;
+        }
         for (int li = 0; li < list.n; ++li) {
             const int h = list.head[li];
             if (paged->heads[h].type == FKV_DYNAMIC && shape->hist_frames > 0) {
                 a.st_kept[li] = -1;
-                a.pg_piece[li] = std::min(shape->seg_tokens, shape->frame_tokens);
                 continue;
             }
             // static heads, and dynamic heads with nothing cached (no history, kv_len unread)
@@ -810,7 +821,6 @@ fkv_status chunk_attention_impl(const fkv_shape *shape, const fkv::HeadList &lis
             a.st_first[li] = p.n_first;
             a.st_gap[li] = p.gap;
             a.st_kept[li] = p.n_kept;
-            a.pg_piece[li] = shape->frame_tokens;
         }
         for (int t = 0; t < shape->hist_frames; ++t) a.slots.slot[t] = paged->frame_slot[t];
     }

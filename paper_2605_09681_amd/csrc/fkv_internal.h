@@ -98,6 +98,7 @@ struct ScoreArgs {
     uint32_t *counters;             // [heads.n + 1] arrivals per listed head, then finished heads
     double *part;                   // [li][row][n_cg] partial sums, row = (u*n_frames + f)*2 + q
     double *totals;                 // [li][row] per-head sums (pooled finish)
+    double *group;                  // [li][arrival group][row] sums of each arrival group's partials
     double *stats;                  // incremental rescoring: [li][H][units][2] = SQ(t), DOT(t, t+1)
     int64_t frame_vecs;             // 16-byte vectors per frame (F*d*esize/16)
     int64_t cur_head_vecs;          // 16-byte vectors per head of K_cur (C*F*d*esize/16)
@@ -142,20 +143,21 @@ struct AttnArgs {
     float scale_log2;               // scale * log2(e)
     // Paged heads (fkv_chunk_attention_static, fkv_chunk_attention_paged): the
     // retained history is read straight from the cache K_hist / V_hist
-    // [n_heads][cap][F][d] as a sequence of kept pieces of pg_piece[li] tokens.
-    // A static entry (st_kept[li] >= 0) keeps frames: kept frame y is logical
+    // [n_heads][cap][F][d] as a sequence of kept pieces of pg_P tokens (one
+    // piece length for the launch; pg_ppf = F / pg_P pieces per frame).  A
+    // static entry (st_kept[li] >= 0) keeps frames: kept frame y is logical
     // frame y (y < st_first[li]) or y + st_gap[li], in slot slots.slot[t], and
     // its history length is st_kept[li] * F (kv_len is not read).  A dynamic
     // entry (st_kept[li] < 0) keeps the segments listed in kept_seg[h] (as
-    // fkv_select writes them), pieces of min(L, F) tokens, and its history
-    // length is kv_len[h].
+    // fkv_select writes them) and its history length is kv_len[h].
     int32_t paged;
     const void *K_hist, *V_hist;
     int32_t F, cap;
+    int32_t pg_P, pg_ppf;           // piece tokens, pieces per frame
+    uint32_t pg_magic_hi, pg_magic_lo;  // floor(2^64 / pg_P) + 1: j0 / pg_P by multiplication
     int32_t pg_L, pg_nseg;          // segment length and segments per head (dynamic entries)
     const int32_t *kept_seg;        // [n_heads][pg_nseg] (dynamic entries)
     int32_t st_first[FKV_MAX_HEADS], st_gap[FKV_MAX_HEADS], st_kept[FKV_MAX_HEADS];
-    int32_t pg_piece[FKV_MAX_HEADS];
     SlotTable slots;
 };
 

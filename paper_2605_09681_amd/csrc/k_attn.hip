@@ -119,33 +119,35 @@ __device__ __forceinline__ void load_tile(const uint16_t *hist, const uint16_t *
     }
 }
 
-// Page table of a head read in place: the cache position of each kept piece,
-// one byte per piece -- piece y's entry sits in byte y >> 6 of lane y & 63, up
-// to 256 pieces in one VGPR, looked up with v_readlane, so the tile loop never
-// waits on a scalar load (whose counter it shares with the LDS reads).  Piece
-// y starts at cache row entry(y) * P of the head (P = the entry's piece
-// length), i.e. entry = slot * (F / P) + unit.
-//   static entry: pieces are frames; kept frame y is logical frame y
-//                 (y < st_first) or y + st_gap, entry = its slot;
-//   dynamic entry: pieces are the min(L, F)-token pieces of the segments in
-//                 kept_seg[h] (ascending, as the selection wrote them); the
-//                 host has checked that every entry fits in a byte.
+// Page table of a head read in place: the cache position of each kept piece
+// (pg_P tokens), one byte per piece -- piece y's entry sits in byte y >> 6 of
+// lane y & 63, up to 256 pieces in one VGPR, looked up with v_readlane, so the
+// tile loop never waits on a scalar load (whose counter it shares with the LDS
+// reads).  Piece y starts at cache row entry(y) * pg_P of the head, entry =
+// slot * pg_ppf + (piece within its frame).
+//   static entry: the pieces of kept frame y / pg_ppf, which is logical frame
+//                 y' (y' < st_first) or y' + st_gap;
+//   dynamic entry: the pieces of the segments in kept_seg[h] (ascending, as
+//                 the selection wrote them).
+// The host has checked that every entry fits in a byte.
 __device__ __forceinline__ uint32_t kept_piece_table(const AttnArgs &a, int li, int kvl, int lane) {
     uint32_t tab = 0;
+    const int ppf = a.pg_ppf;
     const int n = a.st_kept[li];
     if (n >= 0) {
         const int first = a.st_first[li], gap = a.st_gap[li];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const int y = lane + 64 * k;
-            if (y < n) tab |= (uint32_t)a.slots.slot[y < first ? y : y + gap] << (8 * k);
+            if (y < n * ppf) {
+                const int fy = y / ppf, u = y - fy * ppf;
+                tab |= (uint32_t)(a.slots.slot[fy < first ? fy : fy + gap] * ppf + u) << (8 * k);
+            }
         }
         return tab;
     }
-    const int P = a.pg_piece[li];
-    const int ppf = a.F / P;                                  // pieces per frame (1 when L >= F)
     const int m = a.pg_L > a.F ? a.pg_L / a.F : 1;           // pieces per segment
-    const int n_pieces = kvl / P;
+    const int n_pieces = kvl / a.pg_P;
     const int32_t *ks = a.kept_seg + (size_t)a.heads.head[li] * a.pg_nseg;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -176,8 +178,17 @@ __device__ __forceinline__ int kept_piece(uint32_t tab, int y) {
 // With P >= 64 a tile touches at most two kept pieces and the chunk; each part
 // has its own range-checked buffer and the three loads are OR-ed, every row
 // outside a part reading as zero.
+// j0 / P for 0 <= j0 < 2^31 with the launch's 64-bit reciprocal M = floor(2^64 / P) + 1
+// (= magic_hi * 2^32 + magic_lo): floor(j0 * M / 2^64) exactly, since j0 * M / 2^64
+// exceeds j0 / P by less than 2^-33 < 1 / P.  A few scalar multiplies instead of
+// the generic division sequence in every tile load.
+__device__ __forceinline__ int div_piece(const AttnArgs &a, int j0) {
+    const uint64_t p = (uint64_t)(uint32_t)j0 * a.pg_magic_hi + __umulhi((uint32_t)j0, a.pg_magic_lo);
+    return (int)(p >> 32);
+}
+
 template <int D, int N>
-__device__ __forceinline__ void load_tile_paged(const uint16_t *hist, uint32_t tab, int P,
+__device__ __forceinline__ void load_tile_paged(const AttnArgs &a, const uint16_t *hist, uint32_t tab, int P,
                                                 const uint16_t *chunk, int j0, int kvl, int Lk, int Lq,
                                                 u32x4 *dst, uint32_t off0, uint32_t step) {
     if (j0 >= kvl) {
@@ -187,7 +198,7 @@ __device__ __forceinline__ void load_tile_paged(const uint16_t *hist, uint32_t t
         return;
     }
     auto piece = [&](int y) { return hist + (size_t)kept_piece(tab, y) * P * D; };
-    const int y0 = j0 / P, r0 = j0 - y0 * P;
+    const int y0 = div_piece(a, j0), r0 = j0 - y0 * P;
     const int na = min(min(P - r0, kvl - j0), BN);            // rows of kept piece y0
     const auto ra = rsrc(piece(y0) + (size_t)r0 * D, (uint32_t)na * D * 2);
     if (na == BN) {
@@ -206,6 +217,46 @@ __device__ __forceinline__ void load_tile_paged(const uint16_t *hist, uint32_t t
         const uint32_t o = off0 + i * step;
         // rows before a part's start wrap to huge offsets: out of range, read 0
         dst[i] = bload(ra, o) | bload(rb, o - sb) | bload(rc, o - sc);
+    }
+}
+
+// Position of a key tile of a head read in place: its first key j0 and, while
+// j0 is in the history, the kept piece y it starts in and the row r within
+// that piece (j0 = y * P + r).  The tile loop advances it by one tile per
+// iteration with a few scalar adds and no division.
+struct PageCursor {
+    int j0, y, r;
+};
+
+// The tile at `c` (as load_tile_paged).  The history length kvl is a whole
+// number of pieces, so a tile starting in piece y holds min(P - r, BN) rows of
+// it, then the next piece's rows while history lasts, then the chunk's.
+template <int D, int N>
+__device__ __forceinline__ void load_tile_cursor(const uint16_t *hist, uint32_t tab, int P, const PageCursor &c,
+                                                 const uint16_t *chunk, int kvl, int Lk, int Lq, u32x4 *dst,
+                                                 uint32_t off0, uint32_t step) {
+    if (c.j0 >= kvl) {
+        const auto r = rsrc(chunk + (size_t)(c.j0 - kvl) * D, (uint32_t)(Lk - c.j0) * D * 2);
+#pragma unroll
+        for (int i = 0; i < N; ++i) dst[i] = bload(r, off0 + i * step);
+        return;
+    }
+    const int na = min(P - c.r, BN);
+    const auto ra = rsrc(hist + ((size_t)kept_piece(tab, c.y) * P + c.r) * D, (uint32_t)na * D * 2);
+    if (na == BN) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) dst[i] = bload(ra, off0 + i * step);
+        return;
+    }
+    const bool more = c.j0 + na < kvl;  // another kept piece follows, else the chunk
+    const auto rb = rsrc(more ? hist + (size_t)kept_piece(tab, c.y + 1) * P * D : chunk,
+                         (uint32_t)(more ? BN - na : min(BN - na, Lq)) * D * 2);
+    const uint32_t sb = (uint32_t)na * D * 2;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const uint32_t o = off0 + i * step;
+        // rows before the second part's start wrap to huge offsets: out of range, read 0
+        dst[i] = bload(ra, o) | bload(rb, o - sb);
     }
 }
 
@@ -309,7 +360,6 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
     const uint16_t *Kq = (const uint16_t *)a.K_cur + (size_t)h * Lq * D;
     const uint16_t *Vq = (const uint16_t *)a.V_cur + (size_t)h * Lq * D;
     const uint32_t ktab = PAGED ? kept_piece_table(a, li, kvl, lane) : 0u;
-    const int piece_len = PAGED ? a.pg_piece[li] : 0;
 
     // Loop-invariant per-thread load geometry within the thread's group of 256:
     // rows r0 + RPP*i, chunk c (group 0 stages K tiles, group 1 V tiles).
@@ -330,16 +380,37 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
     };
     auto load_k = [&](int j0, u32x4 (&dst)[4]) {
         if (PAGED)
-            load_tile_paged<D, C::NV>(Kc, ktab, piece_len, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
+            load_tile_paged<D, C::NV>(a, Kc, ktab, a.pg_P, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
         else
             load_tile<D, C::NV>(Kc, Kq, j0, kvl, Lk, Lq, dst, voff, C::RPP * D * 2);
     };
     auto load_v = [&](int j0, u32x4 (&dst)[4]) {
         if (gtid < C::VUNITS) {
             if (PAGED)
-                load_tile_paged<D, 4>(Vc, ktab, piece_len, Vq, j0, kvl, Lk, Lq, dst, voffv, D * 2);
+                load_tile_paged<D, 4>(a, Vc, ktab, a.pg_P, Vq, j0, kvl, Lk, Lq, dst, voffv, D * 2);
             else
                 load_tile<D, 4>(Vc, Vq, j0, kvl, Lk, Lq, dst, voffv, D * 2);
+        }
+    };
+    // In the tile loop each group loads tiles of consecutive positions (group 0
+    // V(it + 1), group 1 K(it + 3)); read in place, it follows them with a
+    // cursor instead of dividing every tile's first key by the piece length.
+    const int P = PAGED ? a.pg_P : 0;
+    auto cursor_at = [&](int j) {
+        const int j0 = tile0(j);
+        const int y = j0 < kvl ? div_piece(a, j0) : 0;
+        return PageCursor{j0, y, j0 - y * P};
+    };
+    auto advance = [&](PageCursor &cu) {
+        cu.j0 += BN;
+        if (cu.j0 >= T * BN) {          // the rotated order wraps to the first tile
+            cu = PageCursor{0, 0, 0};
+        } else {
+            cu.r += BN;
+            if (cu.r >= P) {
+                cu.r -= P;
+                ++cu.y;
+            }
         }
     };
     auto store_k = [&](uint16_t *tile, const u32x4 (&src)[4]) {
@@ -486,15 +557,36 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
     // Let every outstanding load (the Q fragments included) land once here, so
     // the loop's score products carry no wait on the staging loads in flight.
     __builtin_amdgcn_s_waitcnt(0);
+    // paged: group 0's next V tile is position 2, group 1's next K tile
+    // position 3; both cursors are kept (uniform, scalar) and advanced together
+    PageCursor cur_v = PAGED && n > 2 ? cursor_at(2) : PageCursor{0, 0, 0};
+    PageCursor cur_k = PAGED && n > 3 ? cursor_at(3) : PageCursor{0, 0, 0};
     for (int it = 0; it < n; ++it) {
         const int j0 = tile0(it);
         softmax(j0);
         if (grp == 0) {
             if (it >= 1) store_vt(Vs[it & 1], stage);
-            if (it >= 1 && it + 1 < n) load_v(tile0(it + 1), stage);
+            if (it >= 1 && it + 1 < n) {
+                if constexpr (PAGED) {
+                    if (gtid < C::VUNITS)
+                        load_tile_cursor<D, 4>(Vc, ktab, P, cur_v, Vq, kvl, Lk, Lq, stage, voffv, D * 2);
+                } else {
+                    load_v(tile0(it + 1), stage);
+                }
+            }
         } else {
             if (it + 2 < n) store_k(Ks[it & 1], stage);
-            if (it + 3 < n) load_k(tile0(it + 3), stage);
+            if (it + 3 < n) {
+                if constexpr (PAGED) {
+                    load_tile_cursor<D, C::NV>(Kc, ktab, P, cur_k, Kq, kvl, Lk, Lq, stage, voff, C::RPP * D * 2);
+                } else {
+                    load_k(tile0(it + 3), stage);
+                }
+            }
+        }
+        if constexpr (PAGED) {
+            if (it >= 1) advance(cur_v);
+            advance(cur_k);
         }
         __syncthreads();
         // (no wave-priority raise around the block: measured 1% slower with it)

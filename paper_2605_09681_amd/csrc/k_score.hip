@@ -17,7 +17,7 @@
 // Streaming.  Workgroup (cg, u, li) owns column group cg -- 2 x 64 adjacent
 // 16-byte vectors -- of unit u of listed head li, and streams those columns of
 // every frame once: its four waves split the frames into four contiguous
-// runs, every lane loads up to four frames of its run at once (bf16),
+// runs, every lane loads up to six frames of its run at once,
 // so no key byte is read twice and every load is a full 1 KB-per-wave
 // coalesced access.  A lane accumulates, per frame, its columns' squares and
 // products with the previous frame (vector 0 then vector 1, elements in
@@ -26,11 +26,12 @@
 // across a run boundary uses the next run's first frame, which its wave
 // leaves in LDS.
 //
-// Finish.  After its partial stores each workgroup bumps its head's arrival
-// counter (agent-scope release / acquire); the last workgroup of the head
-// reduces the head's partials -- per (unit, frame, quantity), four sequential
-// sums over fixed quarters of the column groups, then (p0 + p1) + (p2 + p3) --
-// and then, by mode:
+// Finish.  Each workgroup stores its per-frame sums as one block and arrives
+// on one of its head's kGroups first-level counters (device-scope stores,
+// loads and counters; see put_shared).  The last arrival of a group sums its
+// members' blocks (in increasing order) into the group's sums and arrives on
+// the head's counter; the last of those sums the kGroups group sums in order
+// -- a fixed tree for every (unit, frame, quantity) -- and then, by mode:
 //   full:    the head's scores (and, with `select`, its BottomK selection);
 //   history: per-frame statistics SQ(t), DOT(t) into `stats`, kept across the
 //            AR steps of a chunk (the history does not change, only K_cur);
@@ -54,10 +55,18 @@ constexpr int kThreads = kScoreThreads;  // 4 waves
 constexpr int kWaves = kScoreWaves;
 constexpr int kV = 2;                    // 16-byte vectors per lane and frame
 constexpr int kCols = 64 * kV;           // vectors (columns) per workgroup
-// Frames a lane loads at once: four bf16 frames keep the kernel within 96
-// VGPRs (five waves per SIMD, every workgroup of a 480P layer resident).
-template <bool F32> constexpr int kMaxF = F32 ? 6 : 4;
-constexpr int kRowBatch = kThreads / 4;  // partial rows reduced per pass of the finisher
+// Frames a lane loads at once: the whole run of a 22-frame (480P) pass,
+// within 96 VGPRs (five waves per SIMD, every workgroup of a 480P layer
+// resident at once).
+template <bool F32> constexpr int kMaxF = 4;
+// Arrival counters: device-scope atomics on one address serialise at the
+// memory side, so each counter has a 256-byte line of its own and a head's
+// workgroups arrive in two levels -- kGroups first-level counters (workgroup
+// w on counter w % kGroups), whose last arrivals then meet on the head's
+// counter.  Per listed head: kGroups + 1 counters; one more for pooling.
+constexpr int kGroups = 16;
+constexpr int kCounterStride = 64;       // uint32 per counter (256 bytes)
+constexpr int kCountersPerHead = kGroups + 1;
 
 // One DPP step on a double (both 32-bit halves moved with the same control);
 // lanes without a source, or outside row_mask, contribute 0.
@@ -82,44 +91,36 @@ __device__ __forceinline__ double wave_sum(double v) {
     return v;  // valid in lane 63
 }
 
-// Widen a 16-byte vector to fp64 elements (exact).
+// Element e of a 16-byte vector widened to fp64 (exact): 8 bf16 or 4 fp32.
 template <bool F32>
 struct Vec;
 
 template <>
 struct Vec<false> {  // 8 bf16
     static constexpr int N = 8;
-    __device__ static __forceinline__ void widen(const u32x4 &v, double *x) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            x[2 * i] = (double)__uint_as_float(v[i] << 16);
-            x[2 * i + 1] = (double)__uint_as_float(v[i] & 0xffff0000u);
-        }
+    __device__ static __forceinline__ double at(const u32x4 &v, int e) {
+        const uint32_t w = v[e >> 1];
+        return (double)__uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
     }
 };
 
 template <>
 struct Vec<true> {  // 4 fp32
     static constexpr int N = 4;
-    __device__ static __forceinline__ void widen(const u32x4 &v, double *x) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) x[i] = (double)__uint_as_float(v[i]);
-    }
+    __device__ static __forceinline__ double at(const u32x4 &v, int e) { return (double)__uint_as_float(v[e]); }
 };
 
-// sum over the lane's columns of a*b, vector 0 then vector 1, elements in order
+// Sum over the lane's columns of a*b, vector 0 then vector 1, elements in
+// order; each element is widened where it is used, so only the loaded 16-byte
+// vectors occupy registers (six frames of them in flight).
 template <bool F32>
 __device__ __forceinline__ double lane_dot(const u32x4 (&a)[kV], const u32x4 (&b)[kV]) {
     using V = Vec<F32>;
     double acc = 0.0;
 #pragma unroll
-    for (int j = 0; j < kV; ++j) {
-        double x[V::N], y[V::N];
-        V::widen(a[j], x);
-        V::widen(b[j], y);
+    for (int j = 0; j < kV; ++j)
 #pragma unroll
-        for (int e = 0; e < V::N; ++e) acc = fma(x[e], y[e], acc);
-    }
+        for (int e = 0; e < V::N; ++e) acc = fma(V::at(a[j], e), V::at(b[j], e), acc);
     return acc;
 }
 
@@ -128,13 +129,26 @@ __device__ __forceinline__ double lane_sq(const u32x4 (&a)[kV]) {
     using V = Vec<F32>;
     double acc = 0.0;
 #pragma unroll
-    for (int j = 0; j < kV; ++j) {
-        double x[V::N];
-        V::widen(a[j], x);
+    for (int j = 0; j < kV; ++j)
 #pragma unroll
-        for (int e = 0; e < V::N; ++e) acc = fma(x[e], x[e], acc);
-    }
+        for (int e = 0; e < V::N; ++e) {
+            const double x = V::at(a[j], e);
+            acc = fma(x, x, acc);
+        }
     return acc;
+}
+
+// Values other workgroups read within this launch (partials, per-head sums)
+// are written and read with device-scope accesses (sc1: coherent across the
+// XCDs' L2 caches for that location), so the hand-over needs no cache
+// write-back or invalidation: a generic agent-scope release fence writes back
+// the whole L2 of the XCD (measured ~1 us, serialised per XCD, when every
+// workgroup does it).
+__device__ __forceinline__ void put_shared(double *p, double v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double get_shared(const double *p) {
+    return __hip_atomic_load(const_cast<double *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Partial row of (unit u, streamed frame f, quantity q: 0 = SQ, 1 = DOT).
@@ -145,17 +159,19 @@ __device__ __forceinline__ int row_of(const ScoreArgs &a, int u, int f, int q) {
 // Per-(unit, frame) sums of one head as the scores read them, with the frame
 // given as a logical frame t: T holds this pass's rows (streamed frames
 // [t_begin, t_begin + n_frames)), stats the history statistics (cached mode).
+template <bool SHARED>
 struct Terms {
     const ScoreArgs &a;
-    const double *T;      // rows of this head
+    const double *T;      // rows of this head (LDS, or per-head sums written by other workgroups)
     const double *stats;  // [H][units][2] of this head (cached mode)
+    __device__ __forceinline__ double row(int r) const { return SHARED ? get_shared(T + r) : T[r]; }
     __device__ __forceinline__ double sq(int t, int u) const {
         if (a.mode == kScoreModeCached && t < a.H) return stats[((int64_t)t * a.units + u) * 2];
-        return T[row_of(a, u, t - a.t_begin, 0)];
+        return row(row_of(a, u, t - a.t_begin, 0));
     }
     __device__ __forceinline__ double dot(int t, int u) const {
         if (a.mode == kScoreModeCached && t < a.H - 1) return stats[((int64_t)t * a.units + u) * 2 + 1];
-        return T[row_of(a, u, t - a.t_begin, 1)];
+        return row(row_of(a, u, t - a.t_begin, 1));
     }
 };
 
@@ -178,30 +194,56 @@ __device__ __forceinline__ float cosine(double dot, double na, double nb) {
     return (float)(prod == 0.0 ? 0.0 : dot / sqrt(prod));
 }
 
-// The last workgroup of listed head li: reduce the head's partials into T
-// (LDS, lds_rows doubles) and finish by mode.
+// The last workgroup to arrive of arrival group g of listed head li: for every
+// row (u, f, q) the sum of the group's members' partials -- members are the
+// workgroups wi = u * n_cg + cg with wi % kGroups == g, in increasing cg --
+// into the group sums G[li][g][row] (0 where the group has no member in the
+// row's unit).  Loads go out eight at a time.
+__device__ void group_sum(const ScoreArgs &a, int li, int g) {
+    const int blk = a.n_frames * 2, n_rows = a.units * blk;
+    const double *part = a.part + (int64_t)li * n_rows * a.n_cg;   // [u][cg][f][q]
+    double *G = a.group + ((int64_t)li * kGroups + g) * n_rows;
+    for (int r = threadIdx.x; r < n_rows; r += kThreads) {
+        const int u = r / blk, rp = r - u * blk;
+        const double *p = part + (int64_t)u * a.n_cg * blk + rp;
+        double acc = 0.0;
+        for (int c = (g - (u * a.n_cg) % kGroups + kGroups) % kGroups; c < a.n_cg; c += 8 * kGroups) {
+            double v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int cc = c + i * kGroups;
+                v[i] = cc < a.n_cg ? get_shared(p + (int64_t)cc * blk) : 0.0;
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc += v[i];
+        }
+        put_shared(G + r, acc);
+    }
+}
+
+// The last workgroup of listed head li: the head's per-row sums T (LDS,
+// lds_rows doubles) from the group sums, groups in order, then the finish by
+// mode.
 __device__ void finish_head(const ScoreArgs &a, int li, double *T, float *s_scores, unsigned char *s_forced,
                             unsigned char *s_keep) {
-    __shared__ double red[4][kRowBatch];
     const int tid = threadIdx.x;
     const int h = a.heads.head[li];
     const int n_rows = a.units * a.n_frames * 2;
-    const double *part = a.part + (int64_t)li * n_rows * a.n_cg;
-    // fixed quarters of the column groups: [q*n_cg/4, (q+1)*n_cg/4)
-    const int rr = tid % kRowBatch, qq = tid / kRowBatch;
-    const int c_lo = qq * a.n_cg / 4, c_hi = (qq + 1) * a.n_cg / 4;
-    for (int r0 = 0; r0 < n_rows; r0 += kRowBatch) {
-        const int r = r0 + rr;
+    const double *G = a.group + (int64_t)li * kGroups * n_rows;
+    // groups 0 .. min(n_wg, kGroups) - 1 have members and wrote every row; the
+    // others were not written by this call
+    const int n_groups = min(a.units * a.n_cg, kGroups);
+    for (int r = tid; r < n_rows; r += kThreads) {
+        double v[kGroups];
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) v[g] = g < n_groups ? get_shared(G + (int64_t)g * n_rows + r) : 0.0;
         double acc = 0.0;
-        if (r < n_rows) {
-            const double *p = part + (int64_t)r * a.n_cg;
-            for (int c = c_lo; c < c_hi; ++c) acc += p[c];
-        }
-        red[qq][rr] = acc;
-        __syncthreads();
-        if (tid < kRowBatch && r0 + tid < n_rows) T[r0 + tid] = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
-        __syncthreads();
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g)
+            if (g < n_groups) acc += v[g];
+        T[r] = acc;
     }
+    __syncthreads();
 
     if (a.mode == kScoreModeHistory) {
         // SQ(t) for t < H, DOT(t) for t < H - 1 (t_begin = 0)
@@ -215,10 +257,10 @@ __device__ void finish_head(const ScoreArgs &a, int li, double *T, float *s_scor
     }
     if (a.pooled) {
         double *tot = a.totals + (int64_t)li * n_rows;
-        for (int r = tid; r < n_rows; r += kThreads) tot[r] = T[r];
+        for (int r = tid; r < n_rows; r += kThreads) put_shared(tot + r, T[r]);
         return;  // the caller counts finished heads; the last one scores
     }
-    const Terms tm{a, T, a.stats + (int64_t)li * a.H * a.units * 2};
+    const Terms<false> tm{a, T, a.stats + (int64_t)li * a.H * a.units * 2};
     for (int g = tid; g < a.n_seg; g += kThreads) {
         int u, t0, t1;
         seg_span(a, g, &u, &t0, &t1);
@@ -247,7 +289,7 @@ __device__ void finish_pooled(const ScoreArgs &a) {
         seg_span(a, g, &u, &t0, &t1);
         double dot = 0.0, na = 0.0, nb = 0.0;
         for (int li = 0; li < a.heads.n; ++li) {
-            const Terms tm{a, a.totals + (int64_t)li * n_rows, a.stats + (int64_t)li * a.H * a.units * 2};
+            const Terms<true> tm{a, a.totals + (int64_t)li * n_rows, a.stats + (int64_t)li * a.H * a.units * 2};
             for (int t = t0; t < t1; ++t) {
                 dot += tm.dot(t, u);
                 na += tm.sq(t, u);
@@ -258,10 +300,13 @@ __device__ void finish_pooled(const ScoreArgs &a) {
     }
 }
 
-// Agent-scope arrival on a counter; true in every thread of the workgroup
+// Arrival on a device-scope counter; true in every thread of the workgroup
 // that arrives last (the counter is then reset to zero for the next call).
+// Every wave first waits until its device-scope stores have completed, so the
+// last arrival sees all of them (and, through a chain of arrivals, everything
+// the earlier arrivals saw).
 __device__ __forceinline__ bool arrive_last(uint32_t *counter, uint32_t expected, uint32_t *flag) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // this wave's stores before the arrival
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's stores (vmcnt), LDS and scalar accesses complete
     __syncthreads();
     if (threadIdx.x == 0) {
         const uint32_t old = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -270,14 +315,13 @@ __device__ __forceinline__ bool arrive_last(uint32_t *counter, uint32_t expected
         *flag = last ? 1u : 0u;
     }
     __syncthreads();
-    const bool last = *flag != 0;
-    if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    return last;
+    return *flag != 0;
 }
 
 template <bool F32>
 __global__ __launch_bounds__(kThreads, 5) void score_kernel(ScoreArgs a) {
-    extern __shared__ double dyn[];            // finisher: lds_rows doubles, then n_seg floats + 2 n_seg bytes
+    extern __shared__ double dyn[];            // finisher rows (lds_rows), this workgroup's sums (2 n_frames),
+                                               // then n_seg floats + 2 n_seg bytes
     __shared__ u32x4 edge[kWaves][kV][64];     // first frame of each wave's run
     __shared__ uint32_t flag;
 
@@ -304,9 +348,10 @@ __global__ __launch_bounds__(kThreads, 5) void score_kernel(ScoreArgs a) {
 #pragma unroll
         for (int j = 0; j < kV; ++j) x[j] = ok[j] ? __builtin_nontemporal_load(base + col[j]) : u32x4{0, 0, 0, 0};
     };
-    double *part = a.part + (int64_t)li * (a.units * nf * 2) * a.n_cg + cg;
+    // per-frame sums of this workgroup, staged in LDS and stored as one block
+    double *wg_part = dyn + a.lds_rows;       // 2 * nf doubles after the finisher's rows
     auto put = [&](int f, int q, double v) {
-        if (lane == 63) part[(int64_t)row_of(a, u, f, q) * a.n_cg] = v;
+        if (lane == 63) wg_part[f * 2 + q] = v;
     };
 
     u32x4 prev[kV] = {};
@@ -341,13 +386,24 @@ __global__ __launch_bounds__(kThreads, 5) void score_kernel(ScoreArgs a) {
         put(fb - 1, 1, wave_sum(lane_dot<F32>(prev, nx)));
     }
 
-    if (!arrive_last(a.counters + li, (uint32_t)(a.units * a.n_cg), &flag)) return;
+    __syncthreads();
+    {
+        double *blk = a.part + (((int64_t)li * a.units + u) * a.n_cg + cg) * (nf * 2);
+        for (int r = tid; r < nf * 2; r += kThreads) put_shared(blk + r, wg_part[r]);
+    }
+    // two-level arrival of the head's workgroups
+    const int n_wg = a.units * a.n_cg, wi = u * a.n_cg + cg, g1 = wi % kGroups;
+    uint32_t *cnt = a.counters + (int64_t)li * kCountersPerHead * kCounterStride;
+    if (!arrive_last(cnt + g1 * kCounterStride, (uint32_t)((n_wg - g1 + kGroups - 1) / kGroups), &flag)) return;
+    group_sum(a, li, g1);
+    if (!arrive_last(cnt + kGroups * kCounterStride, (uint32_t)min(n_wg, kGroups), &flag)) return;
     double *T = dyn;
-    float *s_scores = (float *)(dyn + a.lds_rows);
+    float *s_scores = (float *)(dyn + a.lds_rows + nf * 2);
     unsigned char *s_forced = (unsigned char *)(s_scores + a.n_seg);
     finish_head(a, li, T, s_scores, s_forced, s_forced + a.n_seg);
     if (a.pooled && a.mode != kScoreModeHistory) {
-        if (!arrive_last(a.counters + a.heads.n, (uint32_t)a.heads.n, &flag)) return;
+        uint32_t *pc = a.counters + (int64_t)a.heads.n * kCountersPerHead * kCounterStride;
+        if (!arrive_last(pc, (uint32_t)a.heads.n, &flag)) return;
         finish_pooled(a);
     }
 }
@@ -359,25 +415,26 @@ int score_column_groups(int64_t unit_vecs) { return (int)((unit_vecs + kCols - 1
 size_t score_workspace_bytes(int n_list, int H, int units, int n_cg) {
     if (n_list == 0 || H == 0) return 0;
     const size_t rows = (size_t)units * (H + 1) * 2;  // the full pass streams H + 1 frames
-    const size_t counters = ((size_t)(n_list + 1) * sizeof(uint32_t) + 255) & ~(size_t)255;
-    const size_t b = counters + ((size_t)n_list * rows * n_cg + (size_t)n_list * rows) * sizeof(double);
+    const size_t counters = ((size_t)n_list * kCountersPerHead + 1) * kCounterStride * sizeof(uint32_t);
+    const size_t b = counters + ((size_t)n_list * rows * n_cg + (size_t)n_list * rows * (kGroups + 1)) * sizeof(double);
     return (b + 255) & ~(size_t)255;
 }
 
 // The workspace of score_workspace_bytes split into counters, partials, sums.
 void score_workspace_layout(ScoreArgs &a, void *ws, int n_list, int H, int units, int n_cg) {
     const size_t rows = (size_t)units * (H + 1) * 2;
-    const size_t counters = ((size_t)(n_list + 1) * sizeof(uint32_t) + 255) & ~(size_t)255;
+    const size_t counters = ((size_t)n_list * kCountersPerHead + 1) * kCounterStride * sizeof(uint32_t);
     a.counters = (uint32_t *)ws;
     a.part = (double *)((char *)ws + counters);
     a.totals = a.part + (size_t)n_list * rows * n_cg;
+    a.group = a.totals + (size_t)n_list * rows;
 }
 
 hipError_t launch_score(const ScoreArgs &a0, bool f32, hipStream_t s) {
     ScoreArgs a = a0;
     if (a.heads.n == 0 || a.n_frames <= 0) return hipSuccess;
     a.lds_rows = a.units * a.n_frames * 2;
-    size_t lds = (size_t)a.lds_rows * sizeof(double);
+    size_t lds = (size_t)(a.lds_rows + a.n_frames * 2) * sizeof(double);   // + this workgroup's sums
     if (a.select) lds += (size_t)a.n_seg * (sizeof(float) + 2);
     lds = (lds + 15) & ~(size_t)15;
     const dim3 grid((unsigned)a.n_cg, (unsigned)a.units, (unsigned)a.heads.n);
