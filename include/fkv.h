@@ -252,6 +252,11 @@ fkv_status fkv_select_compact_pooled(const fkv_shape *shape, const fkv_head *hea
 fkv_status fkv_select(const fkv_shape *shape, const fkv_head *heads, const float *scores,
                       int32_t shared_row, int32_t *kept_seg, int32_t *kv_len, void *stream);
 
+/* Bytes of device scratch the library holds per GPU for
+ * fkv_score_select_noalloc (8 MiB: a 480P layer's 6 dynamic heads need
+ * 0.4 MiB, a 1080P layer's 2.2 MiB). */
+#define FKV_NOALLOC_SCRATCH_BYTES (8u << 20)
+
 /* fkv_score_segments followed by fkv_select in ONE kernel launch: the
  * workgroup that completes a dynamic head's scores also selects its kept
  * segments.  scores, kept_seg and kv_len are written exactly as the two calls
@@ -341,6 +346,23 @@ fkv_status fkv_chunk_attention_static(const fkv_shape *shape, const fkv_head *he
                                       const void *K_cur, const void *V_cur, float scale,
                                       void *O, float *lse, void *workspace,
                                       size_t workspace_bytes, void *stream);
+
+/* fkv_score_select for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same scores, kept_seg and kv_len, but the scoring workspace
+ * is the library's own device array of FKV_NOALLOC_SCRATCH_BYTES on the
+ * current device (no workspace argument; the call allocates nothing --
+ * no hipMalloc, hipFree or allocating library routine).  Every call on a GPU
+ * shares that GPU's array: calls that may overlap on one GPU (other streams,
+ * other host threads) race and must be ordered by the caller; each call
+ * leaves the array's counters at zero for the next one.  FKV_ERR_CAPACITY
+ * when the shape's scoring workspace (fkv_score_workspace_size) exceeds the
+ * array; FKV_ERR_DEVICE if the array's address cannot be obtained.  Other
+ * arguments and errors as in fkv_score_select. */
+fkv_status fkv_score_select_noalloc(const fkv_shape *shape, const fkv_head *heads,
+                                    const void *K_hist, const int32_t *frame_slot,
+                                    const void *K_cur, float *scores, int32_t *kept_seg,
+                                    int32_t *kv_len, void *stream);
 
 /* Chunk attention with every listed head's kept history read in place from
  * the cache (Eq. 2 for static heads, Eq. 4 for dynamic heads), without a

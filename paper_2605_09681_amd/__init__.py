@@ -45,7 +45,7 @@ FKV_MAX_HEADS, FKV_MAX_FRAMES, FKV_MAX_SEGMENTS = 64, 256, 4096
 EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_score_workspace_size", "fkv_score_segments", "fkv_select_compact",
             "fkv_append_frames", "fkv_score_pooled_workspace_size", "fkv_score_pooled",
-            "fkv_select_compact_pooled", "fkv_select", "fkv_score_select",
+            "fkv_select_compact_pooled", "fkv_select", "fkv_score_select", "fkv_score_select_noalloc",
             "fkv_score_stats_size", "fkv_score_history",
             "fkv_score_segments_cached",
             "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_chunk_attention_heads",
@@ -116,6 +116,8 @@ def lib():
         L.fkv_select.restype = ctypes.c_int
         L.fkv_score_select.argtypes = [S, Hd, P, P, P, P, P, P, P, SZ, P]
         L.fkv_score_select.restype = ctypes.c_int
+        L.fkv_score_select_noalloc.argtypes = [S, Hd, P, P, P, P, P, P, P]
+        L.fkv_score_select_noalloc.restype = ctypes.c_int
         L.fkv_attention_workspace_size.argtypes = [S, ctypes.POINTER(SZ)]
         L.fkv_attention_workspace_size.restype = ctypes.c_int
         L.fkv_chunk_attention.argtypes = [S, P, P, P, I32, P, P, P, F, P, P, P, SZ, P]
@@ -404,6 +406,23 @@ def fkv_score_select(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, scores,
     _raise(lib().fkv_score_select(ctypes.byref(shape), _heads(shape, heads), kh, sl, kc, sc, ks, kl, ws,
                                   workspace.numel(), _stream(stream)))
     return workspace
+
+
+def fkv_score_select_noalloc(shape: fkv_shape, heads, K_hist, frame_slot, K_cur, scores, kept_seg, kv_len,
+                             stream=None):
+    """fkv_score_select with the library's own per-GPU scratch as workspace:
+    nothing is allocated.  Calls that overlap on one GPU race."""
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    n_seg = fkv_num_segments(shape)
+    kh = _check(K_hist, "K_hist", dt, hist)
+    sl = _slots(frame_slot, shape.hist_frames)
+    kc = _check(K_cur, "K_cur", dt, (shape.n_heads, _lq(shape), shape.head_dim))
+    sc = _check(scores, "scores", torch.float32, (shape.n_heads, n_seg))
+    ks = _check(kept_seg, "kept_seg", torch.int32, (shape.n_heads, n_seg))
+    kl = _check(kv_len, "kv_len", torch.int32, (shape.n_heads,))
+    _raise(lib().fkv_score_select_noalloc(ctypes.byref(shape), _heads(shape, heads), kh, sl, kc, sc, ks, kl,
+                                          _stream(stream)))
 
 
 def fkv_select_compact(shape: fkv_shape, heads, scores, K_hist, V_hist, frame_slot, kept_seg,

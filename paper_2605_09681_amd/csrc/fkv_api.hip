@@ -9,6 +9,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "fkv_internal.h"
@@ -556,6 +557,70 @@ fkv_status fkv_score_select(const fkv_shape *shape, const fkv_head *heads, const
     const SelectOut out{heads, kept_seg, kv_len};
     return score_impl(shape, list, false, K_hist, frame_slot, K_cur, scores, workspace, stream,
                       "fkv_score_select launch", fkv::kScoreModeFull, nullptr, &out);
+}
+
+}  // extern "C"
+
+// ------------------------------------------------- scoring that allocates nothing
+// fkv_score_select_noalloc's workspace: a device array of the library (one
+// copy per GPU, held until the process ends), zero at load like every scoring
+// workspace, and left with its arrival counters at zero by every call.
+static constexpr size_t kNoallocScratchBytes = (size_t)FKV_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kNoallocScratchBytes];
+
+namespace {
+
+// The array's device address on the current device.  In host code `scratch`
+// is only a stand-in symbol, never a device address: the address comes from
+// hipGetSymbolAddress, once per device with that device current.
+fkv_status scratch_address(void **out) {
+    static std::mutex mu;
+    static void *addr[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(FKV_ERR_DEVICE, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= 64) return fail(FKV_ERR_DEVICE, "device %d outside [0, 64)", dev);
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(FKV_ERR_DEVICE, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return FKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+fkv_status fkv_score_select_noalloc(const fkv_shape *shape, const fkv_head *heads, const void *K_hist,
+                                    const int32_t *frame_slot, const void *K_cur, float *scores,
+                                    int32_t *kept_seg, int32_t *kv_len, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+    if (!kv_len) return fail(FKV_ERR_ARG, "kv_len is NULL");
+    size_t need = 0;
+    if ((st = fkv_score_workspace_size(shape, heads, &need)) != FKV_OK) return st;
+    if (need > kNoallocScratchBytes)
+        return fail(FKV_ERR_CAPACITY, "scoring needs %zu bytes of scratch, the library holds %zu", need,
+                    kNoallocScratchBytes);
+    if (need == 0)  // no dynamic head, or nothing cached: every dynamic head keeps nothing
+        return select_impl(shape, heads, nullptr, false, kept_seg, kv_len, stream, "fkv_score_select_noalloc launch");
+    if (!K_hist || !K_cur || !scores || !kept_seg) return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    void *ws = nullptr;
+    if ((st = scratch_address(&ws)) != FKV_OK) return st;
+    fkv::HeadList list;
+    memset(&list, 0, sizeof list);
+    for (int h = 0; h < shape->n_heads; ++h)
+        if (heads[h].type == FKV_DYNAMIC) list.head[list.n++] = h;
+    const SelectOut out{heads, kept_seg, kv_len};
+    return score_impl(shape, list, false, K_hist, frame_slot, K_cur, scores, ws, stream,
+                      "fkv_score_select_noalloc launch", fkv::kScoreModeFull, nullptr, &out);
 }
 
 }  // extern "C"

@@ -420,3 +420,22 @@ def test_select_entry_points_arg_errors(fkv):
     assert call(ws=None) == 1
     assert call(kept=None) == 1
     assert call(slots=(ctypes.c_int32 * 4)(0, 1, 2, 4)) == 1
+
+
+def test_noalloc_scoring_capacity_and_args(fkv):
+    """fkv_score_select_noalloc refuses, before any device work, a shape whose
+    scoring workspace exceeds the library's scratch, and bad arguments."""
+    L = fkv.lib()
+    n = 40   # 1080P-sized frames, 40 dynamic heads: far beyond FKV_NOALLOC_SCRATCH_BYTES
+    shape = _shape(fkv, n_heads=n, frame_tokens=8160, seg_tokens=8160, hist_frames=21, cap_frames=21)
+    heads = fkv.make_heads([W.HeadBudget(W.DYNAMIC, 1, 0, 10, W.SCOPE_GLOBAL)] * n)
+    assert fkv.fkv_score_workspace_size(shape, heads) > 8 << 20
+    sl = (ctypes.c_int32 * 21)(*range(21))
+    assert L.fkv_score_select_noalloc(ctypes.byref(shape), heads, FAKE, sl, FAKE, FAKE, FAKE, FAKE, None) == 3
+    assert "scratch" in fkv.fkv_last_error()
+    small = _shape(fkv)
+    sl4 = (ctypes.c_int32 * 4)(0, 1, 2, 3)
+    assert L.fkv_score_select_noalloc(ctypes.byref(small), _heads(fkv), FAKE, sl4, FAKE, FAKE, FAKE, None, None) == 1
+    assert L.fkv_score_select_noalloc(ctypes.byref(small), _heads(fkv), FAKE, sl4, FAKE, FAKE, None, FAKE, None) == 1
+    bad = (ctypes.c_int32 * 4)(0, 1, 2, 9)
+    assert L.fkv_score_select_noalloc(ctypes.byref(small), _heads(fkv), FAKE, bad, FAKE, FAKE, FAKE, FAKE, None) == 1
