@@ -1,24 +1,26 @@
 """Benchmark of the Forcing-KV hot path on one MI355X.
 
 One step = one AR step of one attention layer (a "unit"): segment scoring and
-BottomK selection + compaction for the dynamic heads, the static heads'
-structural pruning, then chunk attention of all heads over their compressed
-caches -- the C-ABI calls, on the 480P Wan-1.3B-style layer (12 heads,
-d = 128, 1560 tokens/frame, 21-frame history, 3-frame chunk, heads 0-5 static
-with sink + 6 recent frames, heads 6-11 dynamic with sink + 10 of 20 frames).
+BottomK selection for the dynamic heads, the static heads' structural pruning,
+then chunk attention of all heads over their retained history -- the C-ABI
+calls, on the 480P Wan-1.3B-style layer (12 heads, d = 128, 1560
+tokens/frame, 21-frame history, 3-frame chunk, heads 0-5 static with sink + 6
+recent frames, heads 6-11 dynamic with sink + 10 of 20 frames).
 
 Inputs are seeded synthetic tensors already resident in HBM.  The step
 rotates through several independent copies of the layer's buffers (as the
 layers of a real rollout would), so a step never finds its cache in the
 256 MB last-level cache from the previous step.
 
-Prints ONE JSON line.  `value` is the wall-clock ms per step (one layer, one
-AR step) over the timed steps, lower is better.  The timed step is the layer
-driver's step (CompressedLayer.step): the static heads' attention -- read in
-place from the cache, no gather -- on a side stream while the dynamic heads
-are scored, compacted and attended on the main stream.  Before the timed
-steps a serial pass of the four calls with HIP events between them gives the
-per-stage breakdown (and brings the clock up).  During the timed steps HIP
+Prints ONE JSON line on stdout (progress lines go to stderr).  `value` is
+the wall-clock ms per step (one layer, one AR step) over the timed steps,
+lower is better.  The timed step is the layer driver's default step
+(CompressedLayer.step, "paged"): one launch scores the dynamic heads'
+segments and selects the kept ones, then one attention launch covers all 12
+heads, every retained history read in place from the cache (no compaction,
+no gather).  Before the timed steps a serial pass of the compacting path's
+four calls with HIP events between them gives the per-stage breakdown (and
+brings the clock up).  During the timed steps HIP
 events on each launch's own stream time every attention launch the step
 makes; `roofline` reports the longest of them (MFMA-bound), `roofline_launches`
 all of them.  `cpu_baseline` times the CPU oracle on the host cores on a
@@ -41,6 +43,12 @@ METRIC = "ms per AR chunk (score+compact+attn) and attn TFLOP/s, 480P/1080P shap
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_FP8_TFLOPS = 5000.0      # MI355X dense FP8 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+EXTRAS = ("parts", "fp8", "scoring", "uncompressed", "sweep", "1080p")
+
+
+def log(msg):
+    """A progress line on stderr (stdout carries only the JSON line)."""
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
 def parse():
@@ -67,6 +75,8 @@ def parse():
                    help="skip the measured 30-layer x 4-step rollouts (10 and 60 chunks)")
     p.add_argument("--no-extras", action="store_true",
                    help="skip the extra measurements (1080P, sweep, FP8, proxy, uncompressed attention)")
+    p.add_argument("--extras", default="all",
+                   help="comma-separated subset of the extra measurements: " + ",".join(EXTRAS) + " (or all)")
     p.add_argument("--schedule", default="balanced", choices=["balanced", "per-item"],
                    help="attention work schedule (balanced needs the attention workspace)")
     p.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "attention_traffic.json"),
@@ -407,6 +417,11 @@ def main():
 
     fkv.lib()  # fail loudly if the HIP library is missing
     torch.cuda.set_device(0)
+    extras_on = set() if args.no_extras else (set(EXTRAS) if args.extras == "all" else set(args.extras.split(",")))
+    unknown = extras_on - set(EXTRAS)
+    if unknown:
+        sys.exit(f"unknown --extras {sorted(unknown)}; choose from {','.join(EXTRAS)}")
+    log(f"{args.resolution} layer: inputs and {args.copies} buffer copies")
     cfg = W.wan_layer_config(args.resolution)
     x = None
     if args.resolution == "480p":
@@ -424,11 +439,15 @@ def main():
     stream = torch.cuda.current_stream()
 
     # per-stage breakdown first: it also brings the clock up before the timed steps
-    stage = staged_breakdown(layers, bufs, slots, max(args.steps, 50), stream)
+    log("per-stage breakdown (serial compacting path)")
+    # (at least 200 serial units, ~0.1 s at 480P: the clock takes some tens of ms of MFMA
+    # load to settle, and the timed steps follow right after)
+    stage = staged_breakdown(layers, bufs, slots, max(args.steps, 200), stream)
     breakdown = stage_report(cfg, layers[0], stage)
 
     traffic = load_traffic(args.traffic_json, cfg.name)
     mode = args.step if args.step == "serial" else step_mode_of(args, cfg)
+    log(f"timed steps ({mode}): {args.warmup} warm-up + {args.steps}")
     wall_ms, launch_ms = timed_steps(cfg, layers, bufs, slots, args, mode)
     launches = launch_rooflines(cfg, layers[0], launch_ms, traffic, mode)
     dominant = max(launches, key=lambda r: r["avg_launch_ms"])
@@ -476,29 +495,37 @@ def main():
     if step_parts is not None:
         out["step_parts"] = step_parts
     extras = None
-    if not args.no_extras:
-        extras = measure_extras(args, cfg, slots, bufs, layers, stream)
+    if extras_on & {"parts", "fp8", "scoring", "uncompressed"}:
+        extras = measure_extras(args, cfg, slots, bufs, layers, stream, extras_on)
         ua = extras.get("uncompressed_attention")
         if ua is not None:
             ua["speedup_of_compressed"] = round(ua["ms"] / breakdown["ms"]["chunk_attention"], 3)
         out["extras"] = extras
-    if not args.no_extras and args.resolution == "480p":
+    if extras_on & {"sweep", "1080p"} and args.resolution == "480p":
+        out.setdefault("extras", {})
         for b in bufs[1:]:
             b.clear()
         del layers
         torch.cuda.empty_cache()
-        out["extras"]["sweep_480p"] = measure_sweep(args, bufs[0], stream)
-        out["extras"]["unit_1080p"] = measure_1080p(args, stream)
+        if "sweep" in extras_on:
+            log("extras: keep-fraction x segment-length sweep")
+            out["extras"]["sweep_480p"] = measure_sweep(args, bufs[0], stream)
+        if "1080p" in extras_on:
+            log("extras: 1080P unit")
+            out["extras"]["unit_1080p"] = measure_1080p(args, stream)
     if not args.no_rollout and not args.no_extras:
         for b in bufs:   # free the single-layer buffers before the 30-layer caches
             b.clear()
         torch.cuda.empty_cache()
+        log("rollout: 30 layers x 4 steps x 10 chunks, three scoring modes")
         out["rollout_480p"] = measure_rollouts({"per_layer_scoring": (False, False),
                                                 "per_layer_incremental_rescoring": (False, True),
                                                 "pooled_first_block_proxy": (True, False)})
+        log("rollout: 60 chunks")
         out["rollout_480p_60_chunks"] = measure_rollouts({"per_layer_scoring": (False, False)}, n_chunks=60,
                                                          reps=1)
     if not args.no_cpu_baseline and args.resolution == "480p":
+        log("cpu_baseline: the oracle on the host cores (480P unit, then the 1080P sample)")
         out["cpu_baseline"] = cpu_baseline(cfg, x, args.cpu_rows)
         out["cpu_baseline"]["leg_1080p"] = cpu_baseline_1080p(args.cpu_rows_1080p)
     print(json.dumps(out), flush=True)
@@ -514,12 +541,14 @@ def _next_pair(layers, bufs):
     return layers[i], bufs[i]
 
 
-def measure_extras(args, cfg, slots, bufs, layers, stream):
-    """Measurements outside the step: where the two-stream step's time goes,
-    the FP8 variant, incremental rescoring, the first-block proxy (scores
-    pooled over all heads, once per chunk, shared by every layer) and the same
-    attention kernel on the uncompressed cache (every head keeps all H frames),
-    for the kernel-level speedup of the compression."""
+def measure_extras(args, cfg, slots, bufs, layers, stream, which):
+    """Measurements outside the step (each selected by name in `which`):
+    parts -- the compacting two-stream step's attention launches, each alone;
+    fp8 -- the FP8 variant (packing + attention); scoring -- incremental
+    rescoring and the first-block proxy (scores pooled over all heads, once per
+    chunk, shared by every layer); uncompressed -- the same attention kernel on
+    the uncompressed cache (every head keeps all H frames), for the
+    kernel-level speedup of the compression."""
     import numpy as np
     import torch
     import workloads as W
@@ -528,84 +557,96 @@ def measure_extras(args, cfg, slots, bufs, layers, stream):
 
     d, F, H, Lq = cfg.head_dim, cfg.frame_tokens, cfg.hist_frames, cfg.lq
     L0, b = layers[0], bufs[0]
-    pooled = torch.empty((L0.n_seg,), dtype=torch.float32, device="cuda")
-    ws = torch.zeros(max(fkv.fkv_score_pooled_workspace_size(L0.shape), 1), dtype=torch.uint8, device="cuda")
-    pooled_ms = _time_ms(lambda: fkv.fkv_score_pooled(L0.shape, b["K_hist"], slots, b["K_cur"], pooled, ws),
-                         20, stream)
-    pooled_bytes = cfg.n_heads * (H + 1) * F * d * 2
-    stats = torch.empty(fkv.fkv_score_stats_size(L0.shape, L0.heads) // 8, dtype=torch.float64, device="cuda")
-    hist_ms = _time_ms(lambda: fkv.fkv_score_history(L0.shape, L0.heads, b["K_hist"], slots, stats,
-                                                     L0.workspace), 20, stream)
-    cached_ms = _time_ms(lambda: fkv.fkv_score_segments_cached(L0.shape, L0.heads, b["K_hist"], slots,
-                                                               b["K_cur"], stats, L0.scores, L0.workspace), 20,
-                         stream)
-    n_dyn = sum(1 for t in L0.types if t == W.DYNAMIC)
+    out = {}
+    if "scoring" in which:
+        log("extras: incremental rescoring and the pooled proxy")
+        pooled = torch.empty((L0.n_seg,), dtype=torch.float32, device="cuda")
+        ws = torch.zeros(max(fkv.fkv_score_pooled_workspace_size(L0.shape), 1), dtype=torch.uint8, device="cuda")
+        pooled_ms = _time_ms(lambda: fkv.fkv_score_pooled(L0.shape, b["K_hist"], slots, b["K_cur"], pooled, ws),
+                             20, stream)
+        pooled_bytes = cfg.n_heads * (H + 1) * F * d * 2
+        stats = torch.empty(fkv.fkv_score_stats_size(L0.shape, L0.heads) // 8, dtype=torch.float64,
+                            device="cuda")
+        hist_ms = _time_ms(lambda: fkv.fkv_score_history(L0.shape, L0.heads, b["K_hist"], slots, stats,
+                                                         L0.workspace), 20, stream)
+        cached_ms = _time_ms(lambda: fkv.fkv_score_segments_cached(L0.shape, L0.heads, b["K_hist"], slots,
+                                                                   b["K_cur"], stats, L0.scores, L0.workspace),
+                             20, stream)
+        n_dyn = sum(1 for t in L0.types if t == W.DYNAMIC)
+        out["incremental_score"] = {
+            "history_ms": round(hist_ms, 4), "step_ms": round(cached_ms, 4),
+            "step_GB_s": round(n_dyn * 2 * F * d * 2 / (cached_ms * 1e-3) / 1e9, 1),
+            "note": "history statistics once per chunk, then per AR step the scores from them plus frames "
+                    "H-1 and H (2 of the 22 frames per dynamic head)"}
+        out["pooled_proxy_score"] = {
+            "ms": round(pooled_ms, 4), "GB_s": round(pooled_bytes / (pooled_ms * 1e-3) / 1e9, 1),
+            "frac_of_hbm_peak": round(pooled_bytes / (pooled_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 3),
+            "note": "all 12 heads pooled, once per AR step for all layers (not part of the step)"}
 
-    # where the two-stream step's time goes: each attention launch alone, the
-    # one 12-head launch, and the step without the dynamic compression (its
-    # attention then reads the compacted cache of the previous step)
-    def rot(fn):
-        return lambda: fn(*_next_pair(layers, bufs))
+    if "parts" in which:
+        # the compacting two-stream step's launches: each attention launch
+        # alone, the one 12-head launch, and the step without the dynamic
+        # compression (its attention then reads the compacted cache of the
+        # previous step)
+        log("extras: the compacting step's launches")
 
-    def static_only(L, bb):
-        L.attention_static(bb["K_hist"], bb["V_hist"], slots, bb["Q"], bb["K_cur"], bb["V_cur"], bb["O"],
-                           None, L.attn_workspace)
+        def rot(fn):
+            return lambda: fn(*_next_pair(layers, bufs))
 
-    def dynamic_only(L, bb):
-        fkv.fkv_chunk_attention_heads(L.shape, L.dynamic_heads, bb["Q"], L.Kc, L.Vc, L.kv_len, bb["K_cur"],
-                                      bb["V_cur"], L.scale, bb["O"], None, L.attn_workspace)
+        def static_only(L, bb):
+            L.attention_static(bb["K_hist"], bb["V_hist"], slots, bb["Q"], bb["K_cur"], bb["V_cur"], bb["O"],
+                               None, L.attn_workspace)
 
-    def all_heads(L, bb):
-        L.attention(bb["Q"], bb["K_cur"], bb["V_cur"], bb["O"])
+        def dynamic_only(L, bb):
+            fkv.fkv_chunk_attention_heads(L.shape, L.dynamic_heads, bb["Q"], L.Kc, L.Vc, L.kv_len, bb["K_cur"],
+                                          bb["V_cur"], L.scale, bb["O"], None, L.attn_workspace)
 
-    def step_nocomp(L, bb):
-        main = torch.cuda.current_stream()
-        L.side.wait_stream(main)
-        with torch.cuda.stream(L.side):
-            static_only(L, bb)
-        dynamic_only(L, bb)
-        main.wait_stream(L.side)
+        def all_heads(L, bb):
+            L.attention(bb["Q"], bb["K_cur"], bb["V_cur"], bb["O"])
 
-    parts = {name: round(_time_ms(rot(fn), 50, stream), 4)
-             for name, fn in (("static_heads_in_place_ms", static_only), ("dynamic_heads_ms", dynamic_only),
-                              ("all_heads_one_launch_ms", all_heads), ("step_without_compression_ms", step_nocomp))}
+        def step_nocomp(L, bb):
+            main = torch.cuda.current_stream()
+            L.side.wait_stream(main)
+            with torch.cuda.stream(L.side):
+                static_only(L, bb)
+            dynamic_only(L, bb)
+            main.wait_stream(L.side)
 
-    O8 = torch.empty_like(b["Q"])
-    pack_ms = _time_ms(lambda: L0.pack_fp8(b["Q"], b["K_cur"], b["V_cur"]), 20, stream)
-    fp8_ms = _time_ms(lambda: L0.attention_fp8_packed(O8), 20, stream)
-    kv_len = L0.kv_len.cpu().numpy().astype(np.int64)
-    attn_flop = attention_flop(cfg, kv_len)
+        parts = {name: round(_time_ms(rot(fn), 50, stream), 4)
+                 for name, fn in (("static_heads_in_place_ms", static_only), ("dynamic_heads_ms", dynamic_only),
+                                  ("all_heads_one_launch_ms", all_heads),
+                                  ("step_without_compression_ms", step_nocomp))}
+        out["compact_step_launches"] = dict(parts, note="the compacting two-stream step's launches, each timed "
+                                                        "alone over the rotated buffer copies")
 
-    full_heads = tuple(W.HeadBudget(W.STATIC, 0, H) for _ in range(cfg.n_heads))
-    full = CompressedLayer(cfg.n_heads, d, F, H, cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype,
-                           full_heads, balanced=args.schedule == "balanced")
-    full.compress_static(b["K_hist"], b["V_hist"], slots)
-    O = torch.empty_like(b["Q"])
-    full_ms = _time_ms(lambda: full.attention(b["Q"], b["K_cur"], b["V_cur"], O), 10, stream)
-    full_flop = 4.0 * Lq * d * cfg.n_heads * (H * F + Lq)
-    del full
-
-    return {
-        "compact_step_launches": dict(parts, note="the compacting two-stream step's launches, each timed alone "
-                                                  "over the rotated buffer copies"),
-        "fp8_attention": {
+    if "fp8" in which:
+        log("extras: FP8 packing + attention")
+        O8 = torch.empty_like(b["Q"])
+        pack_ms = _time_ms(lambda: L0.pack_fp8(b["Q"], b["K_cur"], b["V_cur"]), 20, stream)
+        fp8_ms = _time_ms(lambda: L0.attention_fp8_packed(O8), 20, stream)
+        kv_len = L0.kv_len.cpu().numpy().astype(np.int64)
+        attn_flop = attention_flop(cfg, kv_len)
+        out["fp8_attention"] = {
             "attention_ms": round(fp8_ms, 4), "TFLOP_s": round(attn_flop / (fp8_ms * 1e-3) / 1e12, 1),
             "peak_TFLOP_s": PEAK_FP8_TFLOPS,
             "frac_of_fp8_peak": round(attn_flop / (fp8_ms * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 4),
             "pack_ms": round(pack_ms, 4), "pack_plus_attention_ms": round(pack_ms + fp8_ms, 4),
-            "note": "E4M3 Q/K/V/P on gfx950 FP8 MFMA; pack = statistics + quantise + transpose"},
-        "incremental_score": {"history_ms": round(hist_ms, 4), "step_ms": round(cached_ms, 4),
-                              "step_GB_s": round(n_dyn * 2 * F * d * 2 / (cached_ms * 1e-3) / 1e9, 1),
-                              "note": "history statistics once per chunk, then per AR step the scores from "
-                                      "them plus frames H-1 and H (2 of the 22 frames per dynamic head)"},
-        "pooled_proxy_score": {
-            "ms": round(pooled_ms, 4), "GB_s": round(pooled_bytes / (pooled_ms * 1e-3) / 1e9, 1),
-            "frac_of_hbm_peak": round(pooled_bytes / (pooled_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 3),
-            "note": "all 12 heads pooled, once per AR step for all layers (not part of the step)"},
-        "uncompressed_attention": {
-            "ms": round(full_ms, 4), "TFLOP_s": round(full_flop / (full_ms * 1e-3) / 1e12, 1),
-            "kv_len": H * F},
-    }
+            "note": "E4M3 Q/K/V/P on gfx950 FP8 MFMA; pack = statistics + quantise + transpose"}
+
+    if "uncompressed" in which:
+        log("extras: uncompressed attention")
+        full_heads = tuple(W.HeadBudget(W.STATIC, 0, H) for _ in range(cfg.n_heads))
+        full = CompressedLayer(cfg.n_heads, d, F, H, cfg.cap_frames, cfg.chunk_frames, cfg.seg_tokens, cfg.dtype,
+                               full_heads, balanced=args.schedule == "balanced", step_mode="compact")
+        full.compress_static(b["K_hist"], b["V_hist"], slots)
+        O = torch.empty_like(b["Q"])
+        full_ms = _time_ms(lambda: full.attention(b["Q"], b["K_cur"], b["V_cur"], O), 10, stream)
+        full_flop = 4.0 * Lq * d * cfg.n_heads * (H * F + Lq)
+        del full
+        out["uncompressed_attention"] = {"ms": round(full_ms, 4),
+                                         "TFLOP_s": round(full_flop / (full_ms * 1e-3) / 1e12, 1),
+                                         "kv_len": H * F}
+    return out
 
 
 def measure_sweep(args, b, stream, reps=30):
