@@ -58,6 +58,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=100)
     p.add_argument("--resolution", default="480p", choices=["480p", "1080p"])
     p.add_argument("--copies", type=int, default=4, help="independent layer buffers rotated per step")
+    p.add_argument("--breakdown-reps", type=int, default=200,
+                   help="serial units of the per-stage pass ahead of the timed steps (at least --steps)")
     p.add_argument("--cpu-rows", type=int, default=4680,
                    help="query rows per head in the 480P CPU oracle sample (4680 = every row)")
     p.add_argument("--cpu-rows-1080p", type=int, default=512,
@@ -392,9 +394,9 @@ def load_traffic(path, workload):
             tj = json.load(f)
     except (OSError, ValueError):
         return None
-    if tj.get("workload") != workload or tj.get("kernel_source_sha") != _kernel_sha():
+    if tj.get("kernel_source_sha") != _kernel_sha():
         return None
-    return tj.get("bytes_per_launch_by_launch")
+    return (tj.get("workloads") or {}).get(workload, {}).get("bytes_per_launch_by_launch")
 
 
 def main():
@@ -442,7 +444,7 @@ def main():
     log("per-stage breakdown (serial compacting path)")
     # (at least 200 serial units, ~0.1 s at 480P: the clock takes some tens of ms of MFMA
     # load to settle, and the timed steps follow right after)
-    stage = staged_breakdown(layers, bufs, slots, max(args.steps, 200), stream)
+    stage = staged_breakdown(layers, bufs, slots, max(args.steps, args.breakdown_reps), stream)
     breakdown = stage_report(cfg, layers[0], stage)
 
     traffic = load_traffic(args.traffic_json, cfg.name)
