@@ -58,8 +58,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=100)
     p.add_argument("--resolution", default="480p", choices=["480p", "1080p"])
     p.add_argument("--copies", type=int, default=4, help="independent layer buffers rotated per step")
-    p.add_argument("--breakdown-reps", type=int, default=200,
-                   help="serial units of the per-stage pass ahead of the timed steps (at least --steps)")
+    p.add_argument("--breakdown-reps", type=int, default=50,
+                   help="serial units of the per-stage pass ahead of the timed steps")
     p.add_argument("--cpu-rows", type=int, default=4680,
                    help="query rows per head in the 480P CPU oracle sample (4680 = every row)")
     p.add_argument("--cpu-rows-1080p", type=int, default=512,
@@ -442,9 +442,10 @@ def main():
 
     # per-stage breakdown first: it also brings the clock up before the timed steps
     log("per-stage breakdown (serial compacting path)")
-    # (at least 200 serial units, ~0.1 s at 480P: the clock takes some tens of ms of MFMA
-    # load to settle, and the timed steps follow right after)
-    stage = staged_breakdown(layers, bufs, slots, max(args.steps, args.breakdown_reps), stream)
+    # (50 serial units, ~30 ms at 480P: long enough for the clock to come up; a
+    # longer pass, 200 units, measurably slowed the timed steps that follow --
+    # sustained MFMA load lowers the clock the part holds)
+    stage = staged_breakdown(layers, bufs, slots, max(args.breakdown_reps, 1), stream)
     breakdown = stage_report(cfg, layers[0], stage)
 
     traffic = load_traffic(args.traffic_json, cfg.name)

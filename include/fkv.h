@@ -271,8 +271,9 @@ fkv_status fkv_score_select(const fkv_shape *shape, const fkv_head *heads,
 /* Device workspace fkv_chunk_attention takes for its balanced schedule on the
  * CURRENT device (hipGetDevice): 2 x the device's compute units, rounded down
  * to a multiple of 8, partial-result slots of 256 rows x (2*head_dim + 8)
- * bytes (about 34 MB for head_dim 128 on a 256-CU device).  0 for FKV_F32, which has
- * no balanced schedule.  FKV_ERR_DEVICE if the device cannot be queried. */
+ * bytes (about 34 MB for head_dim 128 on a 256-CU device), then one 256-byte
+ * arrival counter per (head, 256-row query tile).  0 for FKV_F32, which has no
+ * balanced schedule.  FKV_ERR_DEVICE if the device cannot be queried. */
 fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes);
 
 /* Chunk attention over the compressed cache (Eq. 2 for static heads, Eq. 4
@@ -294,11 +295,12 @@ fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes);
  *
  * Work schedule (bf16): with workspace == NULL every (head, 256-row query
  * tile) is one workgroup; heads with longer caches then finish last.  With a
- * device workspace of at least fkv_attention_workspace_size bytes (contents
- * need no initialisation) the key tiles of all heads and query tiles are split
- * evenly over one workgroup per compute unit, and tiles cut by a split are
- * combined by a second kernel on the same stream (FKV_ERR_CAPACITY if the
- * workspace is smaller).  Both schedules compute the same function; a split
+ * device workspace of at least fkv_attention_workspace_size bytes, zero-filled
+ * by the caller before its first use (every bf16 call leaves its counters at
+ * zero again), the key tiles of all heads and query tiles are split evenly
+ * over one workgroup per compute unit, and the parts of a tile cut by a split
+ * are combined by the workgroup that completes the last of them
+ * (FKV_ERR_CAPACITY if the workspace is smaller).  Both schedules compute the same function; a split
  * tile's parts are normalised and rounded to bf16 before they are combined, so
  * its output may differ from the one-workgroup result by about one bf16 step.
  * fp32 ignores the workspace.  Two calls that share a workspace must be

@@ -475,8 +475,9 @@ def _attention_args(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, O, lse, w
 def fkv_chunk_attention(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, scale: float, O,
                         lse: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
                         stream=None):
-    """``workspace`` (uint8 device tensor of fkv_attention_workspace_size bytes)
-    selects the balanced schedule; None runs one workgroup per query tile."""
+    """``workspace`` (uint8 device tensor of fkv_attention_workspace_size bytes,
+    zero-filled before its first use, e.g. torch.zeros) selects the balanced
+    schedule; None runs one workgroup per query tile."""
     q, kc, vc, slab, kl, kq, vq, o, ls, ws, nws = _attention_args(shape, Q, Kc, Vc, kv_len, K_cur, V_cur, O,
                                                                   lse, workspace)
     _raise(lib().fkv_chunk_attention(ctypes.byref(shape), q, kc, vc, slab, kl, kq, vq,

@@ -196,6 +196,14 @@ fkv_status balanced_blocks(int *blocks) {
     return FKV_OK;
 }
 
+// Attention workspace (bf16 balanced schedule): 2 * blocks partial-result
+// slots, then one arrival counter per (head, query tile) item.
+size_t attention_workspace_bytes(const fkv_shape *s, int blocks) {
+    const int64_t lq = (int64_t)s->chunk_frames * s->frame_tokens;
+    const int64_t n_items = (int64_t)s->n_heads * ((lq + fkv::kAttnRowsBf16 - 1) / fkv::kAttnRowsBf16);
+    return 2 * (size_t)blocks * fkv::attention_part_bytes(s->head_dim) + fkv::attention_counter_bytes(n_items);
+}
+
 // Scoring geometry: units of U = min(L, F) tokens per frame, their 16-byte
 // vectors, and the column groups (workgroups) per unit.
 void score_geometry(const fkv_shape *s, int *units, int64_t *unit_vecs, int *n_cg) {
@@ -766,7 +774,7 @@ fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes) {
     if (shape->dtype != FKV_BF16) return ok();
     int blocks = 0;
     if ((st = balanced_blocks(&blocks)) != FKV_OK) return st;
-    *bytes = 2 * (size_t)blocks * fkv::attention_part_bytes(shape->head_dim);
+    *bytes = attention_workspace_bytes(shape, blocks);
     return ok();
 }
 
@@ -822,7 +830,7 @@ fkv_status chunk_attention_impl(const fkv_shape *shape, const fkv::HeadList &lis
     int blocks = 0;
     if (bf16 && workspace) {
         if ((st = balanced_blocks(&blocks)) != FKV_OK) return st;
-        const size_t need = 2 * (size_t)blocks * fkv::attention_part_bytes(shape->head_dim);
+        const size_t need = attention_workspace_bytes(shape, blocks);
         if (workspace_bytes < need)
             return fail(FKV_ERR_CAPACITY, "attention workspace of %zu bytes, %zu needed", workspace_bytes, need);
     }
@@ -850,6 +858,8 @@ fkv_status chunk_attention_impl(const fkv_shape *shape, const fkv::HeadList &lis
     a.items_per_xcd = (a.n_items + 7) / 8;
     a.n_blocks = blocks;
     a.part = (float *)workspace;
+    if (workspace)
+        a.item_counters = (uint32_t *)((char *)workspace + 2 * (size_t)blocks * fkv::attention_part_bytes(shape->head_dim));
     if (paged) {
         a.paged = 1;
         a.K_hist = paged->K_hist;

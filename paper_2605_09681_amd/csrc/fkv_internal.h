@@ -133,6 +133,8 @@ struct AttnArgs {
     int32_t items_per_xcd;          // ceil(n_items / 8)
     int32_t n_blocks;               // balanced schedule: workgroups (multiple of 8); 0 = one per item
     float *part;                    // balanced schedule: 2 * n_blocks partial-result slots
+    uint32_t *item_counters;        // balanced schedule, bf16: arrivals per item (kItemCounterStride apart),
+                                    // zero between calls
     int32_t mass_F;                 // attention mass: keys per bin (frame tokens)
     int32_t mass_bins;              // attention mass: bins per head
     int32_t mass_acc;               // attention mass: 1 = add to mass_out, 0 = overwrite
@@ -194,6 +196,10 @@ hipError_t launch_score(const ScoreArgs &a, bool f32, hipStream_t s);
 void score_workspace_layout(ScoreArgs &a, void *ws, int n_list, int H, int units, int n_cg);
 hipError_t launch_attention_bf16(const AttnArgs &a, int head_dim, hipStream_t s);
 size_t attention_part_bytes(int head_dim);  // bytes of one partial-result slot (bf16 kernel)
+// Arrival counters of the bf16 balanced schedule: one 256-byte line per item,
+// after the 2 * n_blocks partial-result slots of the workspace.
+constexpr int kItemCounterStride = 64;   // uint32 per counter
+inline size_t attention_counter_bytes(int64_t n_items) { return (size_t)n_items * kItemCounterStride * 4; }
 
 // attention mass per key block (head profiling), k_attn.hip; the workspace holds
 // n_heads * n_qtiles * 8 waves * mass_bins floats

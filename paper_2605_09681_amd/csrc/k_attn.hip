@@ -321,6 +321,100 @@ __device__ __forceinline__ void mfma_block(const uint16_t *vs, const uint16_t *k
     }
 }
 
+// Values another workgroup of the same launch reads (the parts of a cut
+// item) are written and read with device-scope accesses (sc1: coherent across
+// the XCDs' L2 caches for that location); no cache write-back or invalidation
+// is needed, which agent-scope fences would do to the whole L2 of the XCD.
+__device__ __forceinline__ void put_shared(unsigned long long *p, uint2 v) {
+    __hip_atomic_store(p, ((unsigned long long)v.y << 32) | v.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void put_shared(float *p, float v) {
+    __hip_atomic_store((uint32_t *)p, __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <bool SHARED>
+__device__ __forceinline__ uint2 get_part(const uint2 *p) {
+    if (!SHARED) return *p;
+    const unsigned long long v =
+        __hip_atomic_load((unsigned long long *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+}
+template <bool SHARED>
+__device__ __forceinline__ float get_part(const float *p) {
+    if (!SHARED) return *p;
+    return __uint_as_float(__hip_atomic_load((uint32_t *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+
+// Combines the parts of a cut item (list entry li, query tile qt; first tile
+// ibase of the concatenated sequence, T tiles), for the 32 rows of wave block
+// w.  With part maxima m_j, sums l_j and normalised outputs o_j of a row,
+//   M = max_j m_j,  w_j = 2^(m_j - M) l_j,  L = sum_j w_j,  O = sum_j w_j o_j / L,
+// and lse = ln 2 * M + ln L, the parts taken in schedule order.  Thread t of
+// the NT that share the block handles row t % 32 and the block's uint2
+// elements i * NT + t -- every element gets the same arithmetic whichever
+// thread does it.  SHARED: the parts were written in this launch.
+template <int D, bool SHARED, int NT>
+__device__ __forceinline__ void merge_rows(const AttnArgs &a, const Schedule &sc, int li, int qt, int64_t ibase,
+                                           int T, int w, int t) {
+    using C = Cfg<D>;
+    constexpr int kML = BM * D / 2;        // float offset of m within a slot
+    constexpr int kVecs = C::MB * 4 * 64;  // uint2s (4 values) of one wave block's accumulators
+    constexpr int kPer = kVecs / NT;
+    const int h = a.heads.head[li];
+    const int b0 = sc.owner(ibase), b1 = sc.owner(ibase + T - 1);
+    // the item is b0's last segment unless b0's range starts with it, and the
+    // first segment of every later workgroup up to b1
+    const int s0 = sc.start(b0) == ibase ? 2 * b0 : 2 * b0 + 1;
+    const int r = t & 31, row = w * 32 + r;
+    const int qrow = qt * BM + row;
+    float M = -__builtin_inff(), L = 0.f;
+    float x[kPer][4] = {};
+    for (int b = b0; b <= b1; ++b) {
+        const float *p = a.part + (size_t)(b == b0 ? s0 : 2 * b) * slot_floats<D>();
+        const float m = get_part<SHARED>(p + kML + row), l = get_part<SHARED>(p + kML + BM + row);
+        uint2 v[kPer];
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) v[i] = get_part<SHARED>((const uint2 *)p + (size_t)w * kVecs + i * NT + t);
+        const float Mn = fmaxf(M, m);
+        const float s = __builtin_amdgcn_exp2f(M - Mn), wg = __builtin_amdgcn_exp2f(m - Mn) * l;
+        M = Mn;
+        L = L * s + wg;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            x[i][0] = x[i][0] * s + wg * bf16_lo(v[i].x);
+            x[i][1] = x[i][1] * s + wg * bf16_hi(v[i].x);
+            x[i][2] = x[i][2] * s + wg * bf16_lo(v[i].y);
+            x[i][3] = x[i][3] * s + wg * bf16_hi(v[i].y);
+        }
+    }
+    if (qrow >= a.Lq) return;
+    if (a.lse && t < 32) a.lse[(size_t)h * a.Lq + qrow] = fmaf(M, 0.69314718055994530942f, logf(L));
+    const float inv = 1.f / L;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int q = i * NT + t;
+        const int mb = q / (4 * 64), g = (q / 64) % 4;
+        const int d0 = 32 * mb + 8 * g + 4 * ((t & 63) >> 5);
+        *(uint2 *)((uint16_t *)a.O + ((size_t)h * a.Lq + qrow) * D + d0) =
+            pack_bf16x4(x[i][0] * inv, x[i][1] * inv, x[i][2] * inv, x[i][3] * inv);
+    }
+}
+
+// Arrival of a workgroup on a device-scope counter, once every wave's
+// device-scope stores have completed; true in every thread of the workgroup
+// that arrives last (which resets the counter to zero for the next call).
+__device__ __forceinline__ bool arrive_last(uint32_t *counter, uint32_t expected, uint32_t *flag) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t old = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const bool last = old + 1 == expected;
+        if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *flag = last ? 1u : 0u;
+    }
+    __syncthreads();
+    return *flag != 0;
+}
+
 // One segment: positions [t0, t1) of item (h, qt), where position j is key
 // tile (j + rot) mod T of the item's T tiles (the order of key tiles does not
 // change the result beyond rounding).  slot == nullptr means the segment is the
@@ -598,17 +692,20 @@ __device__ __forceinline__ void attn_segment(const AttnArgs &a, uint16_t (&Ks)[2
     const float l_tot = l_run + __shfl_xor(l_run, 32);
     const float inv = 1.f / l_tot;
     if (slot) {
-        uint2 *op = (uint2 *)slot;
+        // device-scope stores: the workgroup that merges the item may run on
+        // another XCD, within this launch
+        unsigned long long *op = (unsigned long long *)slot;
 #pragma unroll
         for (int mb = 0; mb < C::MB; ++mb)
 #pragma unroll
-            for (int g = 0; g < 4; ++g)
-                op[((wave * C::MB + mb) * 4 + g) * 64 + lane] =
-                    pack_bf16x4(o[mb][4 * g] * inv, o[mb][4 * g + 1] * inv, o[mb][4 * g + 2] * inv,
-                                o[mb][4 * g + 3] * inv);
+            for (int g = 0; g < 4; ++g) {
+                const uint2 v = pack_bf16x4(o[mb][4 * g] * inv, o[mb][4 * g + 1] * inv, o[mb][4 * g + 2] * inv,
+                                            o[mb][4 * g + 3] * inv);
+                put_shared(op + ((wave * C::MB + mb) * 4 + g) * 64 + lane, v);
+            }
         if (hl == 0) {
-            slot[BM * D / 2 + wave * 32 + l32] = m_run;
-            slot[BM * D / 2 + BM + wave * 32 + l32] = l_tot;
+            put_shared(slot + BM * D / 2 + wave * 32 + l32, m_run);
+            put_shared(slot + BM * D / 2 + BM + wave * 32 + l32, l_tot);
         }
         return;
     }
@@ -636,6 +733,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
     using C = Cfg<D>;
     __shared__ __attribute__((aligned(16))) uint16_t Ks[2][C::TILE];
     __shared__ __attribute__((aligned(16))) uint16_t Vs[2][C::VTILE];
+    __shared__ uint32_t flag;
 
     if (!BAL) {
         const int item = (blockIdx.x & 7) * a.items_per_xcd + (blockIdx.x >> 3);
@@ -668,73 +766,33 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
         // by a range length), so the XCD's L2 serves the re-reads.
         const int rot = (int)((ibase - sc.start(sc.owner(ibase))) % T);
         attn_segment<D, PAGED>(a, Ks, Vs, ip.li, qt, t0, t1, rot, slot);
+        if (slot) {
+            // the last of the item's parts to arrive combines them (no wait:
+            // every other part is complete when its workgroup arrives)
+            const int n_parts = sc.owner(ibase + T - 1) - sc.owner(ibase) + 1;
+            uint32_t *cnt = a.item_counters + (size_t)(ip.li * a.n_qtiles + qt) * kItemCounterStride;
+            if (arrive_last(cnt, (uint32_t)n_parts, &flag))
+                merge_rows<D, true, 64>(a, sc, ip.li, qt, ibase, T, threadIdx.x >> 6, threadIdx.x & 63);
+        }
         cur = ibase + t1;
         first = false;
     }
 }
 
-// Combines the parts of every item the balanced schedule split: with part
-// maxima m_j, sums l_j and normalised outputs o_j of a row,
-//   M = max_j m_j,  w_j = 2^(m_j - M) l_j,  L = sum_j w_j,  O = sum_j w_j o_j / L,
-// and lse = ln 2 * M + ln L.  Workgroup (item, w) handles the 32 rows of wave
-// w of the item's query tile; items computed whole are skipped.
+// Combines the parts of every item the balanced schedule split, in a second
+// kernel (the FP8 path; the bf16 kernel merges in place): workgroup
+// (item, w) handles the 32 rows of wave block w of the item's query tile;
+// items computed whole are skipped.
 template <int D, bool PAGED>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-    using C = Cfg<D>;
-    constexpr int kML = BM * D / 2;  // float offset of m within a slot
     const int item = blockIdx.x, w = blockIdx.y;
     const int li = item / a.n_qtiles, qt = item - li * a.n_qtiles;
-    const int h = a.heads.head[li];
     const WorkList wl = work_list<PAGED>(a);
     const Schedule sc = make_schedule(a, wl);
     const int T = __builtin_amdgcn_readlane(wl.T, li);
     const int64_t P = entry_base(wl, li) + (int64_t)qt * T;
-    const int b0 = sc.owner(P), b1 = sc.owner(P + T - 1);
-    if (b0 == b1) return;
-    // the item is b0's last segment unless b0's range starts with it, and the
-    // first segment of every later workgroup up to b1
-    const int s0 = sc.start(b0) == P ? 2 * b0 : 2 * b0 + 1;
-    auto part = [&](int b) -> const float * {
-        return a.part + (size_t)(b == b0 ? s0 : 2 * b) * slot_floats<D>();
-    };
-    // Thread tid handles row r = tid % 32 of the wave's 32 rows; it combines
-    // the row's parts in one pass with a running maximum.
-    const int tid = threadIdx.x;
-    const int r = tid & 31, row = w * 32 + r;
-    const int qrow = qt * BM + row;
-    constexpr int kVecs = C::MB * 4 * 64;  // uint2s (4 values) of one wave's accumulators
-    constexpr int kPer = kVecs / 256;
-    float M = -__builtin_inff(), L = 0.f;
-    float x[kPer][4] = {};
-    for (int b = b0; b <= b1; ++b) {
-        const float *p = part(b);
-        const float m = p[kML + row], l = p[kML + BM + row];
-        uint2 v[kPer];
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) v[i] = ((const uint2 *)p)[(size_t)w * kVecs + i * 256 + tid];
-        const float Mn = fmaxf(M, m);
-        const float sc = __builtin_amdgcn_exp2f(M - Mn), wg = __builtin_amdgcn_exp2f(m - Mn) * l;
-        M = Mn;
-        L = L * sc + wg;
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-            x[i][0] = x[i][0] * sc + wg * bf16_lo(v[i].x);
-            x[i][1] = x[i][1] * sc + wg * bf16_hi(v[i].x);
-            x[i][2] = x[i][2] * sc + wg * bf16_lo(v[i].y);
-            x[i][3] = x[i][3] * sc + wg * bf16_hi(v[i].y);
-        }
-    }
-    if (qrow >= a.Lq) return;
-    if (a.lse && tid < 32) a.lse[(size_t)h * a.Lq + qrow] = fmaf(M, 0.69314718055994530942f, logf(L));
-    const float inv = 1.f / L;
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-        const int q = i * 256 + tid;
-        const int mb = q / (4 * 64), g = (q / 64) % 4;
-        const int d0 = 32 * mb + 8 * g + 4 * ((tid & 63) >> 5);
-        *(uint2 *)((uint16_t *)a.O + ((size_t)h * a.Lq + qrow) * D + d0) =
-            pack_bf16x4(x[i][0] * inv, x[i][1] * inv, x[i][2] * inv, x[i][3] * inv);
-    }
+    if (sc.owner(P) == sc.owner(P + T - 1)) return;
+    merge_rows<D, false, 256>(a, sc, li, qt, P, T, w, threadIdx.x);
 }
 
 // ------------------------------------------------------------ attention mass
@@ -857,8 +915,7 @@ hipError_t launch_bf16(const AttnArgs &a, int head_dim, hipStream_t s) {
             hipLaunchKernelGGL((attn_bf16_kernel<128, true, PAGED>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
         else
             hipLaunchKernelGGL((attn_bf16_kernel<64, true, PAGED>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
-        const hipError_t e = hipGetLastError();
-        return e != hipSuccess ? e : launch_attention_merge(a, head_dim, s);
+        return hipGetLastError();
     }
     const unsigned blocks = (unsigned)a.items_per_xcd * 8u;
     if (head_dim == 128)

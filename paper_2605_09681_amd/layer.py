@@ -89,7 +89,8 @@ class CompressedLayer:
             with torch.cuda.device(dev):
                 n = fkv_attention_workspace_size(self.shape)
             if n > 0:
-                self.attn_workspace = torch.empty(n, dtype=torch.uint8, device=dev)
+                # zero-filled once (arrival counters); every call leaves it so
+                self.attn_workspace = torch.zeros(n, dtype=torch.uint8, device=dev)
         self.scale = 1.0 / math.sqrt(head_dim)
         self.has_static = FKV_STATIC in self.types
         self.has_dynamic = FKV_DYNAMIC in self.types
@@ -99,7 +100,7 @@ class CompressedLayer:
         self.static_heads = [h for h, t in enumerate(self.types) if t == FKV_STATIC]
         self.dynamic_heads = [h for h, t in enumerate(self.types) if t == FKV_DYNAMIC]
         if self.side is not None and self.attn_workspace is not None:
-            self.attn_workspace2 = torch.empty_like(self.attn_workspace)
+            self.attn_workspace2 = torch.zeros_like(self.attn_workspace)
         # static heads attended in place by step() (bf16, frames >= 64 tokens)
         can = static_in_place_supported(dtype, frame_tokens)
         if in_place and not can:
@@ -356,8 +357,8 @@ class RolloutStack:
         self.pooled_ws = torch.zeros(max(fkv_score_pooled_workspace_size(full), 1), dtype=torch.uint8, device=dev)
         with torch.cuda.device(dev):
             n = fkv_attention_workspace_size(full)
-        self.attn_ws = torch.empty(max(n, 1), dtype=torch.uint8, device=dev) if n > 0 else None
-        self.attn_ws2 = torch.empty_like(self.attn_ws) if (n > 0 and overlap) else None
+        self.attn_ws = torch.zeros(max(n, 1), dtype=torch.uint8, device=dev) if n > 0 else None
+        self.attn_ws2 = torch.zeros_like(self.attn_ws) if (n > 0 and overlap) else None
         self.scale = 1.0 / math.sqrt(head_dim)
         self.side = torch.cuda.Stream(device=dev) if overlap else None
         self.static_in_place = static_in_place_supported(dtype, frame_tokens)
