@@ -219,6 +219,27 @@ def test_paged_step_modes(case, mode):
     assert_attention_close(O, ref, "bf16", lse)
 
 
+def test_paged_step_480p_every_row():
+    """The default step at the 480P shape, every query row of every head
+    against the oracle (rotated ring slots): the balanced schedule cuts nearly
+    every (head, query tile) item at this size, so this checks every cut
+    item's in-kernel merge at full size, not only on sampled rows."""
+    cfg, slot, _ = _case("480p")
+    _print_case("paged-step-every-row", case="480p")
+    x = W.make_layer_inputs(cfg, seed=56, frame_slot=slot)
+    d = dev_inputs(x)
+    layer = make_layer(cfg, step_mode="paged")
+    O = torch.empty_like(d["Q"])
+    lse = torch.empty((cfg.n_heads, cfg.lq), dtype=torch.float32, device="cuda")
+    layer.step(d["K_hist"], d["V_hist"], slot, d["Q"], d["K_cur"], d["V_cur"], O, lse)
+    torch.cuda.synchronize()
+    ref = oracle.run_layer(cfg, x, rows=None, scale=1 / math.sqrt(cfg.head_dim))
+    assert len(ref.rows) == cfg.lq
+    assert_compression_exact(cfg, layer, ref, skip_static=True, skip_dynamic_copy=True)
+    max_abs, rel = assert_attention_close(O, ref, "bf16", lse)
+    print(f"480p every row: max_abs={max_abs:.2e} rel_l2={rel:.2e}", flush=True)
+
+
 def test_paged_empty_history_and_select_only():
     """H = 0: fkv_score_select and fkv_select give every dynamic head kv_len 0
     and the paged launch attends the chunk alone; a pooled score row selects
