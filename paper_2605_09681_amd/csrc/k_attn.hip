@@ -43,8 +43,9 @@
 //
 // Schedules: a work item is (entry of the launch's head list, query tile);
 // one workgroup per item, or the balanced schedule (attn_common.h) that splits
-// the key tiles of all items evenly over one workgroup per CU and merges split
-// items in a second kernel.  Heads with longer caches make the per-item
+// the key tiles of all items evenly over one workgroup per CU; the parts of a
+// split item are merged by the workgroup that completes the last of them
+// (merge_rows).  Heads with longer caches make the per-item
 // schedule uneven (at 480P a dynamic head has 342 key tiles per query tile, a
 // static head 245, on 228 items for 256 CUs).
 #include "attn_common.h"
