@@ -319,8 +319,9 @@ def launch_rooflines(cfg, layer, launch_ms, traffic, mode):
     groups = {"static_attention": [h for h, b in enumerate(budgets) if b.type == W.STATIC],
               "dynamic_attention": [h for h, b in enumerate(budgets) if b.type == W.DYNAMIC],
               "attention": list(range(cfg.n_heads))}
-    paged = "attn_bf16_kernel<128, balanced, paged> + attn_merge_kernel<128, paged>"
-    plain = "attn_bf16_kernel<128, balanced> + attn_merge_kernel<128>"
+    # cut items are merged inside the bf16 kernel: one kernel per launch
+    paged = "attn_bf16_kernel<128, balanced, paged>"
+    plain = "attn_bf16_kernel<128, balanced>"
     kernels = {
         "paged": {"attention": f"fkv_chunk_attention_paged: {paged} (all heads, every kept history read in "
                                "place from the cache)"},
