@@ -126,15 +126,16 @@ __global__ __launch_bounds__(kThreads) void select_copy_kernel(SelectCopyArgs A)
     const int lane = threadIdx.x & 63;
     const bool two = n > 64;  // uniform: a second block of segments 64..127
 
+    const sel::Rule rule = sel::rule_of(a, li);
     const float *srow = a.scores + (int64_t)h * a.score_stride;
     const float s0 = lane < n ? srow[lane] : 0.f;
     const float s1 = two && 64 + lane < n ? srow[64 + lane] : 0.f;
-    const uint64_t F0 = __ballot(lane < n && sel::is_forced(a, li, lane));
-    const uint64_t F1 = two ? __ballot(64 + lane < n && sel::is_forced(a, li, 64 + lane)) : 0;
-    const bool per_frame = a.scope[li] == FKV_SCOPE_FRAME;
+    const uint64_t F0 = __ballot(lane < n && sel::is_forced(a, rule, lane));
+    const uint64_t F1 = two ? __ballot(64 + lane < n && sel::is_forced(a, rule, 64 + lane)) : 0;
+    const bool per_frame = rule.scope == FKV_SCOPE_FRAME;
     const int spf = per_frame ? a.F / a.L : 0;
     const int cnt = per_frame ? spf : n;  // group size, the same for every lane
-    const int kk = a.k[li];
+    const int kk = rule.k;
     // keep flag of segment g (score sg): forced, or fewer than kk group
     // members precede it in the order (isNaN(s), s, g).  Every lane runs the
     // same trip count with all lanes active (the permutes read other lanes);
@@ -151,7 +152,7 @@ __global__ __launch_bounds__(kThreads) void select_copy_kernel(SelectCopyArgs A)
             const float v1 = two ? __shfl(s1, g2 & 63) : 0.f;
             const float v = g2 >= 64 ? v1 : v0;
             const bool f2 = g2 < 64 ? (F0 >> g2) & 1 : (F1 >> (g2 - 64)) & 1;
-            rank += (!f2 && g2 != gc && sel::key_less(v, g2, sg, gc)) ? 1 : 0;
+            rank += (int)(!f2 & (g2 != gc) & sel::key_less(v, g2, sg, gc));
         }
         return valid && (fg || rank < kk);
     };

@@ -196,28 +196,38 @@ __device__ __forceinline__ float cosine(double dot, double na, double nb) {
 
 // The last workgroup to arrive of arrival group g of listed head li: for every
 // row (u, f, q) the sum of the group's members' partials -- members are the
-// workgroups wi = u * n_cg + cg with wi % kGroups == g, in increasing cg --
-// into the group sums G[li][g][row] (0 where the group has no member in the
-// row's unit).  Loads go out eight at a time.
+// workgroups wi = u * n_cg + cg with wi % kGroups == g, cg = c0, c0 + kGroups,
+// ... -- into the group sums G[li][g][row] (0 where the group has no member in
+// the row's unit).  Four adjacent lanes share a row: lane j of the quad sums
+// members j, j + 4, j + 8, ... in order, loading eight at a time, and the
+// quad adds its four sums as (s0 + s1) + (s2 + s3) -- a fixed order, so
+// every pass over the same members gives the same sum.
 __device__ void group_sum(const ScoreArgs &a, int li, int g) {
     const int blk = a.n_frames * 2, n_rows = a.units * blk;
     const double *part = a.part + (int64_t)li * n_rows * a.n_cg;   // [u][cg][f][q]
     double *G = a.group + ((int64_t)li * kGroups + g) * n_rows;
-    for (int r = threadIdx.x; r < n_rows; r += kThreads) {
+    // n_rows * 4 and kThreads are multiples of 4: a quad is active or
+    // inactive as a whole in every iteration
+    for (int x = threadIdx.x; x < n_rows * 4; x += kThreads) {
+        const int r = x >> 2, j = x & 3;
         const int u = r / blk, rp = r - u * blk;
         const double *p = part + (int64_t)u * a.n_cg * blk + rp;
+        const int c0 = (g - (u * a.n_cg) % kGroups + kGroups) % kGroups;
+        const int nm = c0 < a.n_cg ? (a.n_cg - 1 - c0) / kGroups + 1 : 0;   // members in the unit
         double acc = 0.0;
-        for (int c = (g - (u * a.n_cg) % kGroups + kGroups) % kGroups; c < a.n_cg; c += 8 * kGroups) {
+        for (int k0 = j; k0 < nm; k0 += 4 * 8) {
             double v[8];
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const int cc = c + i * kGroups;
-                v[i] = cc < a.n_cg ? get_shared(p + (int64_t)cc * blk) : 0.0;
+                const int k = k0 + 4 * i;
+                v[i] = k < nm ? get_shared(p + (int64_t)(c0 + k * kGroups) * blk) : 0.0;
             }
 #pragma unroll
             for (int i = 0; i < 8; ++i) acc += v[i];
         }
-        put_shared(G + r, acc);
+        acc += __shfl_xor(acc, 1);
+        acc += __shfl_xor(acc, 2);
+        if (j == 0) put_shared(G + r, acc);
     }
 }
 
@@ -228,6 +238,8 @@ __device__ void finish_head(const ScoreArgs &a, int li, double *T, float *s_scor
                             unsigned char *s_keep) {
     const int tid = threadIdx.x;
     const int h = a.heads.head[li];
+    // the keep rule is read here, its loads overlapping the group sums' loads
+    const sel::Rule rule = sel::rule_of(a, li);
     const int n_rows = a.units * a.n_frames * 2;
     const double *G = a.group + (int64_t)li * kGroups * n_rows;
     // groups 0 .. min(n_wg, kGroups) - 1 have members and wrote every row; the
@@ -276,7 +288,7 @@ __device__ void finish_head(const ScoreArgs &a, int li, double *T, float *s_scor
     }
     if (a.select) {
         __syncthreads();
-        sel::select_from_lds(a, li, h, s_scores, s_forced, s_keep, a.kept_seg, a.kv_len, tid, kThreads);
+        sel::select_from_lds(a, rule, h, s_scores, s_forced, s_keep, a.kept_seg, a.kv_len, tid, kThreads);
     }
 }
 

@@ -24,9 +24,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
     const int li = blockIdx.x;
     const int h = a.heads.head[li];
     const int tid = threadIdx.x;
+    const sel::Rule rule = sel::rule_of(a, li);
     for (int g = tid; g < a.n_seg; g += kThreads) s[g] = a.scores[(int64_t)h * a.score_stride + g];
     __syncthreads();
-    sel::select_from_lds(a, li, h, s, forced, keep, a.kept_seg, a.kv_len, tid, kThreads);
+    sel::select_from_lds(a, rule, h, s, forced, keep, a.kept_seg, a.kv_len, tid, kThreads);
 }
 
 }  // namespace

@@ -15,14 +15,21 @@
 namespace fkv {
 namespace sel {
 
+// The key (isNaN(s), s, g) as one unsigned 64-bit integer whose order is the
+// key's: the high word maps the score's bits monotonically (-0 taken as +0,
+// negative scores bit-inverted, the sign bit set on the others, every NaN
+// 0xffffffff), the low word is the index g >= 0.  Comparing two keys is one
+// integer compare -- no branches or lane-mask logic per candidate.
+__device__ __forceinline__ uint64_t sort_key(float s, int g) {
+    uint32_t b = __float_as_uint(s);
+    b = b == 0x80000000u ? 0u : b;
+    b = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+    b = __builtin_isnan(s) ? 0xffffffffu : b;
+    return ((uint64_t)b << 32) | (uint32_t)g;
+}
+
 __device__ __forceinline__ bool key_less(float sa, int ga, float sb, int gb) {
-    const bool na = __builtin_isnan(sa), nb = __builtin_isnan(sb);
-    if (na != nb) return nb;          // a finite/inf score precedes a NaN
-    if (!na) {
-        if (sa < sb) return true;     // -0 and +0 compare equal here
-        if (sa > sb) return false;
-    }
-    return ga < gb;
+    return sort_key(sa, ga) < sort_key(sb, gb);
 }
 
 // Logical frames [first, last] that segment g covers.  F and L divide one
@@ -40,12 +47,23 @@ __device__ __forceinline__ void seg_frames(const A &a, int g, int *first, int *l
     }
 }
 
+// The keep rule of list entry li: sink and recent frames, selection scope and
+// k.  Read once per selection (each field is a load from the launch
+// arguments), ahead of the work that needs it.
+struct Rule {
+    int sink, recent, scope, k;
+};
+template <class A>
+__device__ __forceinline__ Rule rule_of(const A &a, int li) {
+    return Rule{a.sink[li], a.recent[li], a.scope[li], a.k[li]};
+}
+
 // Does segment g intersect logical frames [0, sink) or [H - recent, H)?
 template <class A>
-__device__ __forceinline__ bool is_forced(const A &a, int li, int g) {
+__device__ __forceinline__ bool is_forced(const A &a, const Rule &r, int g) {
     int first, last;
     seg_frames(a, g, &first, &last);
-    return first < a.sink[li] || last >= a.H - a.recent[li];
+    return first < r.sink || last >= a.H - r.recent;
 }
 
 // Tokens of segment g (only the last segment of the history can be short).
@@ -57,44 +75,65 @@ __device__ __forceinline__ int seg_tokens(const A &a, int g) {
     return (last - first + 1) * a.F;
 }
 
-// The helpers take any argument block with the fields F, L, H, n_seg and the
-// per-list-entry arrays sink, recent, scope and k (SelectArgs, ScoreArgs).
+// The helpers take any argument block with the fields F, L, H and n_seg (and,
+// for rule_of, the per-list-entry arrays sink, recent, scope and k):
+// SelectArgs, SelectCopyArgs, ScoreArgs.
 
 // Keep decision of a non-forced segment g with score sg, given the scores s[]
 // and forced flags of all n_seg segments (in LDS): its rank inside its group
 // (one frame's segments for FKV_SCOPE_FRAME, all segments otherwise) is below
 // kk.
 template <class A>
-__device__ __forceinline__ bool keep_by_rank(const A &a, int li, const float *s,
+__device__ __forceinline__ bool keep_by_rank(const A &a, const Rule &r, const float *s,
                                              const unsigned char *forced, int g) {
     int lo = 0, hi = a.n_seg;
-    if (a.scope[li] == FKV_SCOPE_FRAME) {
+    if (r.scope == FKV_SCOPE_FRAME) {
         const int spf = a.F / a.L;
         lo = (g / spf) * spf;
         hi = lo + spf;
     }
-    const int kk = a.k[li];
-    const float sg = s[g];
+    const int kk = r.k;
+    const uint64_t kg = sort_key(s[g], g);
     int rank = 0;
-    for (int g2 = lo; g2 < hi && rank < kk; ++g2)
-        rank += (!forced[g2] && g2 != g && key_less(s[g2], g2, sg, g)) ? 1 : 0;
+    // eight candidates per step, their LDS reads issued together (one read
+    // latency per step rather than per candidate); indices past the group
+    // are clamped to its last member and, like forced segments, not counted
+    // (g itself never counts: its key equals kg)
+    for (int g0 = lo; g0 < hi && rank < kk; g0 += 8) {
+        float sv[8];
+        unsigned char fv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int g2 = min(g0 + i, hi - 1);
+            sv[i] = s[g2];
+            fv[i] = forced[g2];
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int g2 = g0 + i;
+            const uint64_t key = sort_key(sv[i], g2);
+            const bool counts = (g2 < hi) & (fv[i] == 0);
+            rank += (int)(counts & (key < kg));
+        }
+    }
     return rank < kk;
 }
 
-// One workgroup decides head h's keep set from its scores s[0..n_seg) in LDS
-// and writes kept_seg[h] (ascending, -1 padded) and kv_len[h].  forced and
-// keep are LDS scratch of n_seg bytes.  Every thread of the workgroup calls
-// it (it contains barriers); nthreads is the workgroup size.
+// One workgroup decides head h's keep set (rule r) from its scores
+// s[0..n_seg) in LDS and writes kept_seg[h] (ascending, -1 padded) and
+// kv_len[h].  forced and keep are LDS scratch of n_seg bytes.  Every thread
+// of the workgroup calls it (it contains barriers); nthreads is the workgroup
+// size.
 template <class A>
-__device__ __forceinline__ void select_from_lds(const A &a, int li, int h, const float *s,
+__device__ __forceinline__ void select_from_lds(const A &a, const Rule &r, int h, const float *s,
                                                 unsigned char *forced, unsigned char *keep,
                                                 int32_t *kept_seg, int32_t *kv_len, int tid,
                                                 int nthreads) {
     const int n = a.n_seg;
-    for (int g = tid; g < n; g += nthreads) forced[g] = is_forced(a, li, g) ? 1 : 0;
+    for (int g = tid; g < n; g += nthreads) forced[g] = is_forced(a, r, g) ? 1 : 0;
     __syncthreads();
     for (int g = tid; g < n; g += nthreads)
-        keep[g] = (forced[g] || keep_by_rank(a, li, s, forced, g)) ? 1 : 0;
+        keep[g] = (forced[g] || keep_by_rank(a, r, s, forced, g)) ? 1 : 0;
     __syncthreads();
     if (tid < 64) {
         int base = 0;
