@@ -49,6 +49,7 @@
 // schedule uneven (at 480P a dynamic head has 342 key tiles per query tile, a
 // static head 245, on 228 items for 256 CUs).
 #include "attn_common.h"
+#include "handover.h"
 
 namespace fkv {
 namespace {
@@ -322,27 +323,13 @@ __device__ __forceinline__ void mfma_block(const uint16_t *vs, const uint16_t *k
     }
 }
 
-// Values another workgroup of the same launch reads (the parts of a cut
-// item) are written and read with device-scope accesses (sc1: coherent across
-// the XCDs' L2 caches for that location); no cache write-back or invalidation
-// is needed, which agent-scope fences would do to the whole L2 of the XCD.
-__device__ __forceinline__ void put_shared(unsigned long long *p, uint2 v) {
-    __hip_atomic_store(p, ((unsigned long long)v.y << 32) | v.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void put_shared(float *p, float v) {
-    __hip_atomic_store((uint32_t *)p, __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-template <bool SHARED>
-__device__ __forceinline__ uint2 get_part(const uint2 *p) {
-    if (!SHARED) return *p;
-    const unsigned long long v =
-        __hip_atomic_load((unsigned long long *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
-}
-template <bool SHARED>
-__device__ __forceinline__ float get_part(const float *p) {
-    if (!SHARED) return *p;
-    return __uint_as_float(__hip_atomic_load((uint32_t *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+// The parts of a cut item are written with device-scope stores (handover.h);
+// the merge reads them with device-scope loads when they were written in the
+// same launch (SHARED), plainly after a kernel boundary.
+template <bool SHARED, class T>
+__device__ __forceinline__ T get_part(const T *p) {
+    if constexpr (SHARED) return get_shared(p);
+    else return *p;
 }
 
 // Combines the parts of a cut item (list entry li, query tile qt; first tile
@@ -398,22 +385,6 @@ __device__ __forceinline__ void merge_rows(const AttnArgs &a, const Schedule &sc
         *(uint2 *)((uint16_t *)a.O + ((size_t)h * a.Lq + qrow) * D + d0) =
             pack_bf16x4(x[i][0] * inv, x[i][1] * inv, x[i][2] * inv, x[i][3] * inv);
     }
-}
-
-// Arrival of a workgroup on a device-scope counter, once every wave's
-// device-scope stores have completed; true in every thread of the workgroup
-// that arrives last (which resets the counter to zero for the next call).
-__device__ __forceinline__ bool arrive_last(uint32_t *counter, uint32_t expected, uint32_t *flag) {
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const uint32_t old = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const bool last = old + 1 == expected;
-        if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        *flag = last ? 1u : 0u;
-    }
-    __syncthreads();
-    return *flag != 0;
 }
 
 // One segment: positions [t0, t1) of item (h, qt), where position j is key

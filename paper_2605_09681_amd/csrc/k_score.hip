@@ -45,7 +45,10 @@
 // before the cosine.
 //
 // The counters live at the start of the workspace; the caller zero-fills the
-// workspace once and every call returns the counters to zero.
+// workspace once and every call returns the counters to zero.  Partials and
+// sums pass between workgroups through device-scope stores and loads
+// (handover.h).
+#include "handover.h"
 #include "select_common.h"
 
 namespace fkv {
@@ -136,19 +139,6 @@ __device__ __forceinline__ double lane_sq(const u32x4 (&a)[kV]) {
             acc = fma(x, x, acc);
         }
     return acc;
-}
-
-// Values other workgroups read within this launch (partials, per-head sums)
-// are written and read with device-scope accesses (sc1: coherent across the
-// XCDs' L2 caches for that location), so the hand-over needs no cache
-// write-back or invalidation: a generic agent-scope release fence writes back
-// the whole L2 of the XCD (measured ~1 us, serialised per XCD, when every
-// workgroup does it).
-__device__ __forceinline__ void put_shared(double *p, double v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ double get_shared(const double *p) {
-    return __hip_atomic_load(const_cast<double *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Partial row of (unit u, streamed frame f, quantity q: 0 = SQ, 1 = DOT).
@@ -310,24 +300,6 @@ __device__ void finish_pooled(const ScoreArgs &a) {
         }
         a.scores[g] = cosine(dot, na, nb);
     }
-}
-
-// Arrival on a device-scope counter; true in every thread of the workgroup
-// that arrives last (the counter is then reset to zero for the next call).
-// Every wave first waits until its device-scope stores have completed, so the
-// last arrival sees all of them (and, through a chain of arrivals, everything
-// the earlier arrivals saw).
-__device__ __forceinline__ bool arrive_last(uint32_t *counter, uint32_t expected, uint32_t *flag) {
-    __builtin_amdgcn_s_waitcnt(0);   // this wave's stores (vmcnt), LDS and scalar accesses complete
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const uint32_t old = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const bool last = old + 1 == expected;
-        if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        *flag = last ? 1u : 0u;
-    }
-    __syncthreads();
-    return *flag != 0;
 }
 
 template <bool F32>
