@@ -898,11 +898,18 @@ def cpu_baseline_1080p(rows_per_head):
             "measured_s": round(t2 - t0, 2)}
 
 
+# the sources the attention kernel is compiled from
+ATTN_SOURCES = ("k_attn.hip", "attn_common.h", "handover.h")
+
+
 def _kernel_sha():
+    """sha256 (first 16 hex digits) over the attention kernel's sources, in order."""
     import hashlib
-    p = os.path.join(ROOT, "paper_2605_09681_amd", "csrc", "k_attn.hip")
-    with open(p, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name in ATTN_SOURCES:
+        with open(os.path.join(ROOT, "paper_2605_09681_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 if __name__ == "__main__":
