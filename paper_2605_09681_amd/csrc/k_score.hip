@@ -224,8 +224,8 @@ __device__ void group_sum(const ScoreArgs &a, int li, int g) {
 // The last workgroup of listed head li: the head's per-row sums T (LDS,
 // lds_rows doubles) from the group sums, groups in order, then the finish by
 // mode.
-__device__ void finish_head(const ScoreArgs &a, int li, double *T, float *s_scores, unsigned char *s_forced,
-                            unsigned char *s_keep) {
+__device__ void finish_head(const ScoreArgs &a, int li, double *T, uint64_t *s_keys, float *s_scores,
+                            unsigned char *s_forced, unsigned char *s_keep) {
     const int tid = threadIdx.x;
     const int h = a.heads.head[li];
     // the keep rule is read here, its loads overlapping the group sums' loads
@@ -278,7 +278,7 @@ __device__ void finish_head(const ScoreArgs &a, int li, double *T, float *s_scor
     }
     if (a.select) {
         __syncthreads();
-        sel::select_from_lds(a, rule, h, s_scores, s_forced, s_keep, a.kept_seg, a.kv_len, tid, kThreads);
+        sel::select_from_lds(a, rule, h, s_scores, s_keys, s_forced, s_keep, a.kept_seg, a.kv_len, tid, kThreads);
     }
 }
 
@@ -305,7 +305,7 @@ __device__ void finish_pooled(const ScoreArgs &a) {
 template <bool F32>
 __global__ __launch_bounds__(kThreads, 5) void score_kernel(ScoreArgs a) {
     extern __shared__ double dyn[];            // finisher rows (lds_rows), this workgroup's sums (2 n_frames),
-                                               // then n_seg floats + 2 n_seg bytes
+                                               // then (selecting) n_seg keys, n_seg floats, 2 n_seg bytes
     __shared__ u32x4 edge[kWaves][kV][64];     // first frame of each wave's run
     __shared__ uint32_t flag;
 
@@ -382,9 +382,10 @@ __global__ __launch_bounds__(kThreads, 5) void score_kernel(ScoreArgs a) {
     group_sum(a, li, g1);
     if (!arrive_last(cnt + kGroups * kCounterStride, (uint32_t)min(n_wg, kGroups), &flag)) return;
     double *T = dyn;
-    float *s_scores = (float *)(dyn + a.lds_rows + nf * 2);
+    uint64_t *s_keys = (uint64_t *)(dyn + a.lds_rows + nf * 2);
+    float *s_scores = (float *)(s_keys + a.n_seg);
     unsigned char *s_forced = (unsigned char *)(s_scores + a.n_seg);
-    finish_head(a, li, T, s_scores, s_forced, s_forced + a.n_seg);
+    finish_head(a, li, T, s_keys, s_scores, s_forced, s_forced + a.n_seg);
     if (a.pooled && a.mode != kScoreModeHistory) {
         uint32_t *pc = a.counters + (int64_t)a.heads.n * kCountersPerHead * kCounterStride;
         if (!arrive_last(pc, (uint32_t)a.heads.n, &flag)) return;
@@ -419,7 +420,7 @@ hipError_t launch_score(const ScoreArgs &a0, bool f32, hipStream_t s) {
     if (a.heads.n == 0 || a.n_frames <= 0) return hipSuccess;
     a.lds_rows = a.units * a.n_frames * 2;
     size_t lds = (size_t)(a.lds_rows + a.n_frames * 2) * sizeof(double);   // + this workgroup's sums
-    if (a.select) lds += (size_t)a.n_seg * (sizeof(float) + 2);
+    if (a.select) lds += (size_t)a.n_seg * (sizeof(uint64_t) + sizeof(float) + 2);
     lds = (lds + 15) & ~(size_t)15;
     const dim3 grid((unsigned)a.n_cg, (unsigned)a.units, (unsigned)a.heads.n);
     if (f32)

@@ -17,6 +17,7 @@ namespace {
 constexpr int kThreads = 256;
 
 __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
+    __shared__ uint64_t keys[FKV_MAX_SEGMENTS];
     __shared__ float s[FKV_MAX_SEGMENTS];
     __shared__ unsigned char keep[FKV_MAX_SEGMENTS];
     __shared__ unsigned char forced[FKV_MAX_SEGMENTS];
@@ -27,7 +28,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a) {
     const sel::Rule rule = sel::rule_of(a, li);
     for (int g = tid; g < a.n_seg; g += kThreads) s[g] = a.scores[(int64_t)h * a.score_stride + g];
     __syncthreads();
-    sel::select_from_lds(a, rule, h, s, forced, keep, a.kept_seg, a.kv_len, tid, kThreads);
+    sel::select_from_lds(a, rule, h, s, keys, forced, keep, a.kept_seg, a.kv_len, tid, kThreads);
 }
 
 }  // namespace

@@ -79,13 +79,12 @@ __device__ __forceinline__ int seg_tokens(const A &a, int g) {
 // for rule_of, the per-list-entry arrays sink, recent, scope and k):
 // SelectArgs, SelectCopyArgs, ScoreArgs.
 
-// Keep decision of a non-forced segment g with score sg, given the scores s[]
-// and forced flags of all n_seg segments (in LDS): its rank inside its group
-// (one frame's segments for FKV_SCOPE_FRAME, all segments otherwise) is below
-// kk.
+// Keep decision of a non-forced segment g, given the keys of all n_seg
+// segments in LDS (sort_key, the largest key for a forced segment): its rank
+// inside its group (one frame's segments for FKV_SCOPE_FRAME, all segments
+// otherwise) is below kk.
 template <class A>
-__device__ __forceinline__ bool keep_by_rank(const A &a, const Rule &r, const float *s,
-                                             const unsigned char *forced, int g) {
+__device__ __forceinline__ bool keep_by_rank(const A &a, const Rule &r, const uint64_t *keys, int g) {
     int lo = 0, hi = a.n_seg;
     if (r.scope == FKV_SCOPE_FRAME) {
         const int spf = a.F / a.L;
@@ -93,47 +92,41 @@ __device__ __forceinline__ bool keep_by_rank(const A &a, const Rule &r, const fl
         hi = lo + spf;
     }
     const int kk = r.k;
-    const uint64_t kg = sort_key(s[g], g);
+    const uint64_t kg = keys[g];
     int rank = 0;
     // eight candidates per step, their LDS reads issued together (one read
-    // latency per step rather than per candidate); indices past the group
-    // are clamped to its last member and, like forced segments, not counted
-    // (g itself never counts: its key equals kg)
+    // latency per step rather than per candidate); indices past the group are
+    // clamped to its last member and not counted.  Neither g itself (equal
+    // key) nor a forced segment (largest key) precedes g.
     for (int g0 = lo; g0 < hi && rank < kk; g0 += 8) {
-        float sv[8];
-        unsigned char fv[8];
+        uint64_t kv[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int g2 = min(g0 + i, hi - 1);
-            sv[i] = s[g2];
-            fv[i] = forced[g2];
-        }
+        for (int i = 0; i < 8; ++i) kv[i] = keys[min(g0 + i, hi - 1)];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int g2 = g0 + i;
-            const uint64_t key = sort_key(sv[i], g2);
-            const bool counts = (g2 < hi) & (fv[i] == 0);
-            rank += (int)(counts & (key < kg));
-        }
+        for (int i = 0; i < 8; ++i) rank += (int)((g0 + i < hi) & (kv[i] < kg));
     }
     return rank < kk;
 }
 
 // One workgroup decides head h's keep set (rule r) from its scores
 // s[0..n_seg) in LDS and writes kept_seg[h] (ascending, -1 padded) and
-// kv_len[h].  forced and keep are LDS scratch of n_seg bytes.  Every thread
-// of the workgroup calls it (it contains barriers); nthreads is the workgroup
-// size.
+// kv_len[h].  keys (n_seg), forced and keep (n_seg bytes each) are LDS
+// scratch.  Every thread of the workgroup calls it (it contains barriers);
+// nthreads is the workgroup size.
 template <class A>
 __device__ __forceinline__ void select_from_lds(const A &a, const Rule &r, int h, const float *s,
-                                                unsigned char *forced, unsigned char *keep,
+                                                uint64_t *keys, unsigned char *forced, unsigned char *keep,
                                                 int32_t *kept_seg, int32_t *kv_len, int tid,
                                                 int nthreads) {
     const int n = a.n_seg;
-    for (int g = tid; g < n; g += nthreads) forced[g] = is_forced(a, r, g) ? 1 : 0;
+    for (int g = tid; g < n; g += nthreads) {
+        const bool f = is_forced(a, r, g);
+        forced[g] = f ? 1 : 0;
+        keys[g] = f ? ~0ull : sort_key(s[g], g);
+    }
     __syncthreads();
     for (int g = tid; g < n; g += nthreads)
-        keep[g] = (forced[g] || keep_by_rank(a, r, s, forced, g)) ? 1 : 0;
+        keep[g] = (forced[g] || keep_by_rank(a, r, keys, g)) ? 1 : 0;
     __syncthreads();
     if (tid < 64) {
         int base = 0;
