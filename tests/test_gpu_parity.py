@@ -413,7 +413,8 @@ def test_select_crafted_scores(F, L, H):
     x = W.make_layer_inputs(cfg, seed=10)
     n = H * F // L
     rng = np.random.default_rng(10)
-    palette = np.array([0.5, 0.0, -0.0, np.nan, 0.25, 0.5, -1.0, np.inf, -np.inf], np.float32)
+    # NaNs of both signs (the sign bit must not order them), signed zeros, infinities
+    palette = np.array([0.5, 0.0, -0.0, np.nan, -np.nan, 0.25, 0.5, -1.0, np.inf, -np.inf], np.float32)
     scores = palette[rng.integers(0, len(palette), (4, n))].astype(np.float32)
     scores[0] = 0.75                                    # all equal
     layer = make_layer(cfg)

@@ -402,7 +402,7 @@ def _brute_select(scores, H, F, L, sink, recent, k, scope):
                                        (W.SCOPE_GLOBAL, 6, 2)])
 def test_select_brute_force(oracle_lib, scope, F, L):
     rng = np.random.default_rng(0)
-    palette = np.array([0.5, -0.0, 0.0, 0.25, np.nan, -1.0, 0.5, 1.0], np.float32)
+    palette = np.array([0.5, -0.0, 0.0, 0.25, np.nan, -1.0, 0.5, 1.0, -np.nan], np.float32)
     for trial in range(60):
         H = int(rng.integers(1, 6))
         n = -(-H * F // L)
@@ -428,6 +428,10 @@ def test_select_crafted(oracle_lib):
     assert kept[:cnt].tolist() == [1, 3, 4, 5]        # NaN evicted first
     kept, cnt = oracle.select_head(nan, H, F, L, 0, 0, 5, W.SCOPE_GLOBAL)
     assert kept[:cnt].tolist() == [0, 1, 3, 4, 5]     # then NaN by index
+    signed = np.array([np.nan, 0.9, -np.nan, 0.1, 0.5, 0.2], np.float32)
+    assert np.signbit(signed[2]) and not np.signbit(signed[0])
+    kept, cnt = oracle.select_head(signed, H, F, L, 0, 0, 5, W.SCOPE_GLOBAL)
+    assert kept[:cnt].tolist() == [0, 1, 3, 4, 5]     # the NaN's sign does not order it
     low = np.array([0.9, 0.1, 0.8, 0.2, 0.7, 0.3], np.float32)
     kept, cnt = oracle.select_head(low, H, F, L, 1, 1, 2, W.SCOPE_GLOBAL)
     assert kept[:cnt].tolist() == [0, 1, 3, 5]        # sink 0, recent 5, two least similar
