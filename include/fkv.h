@@ -300,9 +300,10 @@ fkv_status fkv_attention_workspace_size(const fkv_shape *shape, size_t *bytes);
  * zero again), the key tiles of all heads and query tiles are split evenly
  * over one workgroup per compute unit, and the parts of a tile cut by a split
  * are combined by the workgroup that completes the last of them
- * (FKV_ERR_CAPACITY if the workspace is smaller).  Both schedules compute the same function; a split
- * tile's parts are normalised and rounded to bf16 before they are combined, so
- * its output may differ from the one-workgroup result by about one bf16 step.
+ * (FKV_ERR_CAPACITY if the workspace is smaller).  Both schedules compute the
+ * same function; a split tile's parts are normalised and rounded to bf16
+ * before they are combined, so its output may differ from the one-workgroup
+ * result by about one bf16 step.
  * fp32 ignores the workspace.  Two calls that share a workspace must be
  * ordered by the caller. */
 fkv_status fkv_chunk_attention(const fkv_shape *shape, const void *Q,
