@@ -17,14 +17,14 @@
 // Streaming.  Workgroup (cg, u, li) owns column group cg -- 2 x 64 adjacent
 // 16-byte vectors -- of unit u of listed head li, and streams those columns of
 // every frame once: its four waves split the frames into four contiguous
-// runs, every lane loads up to six frames of its run at once,
+// runs, every lane loads two frames of its run at once,
 // so no key byte is read twice and every load is a full 1 KB-per-wave
-// coalesced access.  A lane accumulates, per frame, its columns' squares and
-// products with the previous frame (vector 0 then vector 1, elements in
-// order); the wave reduces each sum over its 64 lanes with DPP row scans in a
-// fixed order and writes one partial per (frame, column group).  The product
-// across a run boundary uses the next run's first frame, which its wave
-// leaves in LDS.
+// coalesced access.  A lane widens each frame's elements to fp64 once and
+// accumulates, per frame, its columns' squares and products with the previous
+// frame's widened elements (vector 0 then vector 1, elements in order); the
+// wave reduces each sum over its 64 lanes with DPP row scans in a fixed order
+// and writes one partial per (frame, column group).  The product across a run
+// boundary uses the next run's first frame, which its wave leaves in LDS.
 //
 // Finish.  Each workgroup stores its per-frame sums as one block and arrives
 // on one of its head's kGroups first-level counters (device-scope stores,
@@ -58,10 +58,11 @@ constexpr int kThreads = kScoreThreads;  // 4 waves
 constexpr int kWaves = kScoreWaves;
 constexpr int kV = 2;                    // 16-byte vectors per lane and frame
 constexpr int kCols = 64 * kV;           // vectors (columns) per workgroup
-// Frames a lane loads at once: the whole run of a 22-frame (480P) pass,
-// within 96 VGPRs (five waves per SIMD, every workgroup of a 480P layer
-// resident at once).
-template <bool F32> constexpr int kMaxF = 4;
+// Frames a lane loads at once, next to the widened current and previous frame
+// (32 + 32 VGPRs for bf16), within 96 VGPRs: five waves per SIMD, so every
+// workgroup of a 480P layer is resident at once.  (Four frames at once with
+// each element widened where it is used measured 7% slower at 480P.)
+constexpr int kMaxF = 2;
 // Arrival counters: device-scope atomics on one address serialise at the
 // memory side, so each counter has a 256-byte line of its own and a head's
 // workgroups arrive in two levels -- kGroups first-level counters (workgroup
@@ -113,33 +114,35 @@ struct Vec<true> {  // 4 fp32
     __device__ static __forceinline__ double at(const u32x4 &v, int e) { return (double)__uint_as_float(v[e]); }
 };
 
-// Sum over the lane's columns of a*b, vector 0 then vector 1, elements in
-// order; each element is widened where it is used, so only the loaded 16-byte
-// vectors occupy registers (six frames of them in flight).
+// A lane's columns of one frame widened to fp64 (exact), vector 0 then vector
+// 1, elements in order: each element is converted once, and the frame serves
+// as the current frame (its squares, its product with the previous frame) and
+// then as the previous frame of the next.
 template <bool F32>
-__device__ __forceinline__ double lane_dot(const u32x4 (&a)[kV], const u32x4 (&b)[kV]) {
-    using V = Vec<F32>;
-    double acc = 0.0;
+struct Wide {
+    static constexpr int N = kV * Vec<F32>::N;
+    double v[N];
+    __device__ __forceinline__ void set(const u32x4 (&x)[kV]) {
 #pragma unroll
-    for (int j = 0; j < kV; ++j)
+        for (int j = 0; j < kV; ++j)
 #pragma unroll
-        for (int e = 0; e < V::N; ++e) acc = fma(V::at(a[j], e), V::at(b[j], e), acc);
-    return acc;
-}
-
-template <bool F32>
-__device__ __forceinline__ double lane_sq(const u32x4 (&a)[kV]) {
-    using V = Vec<F32>;
-    double acc = 0.0;
+            for (int e = 0; e < Vec<F32>::N; ++e) v[j * Vec<F32>::N + e] = Vec<F32>::at(x[j], e);
+    }
+    // sum of squares, elements in order
+    __device__ __forceinline__ double sq() const {
+        double acc = 0.0;
 #pragma unroll
-    for (int j = 0; j < kV; ++j)
+        for (int k = 0; k < N; ++k) acc = fma(v[k], v[k], acc);
+        return acc;
+    }
+    // sum of products with frame b, elements in order
+    __device__ __forceinline__ double dot(const Wide &b) const {
+        double acc = 0.0;
 #pragma unroll
-        for (int e = 0; e < V::N; ++e) {
-            const double x = V::at(a[j], e);
-            acc = fma(x, x, acc);
-        }
-    return acc;
-}
+        for (int k = 0; k < N; ++k) acc = fma(v[k], b.v[k], acc);
+        return acc;
+    }
+};
 
 // Partial row of (unit u, streamed frame f, quantity q: 0 = SQ, 1 = DOT).
 __device__ __forceinline__ int row_of(const ScoreArgs &a, int u, int f, int q) {
@@ -338,8 +341,8 @@ __global__ __launch_bounds__(kThreads, 5) void score_kernel(ScoreArgs a) {
         if (lane == 63) wg_part[f * 2 + q] = v;
     };
 
-    u32x4 prev[kV] = {};
-    constexpr int MF = kMaxF<F32>;
+    Wide<F32> prev{};
+    constexpr int MF = kMaxF;
     for (int f0 = fa; f0 < fb; f0 += MF) {
         const int nb = min(MF, fb - f0);
         u32x4 x[MF][kV];
@@ -354,10 +357,11 @@ __global__ __launch_bounds__(kThreads, 5) void score_kernel(ScoreArgs a) {
         for (int i = 0; i < MF; ++i) {
             if (i < nb) {
                 const int f = f0 + i;
-                put(f, 0, wave_sum(lane_sq<F32>(x[i])));
-                if (f > fa) put(f - 1, 1, wave_sum(lane_dot<F32>(prev, x[i])));
-#pragma unroll
-                for (int j = 0; j < kV; ++j) prev[j] = x[i][j];
+                Wide<F32> cur;
+                cur.set(x[i]);
+                put(f, 0, wave_sum(cur.sq()));
+                if (f > fa) put(f - 1, 1, wave_sum(prev.dot(cur)));
+                prev = cur;
             }
         }
     }
@@ -367,7 +371,9 @@ __global__ __launch_bounds__(kThreads, 5) void score_kernel(ScoreArgs a) {
         u32x4 nx[kV];
 #pragma unroll
         for (int j = 0; j < kV; ++j) nx[j] = edge[w + 1][j][lane];
-        put(fb - 1, 1, wave_sum(lane_dot<F32>(prev, nx)));
+        Wide<F32> next;
+        next.set(nx);
+        put(fb - 1, 1, wave_sum(prev.dot(next)));
     }
 
     __syncthreads();
