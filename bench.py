@@ -62,7 +62,7 @@ def parse():
                    help="serial units of the per-stage pass ahead of the timed steps")
     p.add_argument("--cpu-rows", type=int, default=4680,
                    help="query rows per head in the 480P CPU oracle sample (4680 = every row)")
-    p.add_argument("--cpu-rows-1080p", type=int, default=512,
+    p.add_argument("--cpu-rows-1080p", type=int, default=2048,
                    help="query rows per head in the 1080P CPU oracle sample (extrapolated to 24480)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--step", default="paged", choices=["paged", "paged2", "compact", "serial"],
@@ -899,7 +899,7 @@ def cpu_baseline_1080p(rows_per_head):
 
 
 # the sources the attention kernel is compiled from
-ATTN_SOURCES = ("k_attn.hip", "attn_common.h", "handover.h")
+ATTN_SOURCES = ("k_attn.hip", "attn_common.h", "attn_merge.h", "handover.h")
 
 
 def _kernel_sha():

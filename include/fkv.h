@@ -458,7 +458,9 @@ fkv_status fkv_classify_heads(const float *mass, int32_t n_heads, int32_t n_bins
  * the value product; the normaliser sums the same rounded probabilities.
  * O is bf16 [n_heads][C*F][d]; lse as in fkv_chunk_attention.  The workspace
  * selects the balanced schedule exactly as in fkv_chunk_attention (same size
- * query, fkv_attention_workspace_size). */
+ * query, fkv_attention_workspace_size; zero-filled before its first use, its
+ * counters left at zero by every call; cut items are combined by the
+ * workgroup whose part completes last). */
 fkv_status fkv_fp8_sizes(const fkv_shape *shape, int32_t slab, size_t *q_bytes,
                          size_t *kv_bytes, size_t *scale_bytes,
                          size_t *workspace_bytes);

@@ -42,9 +42,9 @@ __device__ __forceinline__ int entry_tiles(const AttnArgs &a, int li) {
 // T_h key tiles; concatenating all items gives one sequence of `total` tiles,
 // which G = min(n_blocks, total) workgroups split into equal contiguous ranges:
 // workgroup r takes tiles [r*total/G, (r+1)*total/G).  An item cut by a range
-// boundary is computed in parts whose results are combined afterwards (by the
-// workgroup completing the last part in the bf16 kernel, by attn_merge_kernel
-// after the FP8 kernel).  Every kernel derives the same schedule from kv_len.
+// boundary is computed in parts whose results are combined by the workgroup
+// completing the last of them (attn_merge.h).  Every kernel derives the same
+// schedule from kv_len.
 struct Schedule {
     int64_t total;
     int G;
@@ -141,10 +141,4 @@ __device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v 
 __device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 
 }  // namespace attn
-
-// Combines the partial results of the items the balanced schedule split, in a
-// second kernel on the same stream (the FP8 path; the bf16 kernel merges them
-// itself).
-hipError_t launch_attention_merge(const AttnArgs &a, int head_dim, hipStream_t s);
-
 }  // namespace fkv

@@ -1075,7 +1075,7 @@ fkv_status fkv_chunk_attention_fp8(const fkv_shape *shape, const void *Q8, const
     int blocks = 0;
     if (workspace) {
         if ((st = balanced_blocks(&blocks)) != FKV_OK) return st;
-        const size_t need = 2 * (size_t)blocks * fkv::attention_part_bytes(shape->head_dim);
+        const size_t need = attention_workspace_bytes(shape, blocks);
         if (workspace_bytes < need)
             return fail(FKV_ERR_CAPACITY, "attention workspace of %zu bytes, %zu needed", workspace_bytes, need);
     }
@@ -1098,6 +1098,8 @@ fkv_status fkv_chunk_attention_fp8(const fkv_shape *shape, const void *Q8, const
     a.items_per_xcd = (a.n_items + 7) / 8;
     a.n_blocks = blocks;
     a.part = (float *)workspace;
+    if (workspace)
+        a.item_counters = (uint32_t *)((char *)workspace + 2 * (size_t)blocks * fkv::attention_part_bytes(shape->head_dim));
     a.fp8_scales = scales;
     a.fp8_rows = ((int64_t)slab + a.Lq + 63) / 64 * 64;
     (void)hipGetLastError();

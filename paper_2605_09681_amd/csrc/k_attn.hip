@@ -49,6 +49,7 @@
 // schedule uneven (at 480P a dynamic head has 342 key tiles per query tile, a
 // static head 245, on 228 items for 256 CUs).
 #include "attn_common.h"
+#include "attn_merge.h"
 #include "handover.h"
 
 namespace fkv {
@@ -320,70 +321,6 @@ __device__ __forceinline__ void mfma_block(const uint16_t *vs, const uint16_t *k
     for (int st = 0; st < NSTEP; ++st) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         if (st + kPrefetch < NSTEP) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-}
-
-// The parts of a cut item are written with device-scope stores (handover.h);
-// the merge reads them with device-scope loads when they were written in the
-// same launch (SHARED), plainly after a kernel boundary.
-template <bool SHARED, class T>
-__device__ __forceinline__ T get_part(const T *p) {
-    if constexpr (SHARED) return get_shared(p);
-    else return *p;
-}
-
-// Combines the parts of a cut item (list entry li, query tile qt; first tile
-// ibase of the concatenated sequence, T tiles), for the 32 rows of wave block
-// w.  With part maxima m_j, sums l_j and normalised outputs o_j of a row,
-//   M = max_j m_j,  w_j = 2^(m_j - M) l_j,  L = sum_j w_j,  O = sum_j w_j o_j / L,
-// and lse = ln 2 * M + ln L, the parts taken in schedule order.  Thread t of
-// the NT that share the block handles row t % 32 and the block's uint2
-// elements i * NT + t -- every element gets the same arithmetic whichever
-// thread does it.  SHARED: the parts were written in this launch.
-template <int D, bool SHARED, int NT>
-__device__ __forceinline__ void merge_rows(const AttnArgs &a, const Schedule &sc, int li, int qt, int64_t ibase,
-                                           int T, int w, int t) {
-    using C = Cfg<D>;
-    constexpr int kML = BM * D / 2;        // float offset of m within a slot
-    constexpr int kVecs = C::MB * 4 * 64;  // uint2s (4 values) of one wave block's accumulators
-    constexpr int kPer = kVecs / NT;
-    const int h = a.heads.head[li];
-    const int b0 = sc.owner(ibase), b1 = sc.owner(ibase + T - 1);
-    // the item is b0's last segment unless b0's range starts with it, and the
-    // first segment of every later workgroup up to b1
-    const int s0 = sc.start(b0) == ibase ? 2 * b0 : 2 * b0 + 1;
-    const int r = t & 31, row = w * 32 + r;
-    const int qrow = qt * BM + row;
-    float M = -__builtin_inff(), L = 0.f;
-    float x[kPer][4] = {};
-    for (int b = b0; b <= b1; ++b) {
-        const float *p = a.part + (size_t)(b == b0 ? s0 : 2 * b) * slot_floats<D>();
-        const float m = get_part<SHARED>(p + kML + row), l = get_part<SHARED>(p + kML + BM + row);
-        uint2 v[kPer];
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) v[i] = get_part<SHARED>((const uint2 *)p + (size_t)w * kVecs + i * NT + t);
-        const float Mn = fmaxf(M, m);
-        const float s = __builtin_amdgcn_exp2f(M - Mn), wg = __builtin_amdgcn_exp2f(m - Mn) * l;
-        M = Mn;
-        L = L * s + wg;
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-            x[i][0] = x[i][0] * s + wg * bf16_lo(v[i].x);
-            x[i][1] = x[i][1] * s + wg * bf16_hi(v[i].x);
-            x[i][2] = x[i][2] * s + wg * bf16_lo(v[i].y);
-            x[i][3] = x[i][3] * s + wg * bf16_hi(v[i].y);
-        }
-    }
-    if (qrow >= a.Lq) return;
-    if (a.lse && t < 32) a.lse[(size_t)h * a.Lq + qrow] = fmaf(M, 0.69314718055994530942f, logf(L));
-    const float inv = 1.f / L;
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-        const int q = i * NT + t;
-        const int mb = q / (4 * 64), g = (q / 64) % 4;
-        const int d0 = 32 * mb + 8 * g + 4 * ((t & 63) >> 5);
-        *(uint2 *)((uint16_t *)a.O + ((size_t)h * a.Lq + qrow) * D + d0) =
-            pack_bf16x4(x[i][0] * inv, x[i][1] * inv, x[i][2] * inv, x[i][3] * inv);
     }
 }
 
@@ -761,27 +698,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnArgs a) {
             const int n_parts = sc.owner(ibase + T - 1) - sc.owner(ibase) + 1;
             uint32_t *cnt = a.item_counters + (size_t)(ip.li * a.n_qtiles + qt) * kItemCounterStride;
             if (arrive_last(cnt, (uint32_t)n_parts, &flag))
-                merge_rows<D, true, 64>(a, sc, ip.li, qt, ibase, T, threadIdx.x >> 6, threadIdx.x & 63);
+                merge_rows<D, 64>(a, sc, ip.li, qt, ibase, T, threadIdx.x >> 6, threadIdx.x & 63);
         }
         cur = ibase + t1;
         first = false;
     }
-}
-
-// Combines the parts of every item the balanced schedule split, in a second
-// kernel (the FP8 path; the bf16 kernel merges in place): workgroup
-// (item, w) handles the 32 rows of wave block w of the item's query tile;
-// items computed whole are skipped.
-template <int D, bool PAGED>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-    const int item = blockIdx.x, w = blockIdx.y;
-    const int li = item / a.n_qtiles, qt = item - li * a.n_qtiles;
-    const WorkList wl = work_list<PAGED>(a);
-    const Schedule sc = make_schedule(a, wl);
-    const int T = __builtin_amdgcn_readlane(wl.T, li);
-    const int64_t P = entry_base(wl, li) + (int64_t)qt * T;
-    if (sc.owner(P) == sc.owner(P + T - 1)) return;
-    merge_rows<D, false, 256>(a, sc, li, qt, P, T, w, threadIdx.x);
 }
 
 // ------------------------------------------------------------ attention mass
@@ -880,22 +801,6 @@ __global__ __launch_bounds__(256) void attn_mass_finalize_kernel(AttnArgs a) {
 }
 
 }  // namespace
-
-hipError_t launch_attention_merge(const AttnArgs &a, int head_dim, hipStream_t s) {
-    const dim3 grid(a.n_items, BM / 32);
-    if (a.paged) {
-        if (head_dim == 128)
-            hipLaunchKernelGGL((attn_merge_kernel<128, true>), grid, dim3(256), 0, s, a);
-        else
-            hipLaunchKernelGGL((attn_merge_kernel<64, true>), grid, dim3(256), 0, s, a);
-    } else {
-        if (head_dim == 128)
-            hipLaunchKernelGGL((attn_merge_kernel<128, false>), grid, dim3(256), 0, s, a);
-        else
-            hipLaunchKernelGGL((attn_merge_kernel<64, false>), grid, dim3(256), 0, s, a);
-    }
-    return hipGetLastError();
-}
 
 template <bool PAGED>
 hipError_t launch_bf16(const AttnArgs &a, int head_dim, hipStream_t s) {

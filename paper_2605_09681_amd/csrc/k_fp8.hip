@@ -20,7 +20,8 @@
 // softmax is unchanged while the keys keep their variation in 3 mantissa bits.
 //
 // Attention: the bf16 kernel's structure (two ping-ponging 4-wave groups, 32
-// query rows per wave, 64-key tiles, balanced schedule and merge) with
+// query rows per wave, 64-key tiles, balanced schedule, cut items combined by
+// the workgroup whose part arrives last) with
 //   S^T = K Q^T    2 x (d/64) MFMAs 32x32x64 per tile (A = K tile from LDS,
 //                  lane l reads 32 bytes of key row l%32 at dims 64ks + 32(l/32));
 //   P' = 2^(x - m + 6) rounded to E4M3 (x = logit in log2 units, m the running
@@ -37,6 +38,7 @@
 // the contraction index to bytes is valid; this was checked on the hardware.
 // Output: O = O^T * s_v[d] / l (bf16), lse = ln2 * (m - 6) + ln l.
 #include "attn_common.h"
+#include "attn_merge.h"
 
 namespace fkv {
 namespace {
@@ -591,19 +593,22 @@ __device__ __forceinline__ void fp8_segment(const AttnArgs &a, uint8_t (&Ks)[2][
     const float inv = 1.f / l_tot;
     const float *sv = sc + SC_SV;
     if (slot) {
-        uint2 *op = (uint2 *)slot;
+        // device-scope stores: the workgroup that combines the item's parts may
+        // run on another XCD, within this launch.  The part's maximum is
+        // m - kPBias, so that l_tot = sum 2^(x - (m - kPBias)) as for bf16 parts.
+        unsigned long long *op = (unsigned long long *)slot;
 #pragma unroll
         for (int mb = 0; mb < C::MB; ++mb)
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const float4 w = *(const float4 *)(sv + 32 * mb + 8 * g + 4 * hl);
-                op[((wave * C::MB + mb) * 4 + g) * 64 + lane] =
-                    pack_bf16x4(o[mb][4 * g] * w.x * inv, o[mb][4 * g + 1] * w.y * inv,
-                                o[mb][4 * g + 2] * w.z * inv, o[mb][4 * g + 3] * w.w * inv);
+                put_shared(op + ((wave * C::MB + mb) * 4 + g) * 64 + lane,
+                           pack_bf16x4(o[mb][4 * g] * w.x * inv, o[mb][4 * g + 1] * w.y * inv,
+                                       o[mb][4 * g + 2] * w.z * inv, o[mb][4 * g + 3] * w.w * inv));
             }
         if (hl == 0) {
-            slot[BM * D / 2 + wave * 32 + l32] = m_run - kPBias;
-            slot[BM * D / 2 + BM + wave * 32 + l32] = l_tot;
+            put_shared(slot + BM * D / 2 + wave * 32 + l32, m_run - kPBias);
+            put_shared(slot + BM * D / 2 + BM + wave * 32 + l32, l_tot);
         }
         return;
     }
@@ -628,6 +633,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fp8_kernel(AttnArgs a) {
     using C = Fp8Cfg<D>;
     __shared__ __attribute__((aligned(16))) uint8_t Ks[2][C::KTILE];
     __shared__ __attribute__((aligned(16))) uint8_t Vs[2][C::VTILE];
+    __shared__ uint32_t flag;
     if (!BAL) {
         const int item = (blockIdx.x & 7) * a.items_per_xcd + (blockIdx.x >> 3);
         if (item >= a.n_items) return;
@@ -673,6 +679,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fp8_kernel(AttnArgs a) {
                                             : a.part + (size_t)(2 * r + (first ? 0 : 1)) * slot_floats<D>();
         const int rot = (int)((ibase - sc.start(sc.owner(ibase))) % T);
         fp8_segment<D>(a, Ks, Vs, h, qt, t0, t1, rot, slot);
+        if (slot) {
+            // the last of the item's parts to arrive combines them
+            const int n_parts = sc.owner(ibase + T - 1) - sc.owner(ibase) + 1;
+            uint32_t *cnt = a.item_counters + (size_t)(ip.li * a.n_qtiles + qt) * kItemCounterStride;
+            if (arrive_last(cnt, (uint32_t)n_parts, &flag))
+                merge_rows<D, 64>(a, sc, ip.li, qt, ibase, T, threadIdx.x >> 6, threadIdx.x & 63);
+        }
         cur = ibase + t1;
         first = false;
     }
@@ -703,8 +716,7 @@ hipError_t launch_attention_fp8(const AttnArgs &a, int head_dim, hipStream_t s) 
             hipLaunchKernelGGL((attn_fp8_kernel<128, true>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
         else
             hipLaunchKernelGGL((attn_fp8_kernel<64, true>), dim3(a.n_blocks), dim3(kThreads), 0, s, a);
-        const hipError_t e = hipGetLastError();
-        return e != hipSuccess ? e : launch_attention_merge(a, head_dim, s);
+        return hipGetLastError();
     }
     const unsigned blocks = (unsigned)a.items_per_xcd * 8u;
     if (head_dim == 128)
