@@ -630,12 +630,42 @@ def measure_extras(args, cfg, slots, bufs, layers, stream, which):
         fp8_ms = _time_ms(lambda: L0.attention_fp8_packed(O8), 20, stream)
         kv_len = L0.kv_len.cpu().numpy().astype(np.int64)
         attn_flop = attention_flop(cfg, kv_len)
+        # the FP8 step with nothing compacted (scores + kept segments, packing
+        # read in place from the cache, FP8 attention) against the bf16 default
+        # step, both over the rotated buffer copies
+        outs8 = [torch.empty_like(bb["Q"]) for bb in bufs]
+
+        def step8(i):
+            L, bb = layers[i % len(layers)], bufs[i % len(layers)]
+            L.step_fp8(bb["K_hist"], bb["V_hist"], slots, bb["Q"], bb["K_cur"], bb["V_cur"], outs8[i % len(layers)])
+
+        def step16(i):
+            L, bb = layers[i % len(layers)], bufs[i % len(layers)]
+            L.step(bb["K_hist"], bb["V_hist"], slots, bb["Q"], bb["K_cur"], bb["V_cur"], bb["O"])
+
+        ctr = [0]
+
+        def nxt(fn):
+            def f():
+                fn(ctr[0])
+                ctr[0] += 1
+            return f
+        steps = {}
+        for name, fn in (("fp8", step8), ("bf16", step16), ("fp8_again", step8), ("bf16_again", step16)):
+            steps[name] = _time_ms(nxt(fn), 50, stream)
+        fp8_step = (steps["fp8"] + steps["fp8_again"]) / 2
+        bf16_step = (steps["bf16"] + steps["bf16_again"]) / 2
         out["fp8_attention"] = {
             "attention_ms": round(fp8_ms, 4), "TFLOP_s": round(attn_flop / (fp8_ms * 1e-3) / 1e12, 1),
             "peak_TFLOP_s": PEAK_FP8_TFLOPS,
             "frac_of_fp8_peak": round(attn_flop / (fp8_ms * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 4),
             "pack_ms": round(pack_ms, 4), "pack_plus_attention_ms": round(pack_ms + fp8_ms, 4),
-            "note": "E4M3 Q/K/V/P on gfx950 FP8 MFMA; pack = statistics + quantise + transpose"}
+            "step_fp8_in_place_ms": round(fp8_step, 4), "step_bf16_in_place_ms": round(bf16_step, 4),
+            "step_speedup_fp8": round(bf16_step / fp8_step, 3),
+            "note": "E4M3 Q/K/V/P on gfx950 FP8 MFMA; pack = statistics + quantise + transpose (over the "
+                    "compacted history); the FP8 step = fkv_score_select + fkv_fp8_pack_paged (history read in "
+                    "place) + fkv_chunk_attention_fp8, against the bf16 step (fkv_score_select + "
+                    "fkv_chunk_attention_paged), alternating, 50 steps each twice"}
 
     if "uncompressed" in which:
         log("extras: uncompressed attention")

@@ -471,6 +471,34 @@ fkv_status fkv_fp8_pack(const fkv_shape *shape, const void *Q, const void *Kc,
                         void *V8T, float *scales, void *workspace,
                         size_t workspace_bytes, void *stream);
 
+/* fkv_fp8_pack_paged: fkv_fp8_pack with every head's retained history read
+ * in place from the slot-permuted cache (App. F with Eq. 2 / Eq. 3): the
+ * history rows of head h are, in order, the kept frames of a static head
+ * (from its budget, as fkv_compress_static gathers them) or the kept
+ * segments of a dynamic head (kept_seg[h] and kv_len[h] as fkv_select or
+ * fkv_score_select write them, as fkv_select_compact gathers them).  The
+ * packed buffers, scales and workspace are byte for byte those of
+ * fkv_compress_static + fkv_select_compact + fkv_fp8_pack over the same
+ * inputs, with no compressed copy made.
+ *   heads      host array [n_heads] (budgets), as for fkv_compress_static
+ *   K_hist, V_hist, frame_slot   the cache and its slot map (frame_slot is host
+ *              data), as for fkv_chunk_attention_paged
+ *   kept_seg   device int32 [n_heads][n_seg], read for dynamic heads
+ *   kv_len     device int32 [n_heads]: read for dynamic heads; the static
+ *              heads' retained lengths are written to it, so that
+ *              fkv_chunk_attention_fp8 can follow (with the same slab)
+ *   slab       packed key rows per head before the chunk (as for
+ *              fkv_fp8_sizes); FKV_ERR_CAPACITY if any head can retain more
+ *              tokens (fkv_kept_tokens_max)
+ * Other arguments, the workspace and errors as for fkv_fp8_pack; bf16 only. */
+fkv_status fkv_fp8_pack_paged(const fkv_shape *shape, const fkv_head *heads,
+                              const void *K_hist, const void *V_hist,
+                              const int32_t *frame_slot, const int32_t *kept_seg,
+                              int32_t *kv_len, const void *Q, const void *K_cur,
+                              const void *V_cur, int32_t slab, void *Q8, void *K8,
+                              void *V8T, float *scales, void *workspace,
+                              size_t workspace_bytes, void *stream);
+
 fkv_status fkv_chunk_attention_fp8(const fkv_shape *shape, const void *Q8,
                                    const void *K8, const void *V8T, int32_t slab,
                                    const int32_t *kv_len, const float *scales,

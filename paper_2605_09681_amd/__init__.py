@@ -17,8 +17,8 @@ Entry points (see ``include/fkv.h`` for the full contract):
 * :func:`fkv_chunk_attention_static` -- the static heads' attention read in
   place from the cache (no compressed copy)
 * :func:`fkv_append_frames`    -- rolling-cache write of a finished chunk
-* :func:`fkv_fp8_pack`, :func:`fkv_chunk_attention_fp8` -- the FP8 variant of
-  the chunk attention (App. F)
+* :func:`fkv_fp8_pack`, :func:`fkv_fp8_pack_paged`, :func:`fkv_chunk_attention_fp8`
+  -- the FP8 variant of the chunk attention (App. F)
 * :func:`fkv_attention_mass`, :func:`fkv_classify_heads` -- offline head
   profiling (Sec. 4.1, Eq. 1)
 * :func:`fkv_score_pooled`, :func:`fkv_select_compact_pooled` -- the
@@ -50,7 +50,7 @@ EXPORTED = ("fkv_num_segments", "fkv_kept_tokens_max", "fkv_compress_static",
             "fkv_score_segments_cached",
             "fkv_attention_workspace_size", "fkv_chunk_attention", "fkv_chunk_attention_heads",
             "fkv_chunk_attention_static", "fkv_chunk_attention_paged",
-            "fkv_fp8_sizes", "fkv_fp8_pack",
+            "fkv_fp8_sizes", "fkv_fp8_pack", "fkv_fp8_pack_paged",
             "fkv_chunk_attention_fp8", "fkv_attention_mass_workspace_size", "fkv_attention_mass",
             "fkv_classify_heads", "fkv_last_error")
 
@@ -138,6 +138,9 @@ def lib():
         L.fkv_fp8_sizes.restype = ctypes.c_int
         L.fkv_fp8_pack.argtypes = [S, P, P, P, I32, P, P, P, P, P, P, P, P, SZ, P]
         L.fkv_fp8_pack.restype = ctypes.c_int
+        L.fkv_fp8_pack_paged.argtypes = [S, Hd, P, P, ctypes.POINTER(I32), P, P, P, P, P, I32, P, P, P, P, P,
+                                         SZ, P]
+        L.fkv_fp8_pack_paged.restype = ctypes.c_int
         L.fkv_chunk_attention_fp8.argtypes = [S, P, P, P, I32, P, P, F, P, P, P, SZ, P]
         L.fkv_chunk_attention_fp8.restype = ctypes.c_int
         L.fkv_attention_mass_workspace_size.argtypes = [S, I32, ctypes.POINTER(SZ)]
@@ -576,6 +579,32 @@ def fkv_fp8_pack(shape: fkv_shape, Q, Kc, Vc, kv_len, K_cur, V_cur, Q8, K8, V8T,
         raise ValueError(f"scales holds {scales.numel() * 4} bytes, {sb} expected")
     args += [_check(workspace, "workspace", torch.uint8), workspace.numel(), _stream(stream)]
     _raise(lib().fkv_fp8_pack(ctypes.byref(shape), *args))
+
+
+def fkv_fp8_pack_paged(shape: fkv_shape, heads, K_hist, V_hist, frame_slot, kept_seg, kv_len, Q, K_cur, V_cur,
+                       slab: int, Q8, K8, V8T, scales, workspace, stream=None):
+    """fkv_fp8_pack with every head's retained history read in place from
+    K_hist / V_hist (kept frames of static heads, kept segments of dynamic
+    heads); writes the static heads' kv_len."""
+    dt = _torch_dtype(shape)
+    hist = (shape.n_heads, shape.cap_frames, shape.frame_tokens, shape.head_dim)
+    chunk = (shape.n_heads, _lq(shape), shape.head_dim)
+    n_seg = fkv_num_segments(shape)
+    qb, kvb, sb, wb = fkv_fp8_sizes(shape, slab)
+    args = [_heads(shape, heads), _check(K_hist, "K_hist", dt, hist), _check(V_hist, "V_hist", dt, hist),
+            _slots(frame_slot, shape.hist_frames),
+            None if kept_seg is None else _check(kept_seg, "kept_seg", torch.int32, (shape.n_heads, n_seg)),
+            _check(kv_len, "kv_len", torch.int32, (shape.n_heads,)), _check(Q, "Q", dt, chunk),
+            _check(K_cur, "K_cur", dt, chunk), _check(V_cur, "V_cur", dt, chunk), int(slab)]
+    for t, name, nb in ((Q8, "Q8", qb), (K8, "K8", kvb), (V8T, "V8T", kvb)):
+        args.append(_check(t, name, torch.uint8))
+        if t.numel() != nb:
+            raise ValueError(f"{name} holds {t.numel()} bytes, {nb} expected")
+    args.append(_check(scales, "scales", torch.float32))
+    if scales.numel() * 4 != sb:
+        raise ValueError(f"scales holds {scales.numel() * 4} bytes, {sb} expected")
+    args += [_check(workspace, "workspace", torch.uint8), workspace.numel(), _stream(stream)]
+    _raise(lib().fkv_fp8_pack_paged(ctypes.byref(shape), *args))
 
 
 def fkv_chunk_attention_fp8(shape: fkv_shape, Q8, K8, V8T, slab: int, kv_len, scales, scale: float, O,

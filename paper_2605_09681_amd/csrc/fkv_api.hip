@@ -1063,6 +1063,89 @@ fkv_status fkv_fp8_pack(const fkv_shape *shape, const void *Q, const void *Kc, c
     return device_status(fkv::launch_fp8_pack(a, (hipStream_t)stream), "fkv_fp8_pack launch");
 }
 
+fkv_status fkv_fp8_pack_paged(const fkv_shape *shape, const fkv_head *heads, const void *K_hist,
+                              const void *V_hist, const int32_t *frame_slot, const int32_t *kept_seg,
+                              int32_t *kv_len, const void *Q, const void *K_cur, const void *V_cur, int32_t slab,
+                              void *Q8, void *K8, void *V8T, float *scales, void *workspace,
+                              size_t workspace_bytes, void *stream) {
+    fkv_status st;
+    if ((st = check_shape(shape)) != FKV_OK) return st;
+    if ((st = check_heads(shape, heads)) != FKV_OK) return st;
+    size_t qb, kvb, sb, wb;
+    if ((st = fkv_fp8_sizes(shape, slab, &qb, &kvb, &sb, &wb)) != FKV_OK) return st;
+    if (!Q || !K_cur || !V_cur || !kv_len || !Q8 || !K8 || !V8T || !scales)
+        return fail(FKV_ERR_ARG, "NULL tensor pointer");
+    const int H = shape->hist_frames;
+    bool any_dynamic = false;
+    for (int h = 0; h < shape->n_heads; ++h) any_dynamic |= heads[h].type == FKV_DYNAMIC;
+    if (H > 0 && (!K_hist || !V_hist)) return fail(FKV_ERR_ARG, "NULL K_hist/V_hist");
+    if (H > 0 && any_dynamic && !kept_seg) return fail(FKV_ERR_ARG, "kept_seg is NULL");
+    if ((st = check_slots(shape, frame_slot)) != FKV_OK) return st;
+    for (int h = 0; h < shape->n_heads; ++h) {
+        int64_t kept = 0;
+        if ((st = fkv_kept_tokens_max(shape, heads, h, &kept)) != FKV_OK) return st;
+        if (kept > slab)
+            return fail(FKV_ERR_CAPACITY, "slab %d below head %d's %lld retained tokens", slab, h, (long long)kept);
+    }
+    if (!workspace) return fail(FKV_ERR_ARG, "workspace is NULL");
+    if (workspace_bytes < wb)
+        return fail(FKV_ERR_CAPACITY, "workspace of %zu bytes, %zu needed", workspace_bytes, wb);
+    fkv::Fp8PackArgs a;
+    memset(&a, 0, sizeof a);
+    a.Q = (const uint16_t *)Q;
+    a.Kc = a.K_cur = (const uint16_t *)K_cur;
+    a.Vc = a.V_cur = (const uint16_t *)V_cur;
+    a.kv_len = kv_len;
+    a.slab = slab;
+    a.n_heads = shape->n_heads;
+    a.Lq = shape->chunk_frames * shape->frame_tokens;
+    a.d = shape->head_dim;
+    a.rows = ((int64_t)slab + a.Lq + 63) / 64 * 64;
+    a.Q8 = (uint8_t *)Q8;
+    a.K8 = (uint8_t *)K8;
+    a.V8T = (uint8_t *)V8T;
+    a.scales = scales;
+    a.ws = (double *)workspace;
+    a.chunk_rows = fkv::kFp8ChunkRows;
+    a.n_kchunks = (int)(((int64_t)slab + a.Lq + fkv::kFp8ChunkRows - 1) / fkv::kFp8ChunkRows);
+    a.n_qchunks = (a.Lq + fkv::kFp8ChunkRows - 1) / fkv::kFp8ChunkRows;
+    a.paged = 1;
+    a.K_hist = (const uint16_t *)(H > 0 ? K_hist : K_cur);
+    a.V_hist = (const uint16_t *)(H > 0 ? V_hist : V_cur);
+    a.F = shape->frame_tokens;
+    a.L = shape->seg_tokens;
+    a.H = H;
+    a.cap = shape->cap_frames;
+    a.n_seg = fkv_num_segments(shape);
+    auto magic = [](int P, uint32_t *hi, uint32_t *lo) {   // floor(2^64 / P) + 1; P = 1 as 0, 0
+        if (P == 1) {
+            *hi = *lo = 0;
+            return;
+        }
+        const unsigned __int128 m = (((unsigned __int128)1) << 64) / (uint64_t)P + 1;
+        *hi = (uint32_t)(uint64_t)(m >> 32);
+        *lo = (uint32_t)(uint64_t)m;
+    };
+    magic(a.F, &a.mf_hi, &a.mf_lo);
+    magic(a.L, &a.ml_hi, &a.ml_lo);
+    a.kept_seg = kept_seg;
+    a.kv_out = kv_len;
+    for (int h = 0; h < shape->n_heads; ++h) {
+        if (heads[h].type == FKV_DYNAMIC && H > 0) {
+            a.st_kept[h] = -1;
+            continue;
+        }
+        // static heads, and dynamic heads with nothing cached
+        const StaticPlan p = heads[h].type == FKV_DYNAMIC ? StaticPlan{0, 0, 0} : static_plan(H, heads[h]);
+        a.st_first[h] = p.n_first;
+        a.st_gap[h] = p.gap;
+        a.st_kept[h] = p.n_kept;
+    }
+    for (int t = 0; t < H; ++t) a.slots.slot[t] = frame_slot[t];
+    (void)hipGetLastError();
+    return device_status(fkv::launch_fp8_pack(a, (hipStream_t)stream), "fkv_fp8_pack_paged launch");
+}
+
 fkv_status fkv_chunk_attention_fp8(const fkv_shape *shape, const void *Q8, const void *K8, const void *V8T,
                                    int32_t slab, const int32_t *kv_len, const float *scales, float scale,
                                    void *O, float *lse, void *workspace, size_t workspace_bytes,

@@ -174,6 +174,20 @@ struct Fp8PackArgs {
     float *scales;                  // [n_heads][fp8_scale_floats(d)]
     double *ws;                     // statistics partials
     int32_t n_kchunks, n_qchunks, chunk_rows;
+    // Read in place (fkv_fp8_pack_paged): the history rows of head h are its
+    // kept frames (static, st_kept[h] >= 0: kept frame y is logical frame y
+    // (y < st_first[h]) or y + st_gap[h]) or its kept segments (dynamic: the
+    // ids in kept_seg[h], kv_len[h] tokens), read from K_hist / V_hist
+    // [n_heads][cap][F][d] through the slot map; the static heads' lengths
+    // are written to kv_out.
+    int32_t paged;
+    const uint16_t *K_hist, *V_hist;
+    int32_t F, L, H, cap, n_seg;
+    uint32_t mf_hi, mf_lo, ml_hi, ml_lo;   // floor(2^64 / F) + 1 and floor(2^64 / L) + 1
+    const int32_t *kept_seg;        // [n_heads][n_seg]
+    int32_t *kv_out;                // [n_heads]: static heads' kv_len
+    int32_t st_first[FKV_MAX_HEADS], st_gap[FKV_MAX_HEADS], st_kept[FKV_MAX_HEADS];
+    SlotTable slots;
 };
 
 constexpr int kScoreThreads = 256;

@@ -18,6 +18,10 @@
 //                expects (below); rows past the head's keys are zero.
 // Subtracting mu shifts every logit of a query row by the same q . mu, so the
 // softmax is unchanged while the keys keep their variation in 3 mantissa bits.
+// The history rows come from the compressed copy [Kc[0:kv_len]], or
+// (fkv_fp8_pack_paged) straight from the slot-permuted cache: each history row
+// is looked up in its head's kept frames or kept segments, in the order the
+// compressed copy would hold them, so both give the same bytes.
 //
 // Attention: the bf16 kernel's structure (two ping-ponging 4-wave groups, 32
 // query rows per wave, 64-key tiles, balanced schedule, cut items combined by
@@ -75,6 +79,58 @@ __device__ __forceinline__ int pk_fp8(float a, float b, int old) {
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// j / P for 0 <= j < 2^31 with M = floor(2^64 / P) + 1 = hi * 2^32 + lo:
+// floor(j * M / 2^64) exactly (j * M / 2^64 exceeds j / P by less than 2^-33).
+// P = 1 (M does not fit in 64 bits) is passed as hi = lo = 0.
+__device__ __forceinline__ int div_magic(int j, uint32_t hi, uint32_t lo) {
+    if (hi == 0 && lo == 0) return j;
+    return (int)(((uint64_t)(uint32_t)j * hi + __umulhi((uint32_t)j, lo)) >> 32);
+}
+
+// History length of head h: kv_len clamped to the packed rows, or, read in
+// place, the static head's kept frames times F.
+__device__ __forceinline__ int pack_kvl(const Fp8PackArgs &a, int h) {
+    if (a.paged && a.st_kept[h] >= 0) return a.st_kept[h] * a.F;
+    int kvl = a.kv_len[h];
+    const int64_t cap = a.paged ? (a.slab < (int64_t)a.H * a.F ? a.slab : (int64_t)a.H * a.F) : a.slab;
+    return kvl < 0 ? 0 : (kvl > cap ? (int)cap : kvl);
+}
+
+// Element offset of key/value row r of head h (r < kvl: history, else the
+// chunk's row r - kvl) and whether it is a history row.  In place, history row
+// r is row r mod F of kept frame r / F (static) or row r mod L of kept segment
+// r / L (dynamic; a segment of several frames spans their rows in order), at
+// its slot of the cache; slots: the slot map in LDS.
+template <int D>
+__device__ __forceinline__ size_t pack_row(const Fp8PackArgs &a, int h, int r, int kvl, const int *slots,
+                                           bool *hist) {
+    *hist = r < kvl;
+    if (!*hist) return ((size_t)h * a.Lq + (r - kvl)) * D;
+    if (!a.paged) return ((size_t)h * a.slab + r) * D;
+    int t, off;
+    if (a.st_kept[h] >= 0) {
+        const int y = div_magic(r, a.mf_hi, a.mf_lo);
+        off = r - y * a.F;
+        t = y < a.st_first[h] ? y : y + a.st_gap[h];
+    } else {
+        const int q = div_magic(r, a.ml_hi, a.ml_lo);
+        const int o = r - q * a.L;
+        // a kept_seg row that disagrees with kv_len must not address outside
+        // the head's cache: clamp the segment id and the frame
+        const int g = min(max(a.kept_seg[(size_t)h * a.n_seg + q], 0), a.n_seg - 1);
+        if (a.L <= a.F) {
+            const int spf = a.F / a.L;
+            t = g / spf;
+            off = (g - t * spf) * a.L + o;
+        } else {
+            const int f = div_magic(o, a.mf_hi, a.mf_lo);
+            t = min(g * (a.L / a.F) + f, a.H - 1);
+            off = o - f * a.F;
+        }
+    }
+    return ((size_t)h * a.cap * a.F + (size_t)slots[t] * a.F + off) * D;
+}
+
 // grid (n_kchunks + n_qchunks, n_heads); thread = (row group, 8-channel group),
 // four rows in flight per thread.  Partials ws[((h * chunks + x) * d + c) * 4 +
 // {sum K, max K, min K, max |V|}]; Q chunks store max |Q| in slot 3.
@@ -85,11 +141,16 @@ __global__ __launch_bounds__(256) void fp8_stats_kernel(Fp8PackArgs a) {
     constexpr int U = 4;               // rows in flight per thread
     __shared__ double red_s[RG][D];
     __shared__ float red_mx[RG][D], red_mn[RG][D], red_v[RG][D];
+    __shared__ int slots[FKV_MAX_FRAMES];
     const int x = blockIdx.x, h = blockIdx.y;
     const int tid = threadIdx.x, cg = tid % CG, rg = tid / CG;
     const int chunks = a.n_kchunks + a.n_qchunks;
-    int kvl = a.kv_len[h];
-    kvl = kvl < 0 ? 0 : (kvl > a.slab ? (int)a.slab : kvl);
+    const int kvl = pack_kvl(a, h);
+    if (a.paged) {
+        for (int t = tid; t < a.H; t += 256) slots[t] = a.slots.slot[t];
+        if (x == 0 && tid == 0 && a.st_kept[h] >= 0) a.kv_out[h] = kvl;
+        __syncthreads();
+    }
     double sum[8];
     float mx[8], mn[8], vm[8];
 #pragma unroll
@@ -111,10 +172,10 @@ __global__ __launch_bounds__(256) void fp8_stats_kernel(Fp8PackArgs a) {
             vv[u] = u32x4{0, 0, 0, 0};
             if (r < r1) {
                 if (keys) {
-                    const bool hist = r < kvl;
-                    const size_t off = hist ? ((size_t)h * a.slab + r) * D : ((size_t)h * a.Lq + (r - kvl)) * D;
-                    kv[u] = *(const u32x4 *)((hist ? a.Kc : a.K_cur) + off + 8 * cg);
-                    vv[u] = *(const u32x4 *)((hist ? a.Vc : a.V_cur) + off + 8 * cg);
+                    bool hist;
+                    const size_t off = pack_row<D>(a, h, r, kvl, slots, &hist);
+                    kv[u] = *(const u32x4 *)((hist ? (a.paged ? a.K_hist : a.Kc) : a.K_cur) + off + 8 * cg);
+                    vv[u] = *(const u32x4 *)((hist ? (a.paged ? a.V_hist : a.Vc) : a.V_cur) + off + 8 * cg);
                 } else {
                     vv[u] = *(const u32x4 *)(a.Q + ((size_t)h * a.Lq + r) * D + 8 * cg);
                 }
@@ -176,8 +237,7 @@ __global__ __launch_bounds__(1024) void fp8_finalize_kernel(Fp8PackArgs a) {
     __shared__ float red_k[D], red_qq[D];
     const int h = blockIdx.x, c = threadIdx.x % D, sl = threadIdx.x / D;
     const int chunks = a.n_kchunks + a.n_qchunks;
-    int kvl = a.kv_len[h];
-    kvl = kvl < 0 ? 0 : (kvl > a.slab ? (int)a.slab : kvl);
+    const int kvl = pack_kvl(a, h);
     const double *p = a.ws + ((size_t)h * chunks * D + c) * 4;
     double s = 0.0;
     float M = -__builtin_inff(), m = __builtin_inff(), v = 0.f, q = 0.f;
@@ -308,10 +368,14 @@ __global__ __launch_bounds__(256) void fp8_pack_kernel(Fp8PackArgs a, int n_ktil
         }
         return;
     }
-    int kvl = a.kv_len[h];
-    kvl = kvl < 0 ? 0 : (kvl > a.slab ? (int)a.slab : kvl);
+    __shared__ int slots[FKV_MAX_FRAMES];
+    const int kvl = pack_kvl(a, h);
     const int Lk = kvl + a.Lq;
     if (t * BN >= Lk) return;  // never read by the attention kernel
+    if (a.paged) {
+        for (int i = tid; i < a.H; i += 256) slots[i] = a.slots.slot[i];
+        __syncthreads();
+    }
     if (tid >= (BN / 4) * CG) return;
     const int kq = tid % (BN / 4), cg = tid / (BN / 4);
     const float *mu = sc + SC_SV + 2 * D + 8 * cg;
@@ -324,10 +388,10 @@ __global__ __launch_bounds__(256) void fp8_pack_kernel(Fp8PackArgs a, int n_ktil
         kw[e] = u32x4{0, 0, 0, 0};
         vw[e] = u32x4{0, 0, 0, 0};
         if (r < Lk) {
-            const bool hist = r < kvl;
-            const size_t off = hist ? ((size_t)h * a.slab + r) * D : ((size_t)h * a.Lq + (r - kvl)) * D;
-            kw[e] = *(const u32x4 *)((hist ? a.Kc : a.K_cur) + off + 8 * cg);
-            vw[e] = *(const u32x4 *)((hist ? a.Vc : a.V_cur) + off + 8 * cg);
+            bool hist;
+            const size_t off = pack_row<D>(a, h, r, kvl, slots, &hist);
+            kw[e] = *(const u32x4 *)((hist ? (a.paged ? a.K_hist : a.Kc) : a.K_cur) + off + 8 * cg);
+            vw[e] = *(const u32x4 *)((hist ? (a.paged ? a.V_hist : a.Vc) : a.V_cur) + off + 8 * cg);
         }
     }
     uint2 vq[4];

@@ -37,7 +37,7 @@ from . import (FKV_DYNAMIC, FKV_STATIC, fkv_append_frames, fkv_attention_mass,
                fkv_attention_workspace_size, fkv_chunk_attention, fkv_chunk_attention_heads,
                fkv_chunk_attention_paged, fkv_chunk_attention_static, fkv_classify_heads, fkv_score_select,
                fkv_select,
-               fkv_chunk_attention_fp8, fkv_compress_static, fkv_fp8_pack, fkv_fp8_sizes,
+               fkv_chunk_attention_fp8, fkv_compress_static, fkv_fp8_pack, fkv_fp8_pack_paged, fkv_fp8_sizes,
                fkv_num_segments, fkv_score_pooled, fkv_score_pooled_workspace_size,
                fkv_score_history, fkv_score_segments, fkv_score_segments_cached,
                fkv_score_stats_size, fkv_score_workspace_size, fkv_select_compact,
@@ -158,6 +158,23 @@ class CompressedLayer:
     def attention_fp8(self, Q, K_cur, V_cur, O, lse=None, scale: Optional[float] = None):
         """FP8 variant of :meth:`attention`: pack, then the FP8 kernel."""
         self.pack_fp8(Q, K_cur, V_cur)
+        self.attention_fp8_packed(O, lse, scale)
+
+    def pack_fp8_paged(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur):
+        """FP8 packing with every head's retained history read in place from
+        the cache (the dynamic heads' kept segments as the selection left them
+        in kept_seg / kv_len); writes the static heads' kv_len."""
+        b = self.fp8_buffers()
+        fkv_fp8_pack_paged(self.shape, self.heads, K_hist, V_hist, frame_slot, self.kept_seg, self.kv_len, Q,
+                           K_cur, V_cur, self.slab, b["Q8"], b["K8"], b["V8T"], b["scales"], b["ws"])
+
+    def step_fp8(self, K_hist, V_hist, frame_slot, Q, K_cur, V_cur, O, lse=None, scale: Optional[float] = None):
+        """One AR step with the FP8 attention and no compressed copy: scores
+        and kept segments of the dynamic heads (one launch), FP8 packing read
+        in place from the cache, then the FP8 attention."""
+        if self.has_dynamic:
+            self.score_select(K_hist, frame_slot, K_cur)
+        self.pack_fp8_paged(K_hist, V_hist, frame_slot, Q, K_cur, V_cur)
         self.attention_fp8_packed(O, lse, scale)
 
     # whole step --------------------------------------------------------------

@@ -2,7 +2,8 @@
 
 * Packing (fkv_fp8_pack) is byte-exact against the oracle's quantisation
   (oracle/fp8.py): E4M3 codes of Q, K - mu and V, the key order of the packed
-  V^T tiles, and every scale bit.
+  V^T tiles, and every scale bit.  Packing read in place from the cache
+  (fkv_fp8_pack_paged) writes the same bytes as the compacting path.
 * The FP8 kernel's only rounding beyond the packed inputs is that of the
   probabilities (E4M3: relative error within +-2^-4 for normal values,
   absolute within +-2^-10 below 2^-6, in the kernel's scaling 2^6 exp(z - max)).  Against exact attention
@@ -181,3 +182,71 @@ def test_fp8_zero_queries():
     layer, O, lse = run_fp8(cfg, x)
     ref, hq = check_pack(cfg, x, layer)
     check_attention(cfg, ref, hq, O, lse, np.arange(cfg.lq, dtype=np.int32))
+
+
+def _packed(layer, cfg, n_keys):
+    """Packed bytes of every head up to its last written 64-row tile, the
+    scales and kv_len, as host arrays."""
+    b = layer.fp8_buffers()
+    nh, d, lq = cfg.n_heads, cfg.head_dim, cfg.lq
+    rows = b["K8"].numel() // (nh * d)
+    k8 = from_dev(b["K8"]).reshape(nh, rows, d)
+    vt = from_dev(b["V8T"]).reshape(nh, rows // 64, d, 64)
+    out = [from_dev(b["Q8"]), from_dev(b["scales"]).view(np.uint32)]
+    for h in range(nh):
+        n = -(-int(n_keys[h]) // 64) * 64
+        out += [k8[h, :n], vt[h, :n // 64]]
+    return out
+
+
+@pytest.mark.parametrize("d,L,H", [(128, 25, 7), (128, 100, 7), (64, 300, 7), (128, 100, 0), (128, 300, 2)])
+def test_fp8_pack_paged_equals_compact(d, L, H):
+    """fkv_fp8_pack_paged (every retained history read in place from the
+    slot-permuted cache after fkv_score_select) writes the same bytes as
+    score + select/compact + static gather + fkv_fp8_pack, the same kv_len
+    (static heads' lengths written by the pack), and the FP8 attention over
+    either gives the same output and lse bit for bit."""
+    heads = (W.HeadBudget(W.STATIC, 1, 2), W.HeadBudget(W.DYNAMIC, 1, 0, 2, W.SCOPE_FRAME if L < 100 else W.SCOPE_GLOBAL),
+             W.HeadBudget(W.DYNAMIC, 0, 1, 3, W.SCOPE_GLOBAL), W.HeadBudget(W.STATIC, 2, 0))
+    cfg = W.LayerConfig("paged-pack", 4, d, 100, H, 9, 2, L, "bf16", heads, 0.85)
+    slot = np.array([3, 0, 8, 1, 5, 2, 7][:H], np.int32)
+    _case("fp8-pack-paged", d=d, L=L, H=H)
+    x = W.make_layer_inputs(cfg, seed=70 + d + L + H, frame_slot=slot)
+    a, O_a, lse_a = run_fp8(cfg, x)
+    bl = make_layer(cfg)
+    dv = dev_inputs(x)
+    O_b = torch.empty_like(dv["Q"])
+    lse_b = torch.empty((cfg.n_heads, cfg.lq), dtype=torch.float32, device="cuda")
+    bl.step_fp8(dv["K_hist"], dv["V_hist"], x.frame_slot, dv["Q"], dv["K_cur"], dv["V_cur"], O_b, lse_b)
+    torch.cuda.synchronize()
+    kv_a, kv_b = from_dev(a.kv_len), from_dev(bl.kv_len)
+    np.testing.assert_array_equal(kv_b, kv_a)
+    n_keys = kv_a + cfg.lq
+    for i, (u, v) in enumerate(zip(_packed(bl, cfg, n_keys), _packed(a, cfg, n_keys))):
+        np.testing.assert_array_equal(u, v, err_msg=f"packed block {i}")
+    np.testing.assert_array_equal(from_dev(O_b), from_dev(O_a))
+    np.testing.assert_array_equal(from_dev(lse_b).view(np.uint32), from_dev(lse_a).view(np.uint32))
+    ref, hq = check_pack(cfg, x, bl)
+    check_attention(cfg, ref, hq, O_b, lse_b, np.arange(cfg.lq, dtype=np.int32))
+
+
+def test_fp8_step_480p():
+    """The in-place FP8 step at 480P: packed bytes and output equal to the
+    compacting FP8 path's, and within the FP8 bound of the oracle."""
+    cfg = W.wan_layer_config("480p")
+    _case("fp8-step-480p")
+    x = W.make_layer_inputs(cfg, seed=3)
+    a, O_a, lse_a = run_fp8(cfg, x)
+    bl = make_layer(cfg)
+    dv = dev_inputs(x)
+    O_b = torch.empty_like(dv["Q"])
+    lse_b = torch.empty((cfg.n_heads, cfg.lq), dtype=torch.float32, device="cuda")
+    bl.step_fp8(dv["K_hist"], dv["V_hist"], x.frame_slot, dv["Q"], dv["K_cur"], dv["V_cur"], O_b, lse_b)
+    torch.cuda.synchronize()
+    kv_a = from_dev(a.kv_len)
+    np.testing.assert_array_equal(from_dev(bl.kv_len), kv_a)
+    for i, (u, v) in enumerate(zip(_packed(bl, cfg, kv_a + cfg.lq), _packed(a, cfg, kv_a + cfg.lq))):
+        np.testing.assert_array_equal(u, v, err_msg=f"packed block {i}")
+    np.testing.assert_array_equal(from_dev(O_b), from_dev(O_a))
+    ref, hq = check_pack(cfg, x, bl)
+    check_attention(cfg, ref, hq, O_b, lse_b, sample_rows(cfg.lq, 12, seed=3))
