@@ -86,6 +86,10 @@ def parse():
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 256 MiB device-to-device copy three times (the known-size "
                         "kernel that FETCH_SIZE / WRITE_SIZE are scaled by) and exit")
+    p.add_argument("--read-reference", action="store_true",
+                   help="only time the runtime's own reductions and copy over the bytes the scoring "
+                        "reads at 480P and 1080P (52.7 and 275.7 MB of bf16), as a reference for what "
+                        "one pass over that many bytes reaches, and exit")
     return p.parse_args()
 
 
@@ -99,6 +103,33 @@ def copy_calibration():
         b.copy_(a)
     torch.cuda.synchronize()
     print(json.dumps({"copy_calibration_bytes": n, "launches": 3}), flush=True)
+
+
+def read_reference():
+    """torch's sum (fp32 accumulation) and copy over 52.7 MB and 275.7 MB of
+    bf16 -- the scoring's reads at 480P and 1080P -- rotating enough buffers
+    that each pass misses the 256 MB MALL; HIP events, mean of 50 calls."""
+    import torch
+    out = []
+    for mb, nbuf in ((52.7, 8), (275.7, 3)):
+        n = int(mb * 1e6 / 2)
+        bufs = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(nbuf)]
+        k = [0]
+
+        def nxt():
+            k[0] += 1
+            return bufs[k[0] % nbuf]
+        for name, fn in (("sum_fp32", lambda: torch.sum(nxt(), dtype=torch.float32)),
+                         ("copy", lambda: nxt().clone())):
+            ms = _time_ms(fn, 50, torch.cuda.current_stream(), warm=5)
+            moved = mb * 1e6 * (2 if name == "copy" else 1)
+            out.append({"MB_read": mb, "op": name, "us": round(ms * 1e3, 1),
+                        "GB_s_moved": round(moved / (ms * 1e-3) / 1e9, 1),
+                        "frac_of_hbm_peak": round(moved / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 3)})
+            log(f"read reference {mb} MB {name}: {ms * 1e3:.1f} us")
+        del bufs
+        torch.cuda.empty_cache()
+    print(json.dumps({"read_reference": out}), flush=True)
 
 
 def to_dev(a, dtype):
@@ -410,6 +441,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.read_reference:
+        read_reference()
         return
 
     import numpy as np
