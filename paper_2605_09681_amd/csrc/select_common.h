@@ -108,17 +108,59 @@ __device__ __forceinline__ bool keep_by_rank(const A &a, const Rule &r, const ui
     return rank < kk;
 }
 
+// n_seg <= 64: one wave decides head h's keep set, lane g holding candidate
+// g; a candidate's rank counts the smaller keys of its group, read from the
+// other lanes with v_readlane one candidate at a time (no LDS round trip, no
+// barrier), then a ballot and a masked bit count give the output positions.
+// Same rule and result as the general path below.
+template <class A>
+__device__ __forceinline__ void select_one_wave(const A &a, const Rule &r, int h, const float *s,
+                                                int32_t *kept_seg, int32_t *kv_len, int lane) {
+    const int n = a.n_seg;
+    const int g = lane;
+    const bool valid = g < n;
+    const bool f = valid && is_forced(a, r, g);
+    const uint64_t key = valid && !f ? sort_key(s[g], g) : ~0ull;
+    int lo = 0, hi = n;
+    if (r.scope == FKV_SCOPE_FRAME) {
+        const int spf = a.F / a.L;
+        lo = (g / spf) * spf;
+        hi = lo + spf;
+    }
+    const uint32_t klo = (uint32_t)key, khi = (uint32_t)(key >> 32);
+    int rank = 0;
+    for (int j = 0; j < n; ++j) {
+        const uint64_t kj = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)khi, j) << 32) |
+                            (uint32_t)__builtin_amdgcn_readlane((int)klo, j);
+        rank += (int)((j >= lo) & (j < hi) & (kj < key));
+    }
+    const bool kp = valid && (f || rank < r.k);
+    const uint64_t mask = __ballot(kp);
+    const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+    if (kp) kept_seg[(int64_t)h * n + below] = g;
+    if (valid && g >= __popcll(mask)) kept_seg[(int64_t)h * n + g] = -1;
+    int tokens = kp ? seg_tokens(a, g) : 0;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) tokens += __shfl_xor(tokens, off);
+    if (lane == 0) kv_len[h] = tokens;
+}
+
 // One workgroup decides head h's keep set (rule r) from its scores
 // s[0..n_seg) in LDS and writes kept_seg[h] (ascending, -1 padded) and
-// kv_len[h].  keys (n_seg), forced and keep (n_seg bytes each) are LDS
-// scratch.  Every thread of the workgroup calls it (it contains barriers);
-// nthreads is the workgroup size.
+// kv_len[h]; with at most 64 segments its first wave does it alone
+// (select_one_wave).  keys (n_seg), forced and keep (n_seg bytes each) are
+// LDS scratch.  Every thread of the workgroup calls it (it contains
+// barriers); nthreads is the workgroup size.
 template <class A>
 __device__ __forceinline__ void select_from_lds(const A &a, const Rule &r, int h, const float *s,
                                                 uint64_t *keys, unsigned char *forced, unsigned char *keep,
                                                 int32_t *kept_seg, int32_t *kv_len, int tid,
                                                 int nthreads) {
     const int n = a.n_seg;
+    if (n <= 64) {
+        if (tid < 64) select_one_wave(a, r, h, s, kept_seg, kv_len, tid);
+        return;
+    }
     for (int g = tid; g < n; g += nthreads) {
         const bool f = is_forced(a, r, g);
         forced[g] = f ? 1 : 0;
