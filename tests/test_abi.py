@@ -355,6 +355,34 @@ def test_fp8_sizes_bound_slab(fkv):
     assert L.fkv_fp8_sizes(ctypes.byref(shape), 2**31 - 1, *args) == 1
 
 
+def test_fp8_pack_paged_arg_errors(fkv):
+    """fkv_fp8_pack_paged validates before any device work: bf16 only, a slab
+    holding every head's largest retained history (FKV_ERR_CAPACITY), the
+    cache, kept_seg (with a dynamic head and H > 0), kv_len and the slot map
+    present, the workspace large enough."""
+    L = fkv.lib()
+
+    def call(shape, heads=None, slab=256, kept=FAKE, kv=FAKE, K=FAKE, ws=FAKE, wsb=1 << 30, slots=None):
+        H = shape.hist_frames
+        sl = None if slots == "none" else (ctypes.c_int32 * max(H, 1))(*(range(H) if slots is None else slots))
+        return L.fkv_fp8_pack_paged(ctypes.byref(shape), heads or _heads(fkv), K, FAKE, sl, kept, kv, FAKE, FAKE,
+                                    FAKE, slab, FAKE, FAKE, FAKE, FAKE, ws, wsb, None)
+    assert call(_shape(fkv, dtype="f32")) == 2
+    # head 0 static (sink 1 + recent 1: 2 frames = 128 tokens), head 1 dynamic keeping 2 of 4 frames
+    assert call(_shape(fkv), slab=127) == 3
+    assert "retained" in fkv.fkv_last_error()
+    assert call(_shape(fkv), slab=257) == 1          # above the cache's 4 x 64 tokens (fkv_fp8_sizes)
+    assert call(_shape(fkv), kept=None) == 1
+    assert call(_shape(fkv), kv=None) == 1
+    assert call(_shape(fkv), K=None) == 1
+    assert call(_shape(fkv), slots="none") == 1
+    assert call(_shape(fkv), slots=[0, 1, 2, 4]) == 1   # slot outside the cache
+    assert call(_shape(fkv), ws=None) == 1
+    assert call(_shape(fkv), wsb=16) == 3
+    static_only = fkv.make_heads((W.HeadBudget(W.STATIC, 1, 1), W.HeadBudget(W.STATIC, 0, 2)))
+    assert call(_shape(fkv), heads=static_only, kept=None, wsb=16) == 3   # no dynamic head: kept_seg not needed
+
+
 def test_binding_rejects_wrong_head_count(fkv):
     """The binding checks that the fkv_head array has exactly shape.n_heads
     entries before any C call reads it."""
