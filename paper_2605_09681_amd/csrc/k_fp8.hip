@@ -99,39 +99,78 @@ __device__ __forceinline__ int pack_kvl(const Fp8PackArgs &a, int h) {
     return kvl < 0 ? 0 : (kvl > cap ? (int)cap : kvl);
 }
 
+// Read in place, the history of head h is a sequence of kept pieces of P
+// rows, each contiguous in the cache: kept frames (static, P = F), kept
+// segments (dynamic, L <= F, P = L) or the frames of kept segments (dynamic,
+// L > F, P = F).  History row r is row r mod P of piece r / P.
+struct Pieces {
+    int P;
+    uint32_t hi, lo;  // div_magic constants of P
+};
+// (The choice is made with masks on loaded values: a select between two
+// fields of the argument block compiles to a select of their addresses, which
+// makes the compiler copy the whole block to scratch memory in every thread.)
+__device__ __forceinline__ Pieces pieces_of(const Fp8PackArgs &a, int h) {
+    const uint32_t m = (a.st_kept[h] >= 0 || a.L > a.F) ? ~0u : 0u;  // P = F, else P = L
+    const uint32_t F = (uint32_t)a.F, L = (uint32_t)a.L;
+    return Pieces{(int)((F & m) | (L & ~m)), (a.mf_hi & m) | (a.ml_hi & ~m), (a.mf_lo & m) | (a.ml_lo & ~m)};
+}
+
+// Cache row (slot * F + row within the frame) of the first row of kept piece
+// p of head h.  A kept_seg entry out of range is clamped, so a row that
+// disagrees with kv_len cannot address outside the head's cache.
+__device__ __forceinline__ int piece_row(const Fp8PackArgs &a, int h, int p, const int *slots) {
+    int t, off = 0;
+    if (a.st_kept[h] >= 0) {
+        t = p < a.st_first[h] ? p : p + a.st_gap[h];
+    } else if (a.L <= a.F) {
+        const int g = min(max(a.kept_seg[(size_t)h * a.n_seg + p], 0), a.n_seg - 1);
+        const int spf = a.F / a.L;
+        t = g / spf;
+        off = (g - t * spf) * a.L;
+    } else {
+        const int m = a.L / a.F;
+        const int q = p / m;
+        const int g = min(max(a.kept_seg[(size_t)h * a.n_seg + q], 0), a.n_seg - 1);
+        t = min(g * m + (p - q * m), a.H - 1);
+    }
+    return slots[t] * a.F + off;
+}
+
+// The workgroup's table of piece start rows for its history rows [r0, r1):
+// the slot map is copied to LDS, then entry i (piece p0 + i) is built by all
+// threads at once (one round of kept_seg loads per workgroup instead of one
+// per row).  At most (r1 - r0) / P + 1 <= cap entries.  Every thread calls it
+// (two barriers).
+struct PieceTable {
+    Pieces pc;
+    int p0;
+};
+__device__ __forceinline__ PieceTable build_pieces(const Fp8PackArgs &a, int h, int r0, int r1, int *slots,
+                                                   int *tab, int cap) {
+    for (int t = threadIdx.x; t < a.H; t += blockDim.x) slots[t] = a.slots.slot[t];
+    __syncthreads();
+    PieceTable pt{pieces_of(a, h), 0};
+    if (r0 < r1) {
+        pt.p0 = div_magic(r0, pt.pc.hi, pt.pc.lo);
+        const int np = min(div_magic(r1 - 1, pt.pc.hi, pt.pc.lo) - pt.p0 + 1, cap);
+        for (int i = threadIdx.x; i < np; i += blockDim.x) tab[i] = piece_row(a, h, pt.p0 + i, slots);
+    }
+    __syncthreads();
+    return pt;
+}
+
 // Element offset of key/value row r of head h (r < kvl: history, else the
-// chunk's row r - kvl) and whether it is a history row.  In place, history row
-// r is row r mod F of kept frame r / F (static) or row r mod L of kept segment
-// r / L (dynamic; a segment of several frames spans their rows in order), at
-// its slot of the cache; slots: the slot map in LDS.
+// chunk's row r - kvl) and whether it is a history row; read in place, history
+// rows go through the workgroup's piece table.
 template <int D>
-__device__ __forceinline__ size_t pack_row(const Fp8PackArgs &a, int h, int r, int kvl, const int *slots,
-                                           bool *hist) {
+__device__ __forceinline__ size_t pack_row(const Fp8PackArgs &a, int h, int r, int kvl, const PieceTable &pt,
+                                           const int *tab, bool *hist) {
     *hist = r < kvl;
     if (!*hist) return ((size_t)h * a.Lq + (r - kvl)) * D;
     if (!a.paged) return ((size_t)h * a.slab + r) * D;
-    int t, off;
-    if (a.st_kept[h] >= 0) {
-        const int y = div_magic(r, a.mf_hi, a.mf_lo);
-        off = r - y * a.F;
-        t = y < a.st_first[h] ? y : y + a.st_gap[h];
-    } else {
-        const int q = div_magic(r, a.ml_hi, a.ml_lo);
-        const int o = r - q * a.L;
-        // a kept_seg row that disagrees with kv_len must not address outside
-        // the head's cache: clamp the segment id and the frame
-        const int g = min(max(a.kept_seg[(size_t)h * a.n_seg + q], 0), a.n_seg - 1);
-        if (a.L <= a.F) {
-            const int spf = a.F / a.L;
-            t = g / spf;
-            off = (g - t * spf) * a.L + o;
-        } else {
-            const int f = div_magic(o, a.mf_hi, a.mf_lo);
-            t = min(g * (a.L / a.F) + f, a.H - 1);
-            off = o - f * a.F;
-        }
-    }
-    return ((size_t)h * a.cap * a.F + (size_t)slots[t] * a.F + off) * D;
+    const int p = div_magic(r, pt.pc.hi, pt.pc.lo);
+    return ((size_t)h * a.cap * a.F + tab[p - pt.p0] + (r - p * pt.pc.P)) * D;
 }
 
 // grid (n_kchunks + n_qchunks, n_heads); thread = (row group, 8-channel group),
@@ -144,16 +183,12 @@ __global__ __launch_bounds__(256) void fp8_stats_kernel(Fp8PackArgs a) {
     constexpr int U = 4;               // rows in flight per thread
     __shared__ double red_s[RG][D];
     __shared__ float red_mx[RG][D], red_mn[RG][D], red_v[RG][D];
-    __shared__ int slots[FKV_MAX_FRAMES];
+    __shared__ int slots[FKV_MAX_FRAMES], tab[kFp8ChunkRows + 1];  // read in place
     const int x = blockIdx.x, h = blockIdx.y;
     const int tid = threadIdx.x, cg = tid % CG, rg = tid / CG;
     const int chunks = a.n_kchunks + a.n_qchunks;
     const int kvl = pack_kvl(a, h);
-    if (a.paged) {
-        for (int t = tid; t < a.H; t += 256) slots[t] = a.slots.slot[t];
-        if (x == 0 && tid == 0 && a.st_kept[h] >= 0) a.kv_out[h] = kvl;
-        __syncthreads();
-    }
+    if (a.paged && x == 0 && tid == 0 && a.st_kept[h] >= 0) a.kv_out[h] = kvl;
     double sum[8];
     float mx[8], mn[8], vm[8];
 #pragma unroll
@@ -166,6 +201,9 @@ __global__ __launch_bounds__(256) void fp8_stats_kernel(Fp8PackArgs a) {
     const bool keys = x < a.n_kchunks;
     const int r0 = (keys ? x : x - a.n_kchunks) * a.chunk_rows;
     const int r1 = min(r0 + a.chunk_rows, keys ? kvl + a.Lq : a.Lq);
+    // (chunk_rows is kFp8ChunkRows: at most kFp8ChunkRows + 1 pieces)
+    const PieceTable pt = a.paged && keys ? build_pieces(a, h, r0, min(r1, kvl), slots, tab, kFp8ChunkRows + 1)
+                                          : PieceTable{};
     for (int rb = r0 + rg; rb < r1; rb += U * RG) {
         u32x4 kv[U], vv[U];
 #pragma unroll
@@ -176,7 +214,7 @@ __global__ __launch_bounds__(256) void fp8_stats_kernel(Fp8PackArgs a) {
             if (r < r1) {
                 if (keys) {
                     bool hist;
-                    const size_t off = pack_row<D>(a, h, r, kvl, slots, &hist);
+                    const size_t off = pack_row<D>(a, h, r, kvl, pt, tab, &hist);
                     kv[u] = *(const u32x4 *)((hist ? (a.paged ? a.K_hist : a.Kc) : a.K_cur) + off + 8 * cg);
                     vv[u] = *(const u32x4 *)((hist ? (a.paged ? a.V_hist : a.Vc) : a.V_cur) + off + 8 * cg);
                 } else {
@@ -371,14 +409,11 @@ __global__ __launch_bounds__(256) void fp8_pack_kernel(Fp8PackArgs a, int n_ktil
         }
         return;
     }
-    __shared__ int slots[FKV_MAX_FRAMES];
+    __shared__ int slots[FKV_MAX_FRAMES], tab[BN + 1];  // read in place
     const int kvl = pack_kvl(a, h);
     const int Lk = kvl + a.Lq;
     if (t * BN >= Lk) return;  // never read by the attention kernel
-    if (a.paged) {
-        for (int i = tid; i < a.H; i += 256) slots[i] = a.slots.slot[i];
-        __syncthreads();
-    }
+    const PieceTable pt = a.paged ? build_pieces(a, h, t * BN, min(t * BN + BN, kvl), slots, tab, BN + 1) : PieceTable{};
     if (tid >= (BN / 4) * CG) return;
     const int kq = tid % (BN / 4), cg = tid / (BN / 4);
     const float *mu = sc + SC_SV + 2 * D + 8 * cg;
@@ -392,7 +427,7 @@ __global__ __launch_bounds__(256) void fp8_pack_kernel(Fp8PackArgs a, int n_ktil
         vw[e] = u32x4{0, 0, 0, 0};
         if (r < Lk) {
             bool hist;
-            const size_t off = pack_row<D>(a, h, r, kvl, slots, &hist);
+            const size_t off = pack_row<D>(a, h, r, kvl, pt, tab, &hist);
             kw[e] = *(const u32x4 *)((hist ? (a.paged ? a.K_hist : a.Kc) : a.K_cur) + off + 8 * cg);
             vw[e] = *(const u32x4 *)((hist ? (a.paged ? a.V_hist : a.Vc) : a.V_cur) + off + 8 * cg);
         }
