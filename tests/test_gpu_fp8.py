@@ -199,7 +199,10 @@ def _packed(layer, cfg, n_keys):
     return out
 
 
-@pytest.mark.parametrize("d,L,H", [(128, 25, 7), (128, 100, 7), (64, 300, 7), (128, 100, 0), (128, 300, 2)])
+# L = 4 and L = 1: short pieces, so a statistics workgroup's piece table holds
+# up to 129 and 513 entries and a pack workgroup's up to 17 and 65
+@pytest.mark.parametrize("d,L,H", [(128, 25, 7), (128, 100, 7), (64, 300, 7), (128, 100, 0), (128, 300, 2),
+                                   (128, 4, 7), (64, 1, 3)])
 def test_fp8_pack_paged_equals_compact(d, L, H):
     """fkv_fp8_pack_paged (every retained history read in place from the
     slot-permuted cache after fkv_score_select) writes the same bytes as
